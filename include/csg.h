@@ -1,0 +1,247 @@
+/*
+ * csg.h -- chunk-scheduled GEMM for MI355X (gfx950): the C ABI.
+ *
+ * One persistent GEMM kernel whose tile scheduler follows a communication-chunk
+ * schedule (Syncopate, arXiv 2601.20595, Section 5.2): tiles that consume a
+ * chunk wait for that chunk's ready flag and are visited in chunk-arrival
+ * order; tiles that produce an output chunk signal it when the chunk is
+ * complete. On one GPU the "remote" side of a rank is simulated: remote shards
+ * are staged in HBM and moved by SDMA copy-engine copies (Section 2.3, copy
+ * engine backend; Section 5.2, realization (1): copy engine + global-memory
+ * signals). Copies are issued by the calling thread straight to the SDMA engines;
+ * a call that moves chunks returns once its copies have completed, while its
+ * kernel may still be running on the compute stream.
+ *
+ * Conventions for every entry point
+ *   - Every call returns csg_status; nothing throws or aborts across the ABI.
+ *     A failing call leaves a thread-local message readable by csg_last_error().
+ *   - Pointers named *_host are host memory; every other data pointer is device
+ *     memory of the plan's device, owned by the caller. Streams are hipStream_t
+ *     values passed as void*; they are owned by the caller and must belong to
+ *     the plan's device.
+ *   - Matrices are dense row-major with no padding: A is M x K, B is N x K
+ *     (K contiguous, the local kernel's a . b^T form), C is M x N; grouped
+ *     weights are E x N x K. dtype CSG_BF16 elements are raw bfloat16 bit
+ *     patterns (uint16), CSG_F32 are IEEE binary32.
+ *   - Objects (schedules, plans) are not thread-safe; distinct objects are
+ *     independent.
+ */
+#ifndef CSG_H_
+#define CSG_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    CSG_OK = 0,
+    CSG_ERR_INVALID = 1,      /* bad argument or schedule; nothing was enqueued */
+    CSG_ERR_UNSUPPORTED = 2,  /* valid request this build cannot serve (device, dtype, tile) */
+    CSG_ERR_HIP = 3,          /* a HIP runtime call failed; csg_last_error() has its text */
+    CSG_ERR_NOMEM = 4,        /* host or device allocation failed */
+    CSG_ERR_TIMEOUT = 5,      /* a bounded wait expired (see csg_diag) */
+    CSG_ERR_STATE = 6         /* call not allowed in the object's current state */
+} csg_status;
+
+typedef enum { CSG_BF16 = 0, CSG_F32 = 1 } csg_dtype;
+
+typedef enum {
+    CSG_AG_GEMM = 0,        /* AllGather(A) + GEMM: tiles consume arriving A row chunks */
+    CSG_GEMM_RS = 1,        /* GEMM + ReduceScatter: tiles produce C row chunks that are sent */
+    CSG_GROUPED_GEMM = 2    /* all-to-all(X) + grouped GEMM: per-(source, expert) row segments */
+} csg_op;
+
+typedef enum {
+    CSG_ORDER_RING = 0,         /* local shard, then shards r-1, r-2, ... (ring AllGather) */
+    CSG_ORDER_SWIZZLE1D = 1,    /* local shard, then peers (i + r) mod W, i = 1..W-1 */
+    CSG_ORDER_PERMUTATION = 2,  /* local chunks, then remote chunks in a caller-given order */
+    CSG_ORDER_RS_RING = 3       /* shards (r + 1 + t) mod W, t = 0..W-1 (own shard last) */
+} csg_order;
+
+typedef enum {
+    CSG_MODE_OVERLAP = 0,       /* copies and kernel run concurrently */
+    CSG_MODE_COMPUTE_ONLY = 1,  /* every flag pre-set, no copies; the kernel still polls */
+    CSG_MODE_COPY_ONLY = 2      /* copies only (reduce-scatter: C must already hold the output) */
+} csg_mode;
+
+/* One chunk: the contiguous row range [row_begin, row_end) of A (AG, grouped) or
+ * of C (RS) moved as one unit (Section 5.1, chunk definition). src_rank is the
+ * rank that owns it, group the expert index (grouped GEMM; 0 otherwise),
+ * is_local != 0 when the chunk is already on this rank (never copied). */
+typedef struct {
+    int64_t row_begin;
+    int64_t row_end;
+    int32_t src_rank;
+    int32_t group;
+    int32_t is_local;
+    int32_t reserved;       /* must be 0 */
+} csg_chunk;
+
+/* Tile and runtime knobs. Zero means "default" for every field.
+ *   bm, bn, bk      tile shape; must name a compiled kernel variant on a device plan
+ *   intra_order     0 = raster (m, n) inside a chunk (the local kernel's own traversal)
+ *   tile_dispatch   0 or 1 = workgroups take the next entry of the tile list from an
+ *                   atomic ticket; 2 = workgroup w takes entries w, w + G, w + 2G, ...
+ *   num_workgroups  persistent grid size G (0 = one per co-resident slot)
+ *   copy_engines    SDMA engines the chunk copies are spread over (0 = every engine the
+ *                   device offers for device-to-device copies)
+ *   timeout_ms      bound on every wait (kernel flag polls, host waits); 0 = 2000 */
+typedef struct {
+    int32_t bm, bn, bk;
+    int32_t intra_order;
+    int32_t tile_dispatch;
+    int32_t num_workgroups;
+    int32_t copy_engines;
+    int32_t timeout_ms;
+} csg_plan_cfg;
+
+typedef struct csg_schedule csg_schedule;
+typedef struct csg_plan csg_plan;
+
+typedef struct {
+    int32_t n_tiles;        /* tiles of the output */
+    int32_t n_chunks;
+    int32_t nnz;            /* sum over tiles of the chunks each tile touches */
+    int32_t n_tiles_n;      /* tiles along N */
+    int32_t num_workgroups; /* persistent grid actually used (0 on a host-only plan) */
+    int32_t bm, bn, bk;     /* tile shape actually used */
+} csg_plan_info;
+
+/* Diagnostics of the last call on a plan (filled by csg_plan_check). */
+typedef struct {
+    int32_t timed_out;      /* 1 if a kernel flag wait or a host wait expired */
+    int32_t chunk;          /* chunk id waited on, -1 if none */
+    int32_t tile;           /* raster id of the tile that waited, -1 if none */
+    uint32_t observed;      /* flag value seen when the wait gave up */
+    uint32_t epoch;         /* epoch the wait needed */
+    int32_t reserved;
+} csg_diag;
+
+/* Library version string, static storage. */
+const char* csg_version(void);
+
+/* Human-readable name of a status, static storage. */
+const char* csg_status_str(csg_status s);
+
+/* Message of the last failing call on this thread ("" if none), thread-local storage. */
+const char* csg_last_error(void);
+
+/* Writes the device's architecture name into arch (NUL-terminated, truncated to
+ * arch_len). CSG_OK if it is gfx950, CSG_ERR_UNSUPPORTED otherwise, CSG_ERR_HIP if
+ * the device cannot be queried. */
+csg_status csg_device_check(int device, char* arch, size_t arch_len);
+
+/* ---- schedules (host only; Section 5.1) ---------------------------------------- */
+
+/* General schedule: n chunks (copied) that must tile [0, chunks[n-1].row_end) in
+ * row order, each non-empty, and order[0..n-1] a permutation of 0..n-1 giving the
+ * arrival (AG, grouped) or emission (RS) order. CSG_ERR_INVALID otherwise. */
+csg_status csg_schedule_create(const csg_chunk* chunks, int32_t n, const int32_t* order,
+                               csg_schedule** out);
+
+/* Uniform schedule of one rank (template specialisation, Section 5.1): world
+ * ranks each own shard_rows rows split into chunks_per_shard equal chunks; chunk
+ * c = s*Q + q covers rows [s*S + q*h, s*S + (q+1)*h). For CSG_ORDER_PERMUTATION,
+ * remote_perm_host holds a permutation of 0..(world-1)*Q-1 applied to the
+ * ascending list of remote chunk ids (it is ignored, and may be NULL, for the
+ * other orders). */
+csg_status csg_schedule_uniform(int32_t world, int32_t rank, int64_t shard_rows,
+                                int32_t chunks_per_shard, csg_order order,
+                                const int32_t* remote_perm_host, csg_schedule** out);
+
+/* All-to-all schedule of one rank: counts_host[s * n_groups + e] routed rows come
+ * from source rank s for local expert e. Rows are laid out expert-major, then
+ * source-major; each non-empty (s, e) segment is a chunk of group e; arrival is
+ * the rank's own segments, then sources r-1, r-2, ..., experts ascending. */
+csg_status csg_schedule_grouped(int32_t world, int32_t rank, int32_t n_groups,
+                                const int64_t* counts_host, csg_schedule** out);
+
+/* Number of chunks and rows covered. */
+csg_status csg_schedule_info(const csg_schedule* s, int32_t* n_chunks, int64_t* total_rows);
+
+/* Copies the chunk list and the order out (arrays of n_chunks entries; either may be NULL). */
+csg_status csg_schedule_get(const csg_schedule* s, csg_chunk* chunks_host, int32_t* order_host);
+
+void csg_schedule_destroy(csg_schedule* s);
+
+/* ---- plans ------------------------------------------------------------------ */
+
+/* Builds the chunk-tile dependence map and the chunk-ordered tile list
+ * (Section 5.2: dependency parsing, tile-scheduler swizzling) for
+ * C[M x N] = A[M x K] . B[N x K]^T under schedule s, and, when device >= 0, the
+ * device state one call needs (tile list, wait lists, flags, counters).
+ * device < 0 makes a host-only plan: the map can be read, no GEMM can run.
+ * op CSG_GROUPED_GEMM needs group_rows_host[n_groups] (rows per expert, summing to
+ * M) and chunks that stay inside their group; other ops pass NULL, 0.
+ * The schedule is copied; it may be destroyed afterwards. */
+csg_status csg_plan_create(csg_op op, int64_t M, int64_t N, int64_t K, csg_dtype in_dtype,
+                           csg_dtype out_dtype, const csg_schedule* s,
+                           const int64_t* group_rows_host, int32_t n_groups,
+                           const csg_plan_cfg* cfg, int device, csg_plan** out);
+
+csg_status csg_plan_info_get(const csg_plan* p, csg_plan_info* info);
+
+/* Copies out the map, all host arrays (any may be NULL):
+ *   tile_ptr[n_tiles+1], tile_chunks[nnz]   D(t): ascending chunk ids per raster tile id
+ *   chunk_ptr[n_chunks+1], chunk_tiles[nnz] T(c): ascending raster tile ids per chunk
+ *   tile_order[n_tiles]                     raster ids in execution order, sorted by
+ *                                           (max (consumers) / min (RS) arrival position
+ *                                           of D(t), raster id)
+ * Raster id = global row-tile index * n_tiles_n + n; grouped row tiles are numbered
+ * group by group. */
+csg_status csg_plan_get_map(const csg_plan* p, int32_t* tile_ptr, int32_t* tile_chunks,
+                            int32_t* chunk_ptr, int32_t* chunk_tiles, int32_t* tile_order);
+
+/* Per-remote-chunk release delays in microseconds, in arrival order
+ * (n = number of remote chunks); the chunk at arrival position i of the remote
+ * chunks is not copied before sum_{j<=i} delay_us[j] after the call starts.
+ * NULL clears them. With delays set, copies are issued from the calling thread
+ * at their release times, so the call returns only after the last copy is
+ * issued. */
+csg_status csg_plan_set_copy_delays(csg_plan* p, const float* delay_us_host, int32_t n);
+
+/* AllGather + GEMM on one rank. a_landing is the full M x K A whose local rows are
+ * already in place; a_staging has the same layout and holds the remote rows (the
+ * simulated peers' shards). The prologue and the persistent kernel are queued on
+ * `compute`; then, once the work queued earlier on `copy` and the plan's previous
+ * kernel have completed, the calling thread issues, for each remote chunk in
+ * arrival order, an SDMA copy staging -> landing followed by an SDMA copy that
+ * raises the chunk's flag, and returns when all of them have completed. The
+ * kernel runs tiles in chunk order, each waiting for its chunks. Work queued on
+ * `compute` afterwards is ordered after the kernel. Asynchronous failures (a flag
+ * wait that timed out) surface through csg_plan_check. CSG_ERR_TIMEOUT if a host
+ * wait expired. */
+csg_status csg_ag_gemm(csg_plan* p, void* a_landing, const void* a_staging, const void* b_nk,
+                       void* c, csg_mode mode, void* compute_stream, void* copy_stream);
+
+/* GEMM + ReduceScatter on one rank: the kernel computes C tiles in emission
+ * order; the last tile of an output chunk releases the chunk's flag, and the
+ * calling thread then copies the chunk by SDMA from c to c_outgoing (non-local
+ * chunks only). The call returns when every copy has completed, i.e. shortly
+ * after the kernel has emitted its last non-local chunk. In copy-only mode c must
+ * already hold the output (the plan's previous kernel is waited for). */
+csg_status csg_gemm_rs(csg_plan* p, const void* a, const void* b_nk, void* c, void* c_outgoing,
+                       csg_mode mode, void* compute_stream, void* copy_stream);
+
+/* All-to-all + grouped GEMM on one rank: x_landing / x_staging as in csg_ag_gemm
+ * (expert-major rows), b_enk the E x N x K expert weights; tile rows never cross
+ * an expert boundary. */
+csg_status csg_grouped_gemm(csg_plan* p, void* x_landing, const void* x_staging,
+                            const void* b_enk, void* c, csg_mode mode, void* compute_stream,
+                            void* copy_stream);
+
+/* Waits for the plan's last call to complete and reports its diagnostics.
+ * CSG_ERR_TIMEOUT if a wait expired (details in *out), CSG_OK otherwise. */
+csg_status csg_plan_check(csg_plan* p, csg_diag* out);
+
+/* Waits for the plan's last call, then frees everything the plan owns. */
+void csg_plan_destroy(csg_plan* p);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CSG_H_ */

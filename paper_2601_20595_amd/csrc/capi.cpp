@@ -1,0 +1,745 @@
+// C ABI of the chunk-scheduled GEMM library (declared in include/csg.h) and the
+// host runtime behind it: plan state on the device, the copy-engine driver that
+// moves chunks and raises their flags, and the kernel launches.
+//
+// Copy-engine realization (Section 5.2, realization (1): copy engine with
+// global-memory signals). Every chunk copy goes straight to an SDMA engine through
+// the HSA runtime (sdma.cpp), consecutive chunks on consecutive engines; a chunk's
+// ready flag is raised by a second 4-byte SDMA copy on the same engine that starts
+// once the chunk's copy has completed (HSA signal dependency). Its source is entry
+// `epoch` of a static table holding 0, 1, 2, ..., so the flag copy depends on
+// nothing but the chunk copy. No copy enters a HIP stream: on this platform a
+// stream wait (and the stream write/wait-value operations, which run as kernels)
+// can end up behind the persistent kernel in a shared hardware queue, and a copy
+// behind it could not progress until the kernel that waits for its flag ends.
+//
+// The ordering the copies need is enforced by the calling thread before it issues
+// them (the caller's copy stream has reached the call; the previous call's kernel
+// no longer reads the buffer being rewritten), and a call returns once its copies
+// have completed, so work queued afterwards on any stream sees them. This matches
+// the paper's copy-engine backend, whose transfers are launched from the host
+// (Section 2.3). Reduce-scatter output chunks are copied out by the calling thread
+// as their completion flags (coherent host memory) rise.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <chrono>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <thread>
+#include <vector>
+
+#include "../../include/csg.h"
+#include "kernels.hpp"
+#include "planner.hpp"
+#include "sdma.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+csg_status fail(csg_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+csg_status hip_fail(hipError_t e, const char* what) {
+  return fail(e == hipErrorOutOfMemory ? CSG_ERR_NOMEM : CSG_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define CSG_HIP(expr)                                      \
+  do {                                                     \
+    hipError_t e_ = (expr);                                \
+    if (e_ != hipSuccess) return hip_fail(e_, #expr);      \
+  } while (0)
+
+// Restores the caller's current device on scope exit.
+struct DeviceGuard {
+  int prev = -1;
+  hipError_t err = hipSuccess;
+  explicit DeviceGuard(int dev) {
+    err = hipGetDevice(&prev);
+    if (err == hipSuccess && prev != dev) err = hipSetDevice(dev);
+  }
+  ~DeviceGuard() {
+    if (prev >= 0) (void)hipSetDevice(prev);
+  }
+};
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Epochs run 1 .. kEpochTable - 1; the flag copy of epoch e reads table entry e.
+constexpr uint32_t kEpochTable = 1u << 16;
+
+}  // namespace
+
+struct csg_schedule {
+  csg::Schedule s;
+};
+
+struct csg_plan {
+  csg_op op = CSG_AG_GEMM;
+  int64_t M = 0, N = 0, K = 0;
+  csg_dtype in_dtype = CSG_BF16, out_dtype = CSG_BF16;
+  csg::Schedule sched;
+  std::vector<int64_t> group_rows;
+  csg_plan_cfg cfg{};
+  csg::TileMap map;
+  int device = -1;
+  csg::KernelKey key{};
+  int32_t grid = 0;
+  std::vector<int32_t> remote_order;   // non-local chunk ids in arrival / emission order
+  std::vector<float> delays_us;        // per remote chunk, in remote_order order
+  uint32_t epoch = 0;
+  bool kernel_pending[2] = {false, false};  // a kernel was launched with epoch parity i
+
+  // device state
+  csg::TileDesc* d_tiles = nullptr;
+  int32_t* d_list_ptr = nullptr;
+  int32_t* d_list_ids = nullptr;
+  int32_t* d_raster = nullptr;
+  int32_t* d_need = nullptr;
+  uint32_t* d_flags = nullptr;         // fine-grained device memory: [n_chunks] ready flags
+  uint32_t* d_epoch_table = nullptr;   // [kEpochTable], entry i == i: source of the flag copies
+  uint32_t* d_counters = nullptr;
+  uint32_t* d_ticket = nullptr;
+  csg::DeviceDiag* d_diag = nullptr;
+  uint32_t* h_out_flags = nullptr;     // coherent host memory (reduce-scatter completion flags)
+  uint32_t* h_out_flags_dev = nullptr; // its device address
+  uint32_t* d_scratch = nullptr;       // target of the engines' warm-up copies
+  csg::SdmaEngines sdma;
+  std::vector<hsa_signal_t> sig_data;  // per remote chunk position: chunk copy done
+  std::vector<hsa_signal_t> sig_flag;  // per remote chunk position: flag copy done
+  bool copies_in_flight = false;       // a call returned before its copies completed (error path)
+  hipEvent_t ev_copy_in = nullptr;     // the caller's copy stream reached the call
+  hipEvent_t ev_prologue = nullptr;    // the prologue finished (waited for on an epoch wrap)
+  hipEvent_t ev_kernel_done[2] = {nullptr, nullptr};  // by epoch parity
+  hipStream_t aux = nullptr;           // plan-internal transfers (diagnostics)
+  csg_diag host_diag{};                // host-side wait failures of the last call
+
+  int32_t n_chunks() const { return static_cast<int32_t>(sched.chunks.size()); }
+  bool consumer() const { return op != CSG_GEMM_RS; }
+};
+
+namespace {
+
+void free_plan_device(csg_plan* p) {
+  if (p->device < 0) return;
+  DeviceGuard g(p->device);
+  for (size_t i = 0; i < p->sig_flag.size(); ++i) {
+    if (p->copies_in_flight) {
+      (void)csg::sdma_wait(p->sig_data[i], 0, 10000);
+      (void)csg::sdma_wait(p->sig_flag[i], 0, 10000);
+    }
+  }
+  for (hsa_signal_t sgn : p->sig_data)
+    if (sgn.handle) hsa_signal_destroy(sgn);
+  for (hsa_signal_t sgn : p->sig_flag)
+    if (sgn.handle) hsa_signal_destroy(sgn);
+  p->sdma.close();
+  for (hipEvent_t e : p->ev_kernel_done)
+    if (e) (void)hipEventSynchronize(e);
+  for (void* ptr : {static_cast<void*>(p->d_tiles), static_cast<void*>(p->d_list_ptr),
+                    static_cast<void*>(p->d_list_ids), static_cast<void*>(p->d_raster), static_cast<void*>(p->d_need),
+                    static_cast<void*>(p->d_flags), static_cast<void*>(p->d_epoch_table),
+                    static_cast<void*>(p->d_counters), static_cast<void*>(p->d_ticket), static_cast<void*>(p->d_diag),
+                    static_cast<void*>(p->d_scratch)})
+    if (ptr) (void)hipFree(ptr);
+  if (p->h_out_flags) (void)hipHostFree(p->h_out_flags);
+  for (hipEvent_t e : {p->ev_copy_in, p->ev_prologue, p->ev_kernel_done[0], p->ev_kernel_done[1]})
+    if (e) (void)hipEventDestroy(e);
+  if (p->aux) (void)hipStreamDestroy(p->aux);
+}
+
+template <class T>
+csg_status upload(T** dst, const std::vector<T>& src) {
+  const size_t bytes = std::max<size_t>(src.size(), 1) * sizeof(T);
+  CSG_HIP(hipMalloc(reinterpret_cast<void**>(dst), bytes));
+  if (!src.empty()) CSG_HIP(hipMemcpy(*dst, src.data(), src.size() * sizeof(T), hipMemcpyHostToDevice));
+  return CSG_OK;
+}
+
+csg_status setup_device(csg_plan* p) {
+  DeviceGuard g(p->device);
+  if (g.err != hipSuccess) return hip_fail(g.err, "hipSetDevice");
+  const csg::TileMap& m = p->map;
+  const int32_t n_tiles = m.n_tiles();
+  const int32_t nN = m.n_tiles_n;
+  std::vector<csg::TileDesc> tiles(n_tiles);
+  std::vector<int32_t> lptr(n_tiles + 1, 0), lids, raster(n_tiles);
+  for (int32_t i = 0; i < n_tiles; ++i) {
+    const int32_t t = m.order[i];
+    const csg::RowTile& rt = m.row_tiles[t / nN];
+    tiles[i] = {static_cast<int32_t>(rt.row_begin), static_cast<int32_t>(rt.row_end), t % nN, rt.group};
+    raster[i] = t;
+    for (int32_t q = m.tile_ptr[t]; q < m.tile_ptr[t + 1]; ++q) {
+      const int32_t c = m.tile_chunks[q];
+      // consumers wait only for chunks that have to arrive; producers signal every chunk
+      if (!p->consumer() || !p->sched.chunks[c].is_local) lids.push_back(c);
+    }
+    lptr[i + 1] = static_cast<int32_t>(lids.size());
+  }
+  std::vector<int32_t> need(p->n_chunks());
+  for (int32_t c = 0; c < p->n_chunks(); ++c) need[c] = m.chunk_ptr[c + 1] - m.chunk_ptr[c];
+  std::vector<uint32_t> table(kEpochTable);
+  for (uint32_t i = 0; i < kEpochTable; ++i) table[i] = i;
+  csg_status st;
+  if ((st = upload(&p->d_tiles, tiles)) != CSG_OK) return st;
+  if ((st = upload(&p->d_list_ptr, lptr)) != CSG_OK) return st;
+  if ((st = upload(&p->d_list_ids, lids)) != CSG_OK) return st;
+  if ((st = upload(&p->d_raster, raster)) != CSG_OK) return st;
+  if ((st = upload(&p->d_need, need)) != CSG_OK) return st;
+  if ((st = upload(&p->d_epoch_table, table)) != CSG_OK) return st;
+  const size_t nflag = static_cast<size_t>(std::max(p->n_chunks(), 1));
+  CSG_HIP(hipExtMallocWithFlags(reinterpret_cast<void**>(&p->d_flags), nflag * 4, hipDeviceMallocFinegrained));
+  CSG_HIP(hipMemset(p->d_flags, 0, nflag * 4));
+  CSG_HIP(hipMalloc(&p->d_counters, nflag * 4));
+  CSG_HIP(hipMemset(p->d_counters, 0, nflag * 4));
+  CSG_HIP(hipMalloc(&p->d_ticket, 4));
+  CSG_HIP(hipMalloc(&p->d_diag, sizeof(csg::DeviceDiag)));
+  CSG_HIP(hipMemset(p->d_diag, 0, sizeof(csg::DeviceDiag)));
+  CSG_HIP(hipHostMalloc(&p->h_out_flags, nflag * 4, hipHostMallocMapped | hipHostMallocCoherent));
+  std::memset(p->h_out_flags, 0, nflag * 4);
+  CSG_HIP(hipHostGetDevicePointer(reinterpret_cast<void**>(&p->h_out_flags_dev), p->h_out_flags, 0));
+  CSG_HIP(hipMalloc(&p->d_scratch, 64));
+  CSG_HIP(hipDeviceSynchronize());
+  std::string err = p->sdma.open(p->device, p->cfg.copy_engines, p->d_scratch, p->d_epoch_table);
+  if (!err.empty()) return fail(CSG_ERR_HIP, "copy engines: %s", err.c_str());
+  p->sig_data.assign(p->remote_order.size(), hsa_signal_t{0});
+  p->sig_flag.assign(p->remote_order.size(), hsa_signal_t{0});
+  for (size_t i = 0; i < p->remote_order.size(); ++i) {
+    hsa_status_t hs = hsa_signal_create(0, 0, nullptr, &p->sig_data[i]);
+    if (hs == HSA_STATUS_SUCCESS) hs = hsa_signal_create(0, 0, nullptr, &p->sig_flag[i]);
+    if (hs != HSA_STATUS_SUCCESS) return fail(CSG_ERR_NOMEM, "hsa_signal_create: %s", csg::hsa_error(hs).c_str());
+  }
+  CSG_HIP(hipEventCreateWithFlags(&p->ev_copy_in, hipEventDisableTiming));
+  CSG_HIP(hipEventCreateWithFlags(&p->ev_prologue, hipEventDisableTiming));
+  for (hipEvent_t& e : p->ev_kernel_done) CSG_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+  CSG_HIP(hipStreamCreateWithFlags(&p->aux, hipStreamNonBlocking));
+  CSG_HIP(hipDeviceSynchronize());
+  return CSG_OK;
+}
+
+int64_t in_bytes(const csg_plan* p) { return p->in_dtype == CSG_BF16 ? 2 : 4; }
+int64_t out_bytes(const csg_plan* p) { return p->out_dtype == CSG_BF16 ? 2 : 4; }
+
+using Clock = std::chrono::steady_clock;
+
+void spin_until(Clock::time_point t) {
+  while (Clock::now() < t) {
+  }
+}
+
+// Host-side wait for an event, bounded; polls so the caller resumes within microseconds.
+csg_status host_wait(csg_plan* p, hipEvent_t e, const char* what) {
+  const Clock::time_point t0 = Clock::now();
+  const auto budget = std::chrono::milliseconds(p->cfg.timeout_ms) * 4;
+  for (;;) {
+    const hipError_t q = hipEventQuery(e);
+    if (q == hipSuccess) return CSG_OK;
+    if (q != hipErrorNotReady) return hip_fail(q, what);
+    if (Clock::now() - t0 > budget) {
+      p->host_diag = csg_diag{1, -1, -1, 0, p->epoch, 0};
+      return fail(CSG_ERR_TIMEOUT, "%s did not complete in time", what);
+    }
+  }
+}
+
+struct CallState {
+  bool wrapped = false;
+  int prev_parity = 0;
+  bool prev_kernel = false;
+};
+
+// Waits for the copies a previous call left running (only after an error return).
+csg_status drain_copies(csg_plan* p) {
+  if (!p->copies_in_flight) return CSG_OK;
+  const int budget = p->cfg.timeout_ms * 4;
+  for (size_t i = 0; i < p->sig_flag.size(); ++i) {
+    if (csg::sdma_wait(p->sig_data[i], 0, budget) != 0 || csg::sdma_wait(p->sig_flag[i], 0, budget) != 0)
+      return fail(CSG_ERR_TIMEOUT, "copies of the previous call did not complete");
+  }
+  p->copies_in_flight = false;
+  return CSG_OK;
+}
+
+// Front half of a call: the prologue is queued on the compute stream.
+csg_status begin_call(csg_plan* p, csg_mode mode, hipStream_t compute, CallState* cs) {
+  if (mode != CSG_MODE_OVERLAP && mode != CSG_MODE_COMPUTE_ONLY && mode != CSG_MODE_COPY_ONLY)
+    return fail(CSG_ERR_INVALID, "unknown mode %d", static_cast<int>(mode));
+  csg_status st = drain_copies(p);
+  if (st != CSG_OK) return st;
+  cs->prev_parity = p->epoch & 1;
+  cs->prev_kernel = p->kernel_pending[cs->prev_parity];
+  if (p->epoch + 1 >= kEpochTable) {  // wrap (from an odd epoch): clear every flag, restart at 2
+    p->epoch = 1;                     // so the new epoch's parity differs from the last one's
+    cs->wrapped = true;
+  }
+  ++p->epoch;
+  p->host_diag = csg_diag{0, -1, -1, 0, p->epoch, 0};
+  CSG_HIP(csg::launch_prologue(p->d_flags, p->n_chunks(), p->epoch, mode == CSG_MODE_COMPUTE_ONLY ? 1 : 0,
+                               cs->wrapped ? 1 : 0, p->consumer() ? nullptr : p->d_counters, p->d_ticket, p->d_diag,
+                               compute));
+  CSG_HIP(hipEventRecord(p->ev_prologue, compute));
+  p->kernel_pending[p->epoch & 1] = false;
+  return CSG_OK;
+}
+
+// Ordering the copies need, enforced from the host (see the file comment).
+csg_status ready_copies(csg_plan* p, hipStream_t copy, const CallState& cs, bool war_on_previous_kernel) {
+  CSG_HIP(hipEventRecord(p->ev_copy_in, copy));
+  csg_status st = host_wait(p, p->ev_copy_in, "the copy stream's earlier work");
+  if (st != CSG_OK) return st;
+  if (war_on_previous_kernel && cs.prev_kernel) {
+    st = host_wait(p, p->ev_kernel_done[cs.prev_parity], "the previous call's kernel");
+    if (st != CSG_OK) return st;
+  }
+  // the prologue clears counters (producer) and, on a wrap, the flags
+  st = host_wait(p, p->ev_prologue, "the call's prologue");
+  if (st != CSG_OK) return st;
+  p->copies_in_flight = true;
+  return CSG_OK;
+}
+
+// Waits until every issued copy (and flag copy) of this call has completed.
+csg_status finish_copies(csg_plan* p, size_t issued, bool with_flags) {
+  const int budget = p->cfg.timeout_ms * 4;
+  for (size_t i = 0; i < issued; ++i) {
+    hsa_signal_value_t v = csg::sdma_wait(with_flags ? p->sig_flag[i] : p->sig_data[i], 0, budget);
+    if (v < 0) return fail(CSG_ERR_HIP, "SDMA copy %zu reported an error", i);
+    if (v != 0) {
+      p->host_diag = csg_diag{1, p->remote_order[i], -1, 0, p->epoch, 0};
+      return fail(CSG_ERR_TIMEOUT, "SDMA copy of chunk %d did not complete in time", p->remote_order[i]);
+    }
+  }
+  p->copies_in_flight = false;
+  return CSG_OK;
+}
+
+csg_status launch_gemm(csg_plan* p, const void* A, const void* B, void* C, hipStream_t compute) {
+  csg::GemmArgs a{};
+  a.A = A;
+  a.B = B;
+  a.C = C;
+  a.M = p->M;
+  a.N = p->N;
+  a.K = p->K;
+  a.b_group_stride = p->op == CSG_GROUPED_GEMM ? p->N * p->K : 0;
+  a.tiles = p->d_tiles;
+  a.list_ptr = p->d_list_ptr;
+  a.list_ids = p->d_list_ids;
+  a.raster = p->d_raster;
+  a.flags = p->d_flags;
+  a.counters = p->d_counters;
+  a.need = p->d_need;
+  a.out_flags = p->h_out_flags_dev;
+  a.ticket = p->d_ticket;
+  a.diag = p->d_diag;
+  a.timeout_ticks = static_cast<uint64_t>(p->cfg.timeout_ms) * 100000ull;  // 100 MHz wall clock
+  a.epoch = p->epoch;
+  a.n_tiles = p->map.n_tiles();
+  a.n_chunks = p->n_chunks();
+  a.dynamic_ticket = p->cfg.tile_dispatch == 2 ? 0 : 1;
+  CSG_HIP(csg::launch_chunk_gemm(p->key, a, p->grid, compute));
+  CSG_HIP(hipEventRecord(p->ev_kernel_done[p->epoch & 1], compute));
+  p->kernel_pending[p->epoch & 1] = true;
+  return CSG_OK;
+}
+
+// Consumer copies: staging -> landing per remote chunk, then the chunk's flag, both
+// on engine (i mod engines) for the i-th remote chunk in arrival order.
+csg_status issue_consumer_copies(csg_plan* p, void* landing, const void* staging) {
+  const int64_t row_bytes = p->K * in_bytes(p);
+  const bool delayed = !p->delays_us.empty();
+  const Clock::time_point t0 = Clock::now();
+  double release_us = 0.0;
+  const uint32_t* epoch_src = p->d_epoch_table + p->epoch;
+  for (size_t i = 0; i < p->remote_order.size(); ++i) {
+    const int32_t cid = p->remote_order[i];
+    const csg::ChunkDesc& c = p->sched.chunks[cid];
+    if (delayed) {
+      release_us += p->delays_us[i];
+      spin_until(t0 + std::chrono::nanoseconds(static_cast<int64_t>(release_us * 1000.0)));
+    }
+    const int64_t off = c.row_begin * row_bytes;
+    const int64_t bytes = (c.row_end - c.row_begin) * row_bytes;
+    hsa_signal_store_relaxed(p->sig_data[i], 1);
+    hsa_signal_store_relaxed(p->sig_flag[i], 1);
+    const int eng = static_cast<int>(i % p->sdma.count());
+    hsa_status_t hs = p->sdma.copy(static_cast<char*>(landing) + off, static_cast<const char*>(staging) + off,
+                                   static_cast<size_t>(bytes), eng, nullptr, p->sig_data[i]);
+    if (hs == HSA_STATUS_SUCCESS)
+      hs = p->sdma.copy(p->d_flags + cid, epoch_src, 4, eng, &p->sig_data[i], p->sig_flag[i]);
+    if (hs != HSA_STATUS_SUCCESS) {
+      hsa_signal_store_relaxed(p->sig_data[i], 0);
+      hsa_signal_store_relaxed(p->sig_flag[i], 0);
+      (void)finish_copies(p, i, true);
+      return fail(CSG_ERR_HIP, "SDMA copy: %s", csg::hsa_error(hs).c_str());
+    }
+  }
+  return finish_copies(p, p->remote_order.size(), true);
+}
+
+csg_status consumer_call(csg_plan* p, void* landing, const void* staging, const void* b, void* c, csg_mode mode,
+                         void* compute_v, void* copy_v) {
+  if (p->device < 0) return fail(CSG_ERR_STATE, "host-only plan (created with device < 0) cannot run");
+  if (!landing || !b || !c || (mode != CSG_MODE_COMPUTE_ONLY && !staging && !p->remote_order.empty()))
+    return fail(CSG_ERR_INVALID, "NULL buffer");
+  if (!aligned16(landing) || !aligned16(staging) || !aligned16(b) || !aligned16(c))
+    return fail(CSG_ERR_INVALID, "buffers must be 16-byte aligned");
+  hipStream_t compute = static_cast<hipStream_t>(compute_v), copy = static_cast<hipStream_t>(copy_v);
+  DeviceGuard g(p->device);
+  if (g.err != hipSuccess) return hip_fail(g.err, "hipSetDevice");
+  CallState cs;
+  csg_status st = begin_call(p, mode, compute, &cs);
+  if (st != CSG_OK) return st;
+  // the kernel is queued first: it starts as soon as the previous kernel ends and
+  // waits for its chunks, while the host releases the copies
+  if (mode != CSG_MODE_COPY_ONLY && (st = launch_gemm(p, landing, b, c, compute)) != CSG_OK) return st;
+  if (mode == CSG_MODE_COMPUTE_ONLY || p->remote_order.empty()) return CSG_OK;
+  // the landing rows are rewritten: the previous kernel must be done reading them
+  if ((st = ready_copies(p, copy, cs, true)) != CSG_OK) return st;
+  return issue_consumer_copies(p, landing, staging);
+}
+
+}  // namespace
+
+// =====================================================================================
+// C ABI
+// =====================================================================================
+extern "C" {
+
+const char* csg_version(void) { return "csg 0.1.0 (gfx950)"; }
+
+const char* csg_status_str(csg_status s) {
+  switch (s) {
+    case CSG_OK: return "CSG_OK";
+    case CSG_ERR_INVALID: return "CSG_ERR_INVALID";
+    case CSG_ERR_UNSUPPORTED: return "CSG_ERR_UNSUPPORTED";
+    case CSG_ERR_HIP: return "CSG_ERR_HIP";
+    case CSG_ERR_NOMEM: return "CSG_ERR_NOMEM";
+    case CSG_ERR_TIMEOUT: return "CSG_ERR_TIMEOUT";
+    case CSG_ERR_STATE: return "CSG_ERR_STATE";
+  }
+  return "CSG_ERR_UNKNOWN";
+}
+
+const char* csg_last_error(void) { return g_last_error.c_str(); }
+
+csg_status csg_device_check(int device, char* arch, size_t arch_len) {
+  hipDeviceProp_t prop;
+  hipError_t e = hipGetDeviceProperties(&prop, device);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDeviceProperties");
+  if (arch && arch_len) {
+    std::strncpy(arch, prop.gcnArchName, arch_len - 1);
+    arch[arch_len - 1] = '\0';
+  }
+  if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+    return fail(CSG_ERR_UNSUPPORTED, "device %d is %s; this library is built for gfx950 only", device,
+                prop.gcnArchName);
+  return CSG_OK;
+}
+
+csg_status csg_schedule_create(const csg_chunk* chunks, int32_t n, const int32_t* order, csg_schedule** out) {
+  if (!out) return fail(CSG_ERR_INVALID, "out is NULL");
+  *out = nullptr;
+  if (!chunks || !order || n < 1) return fail(CSG_ERR_INVALID, "chunks/order NULL or n < 1");
+  csg::Schedule s;
+  for (int32_t i = 0; i < n; ++i) {
+    if (chunks[i].reserved != 0) return fail(CSG_ERR_INVALID, "chunk %d: reserved field must be 0", i);
+    s.chunks.push_back({chunks[i].row_begin, chunks[i].row_end, chunks[i].src_rank, chunks[i].group,
+                        chunks[i].is_local ? 1 : 0});
+  }
+  s.order.assign(order, order + n);
+  std::string err = csg::validate_schedule(s.chunks, s.order);
+  if (!err.empty()) return fail(CSG_ERR_INVALID, "%s", err.c_str());
+  s.total_rows = s.chunks.back().row_end;
+  csg_schedule* r = new (std::nothrow) csg_schedule{std::move(s)};
+  if (!r) return fail(CSG_ERR_NOMEM, "out of host memory");
+  *out = r;
+  return CSG_OK;
+}
+
+csg_status csg_schedule_uniform(int32_t world, int32_t rank, int64_t shard_rows, int32_t chunks_per_shard,
+                                csg_order order, const int32_t* remote_perm_host, csg_schedule** out) {
+  if (!out) return fail(CSG_ERR_INVALID, "out is NULL");
+  *out = nullptr;
+  if (order < CSG_ORDER_RING || order > CSG_ORDER_RS_RING) return fail(CSG_ERR_INVALID, "unknown order");
+  csg::Schedule s;
+  std::string err = csg::make_uniform_schedule(world, rank, shard_rows, chunks_per_shard,
+                                               static_cast<csg::OrderKind>(order), remote_perm_host, &s);
+  if (!err.empty()) return fail(CSG_ERR_INVALID, "%s", err.c_str());
+  csg_schedule* r = new (std::nothrow) csg_schedule{std::move(s)};
+  if (!r) return fail(CSG_ERR_NOMEM, "out of host memory");
+  *out = r;
+  return CSG_OK;
+}
+
+csg_status csg_schedule_grouped(int32_t world, int32_t rank, int32_t n_groups, const int64_t* counts_host,
+                                csg_schedule** out) {
+  if (!out) return fail(CSG_ERR_INVALID, "out is NULL");
+  *out = nullptr;
+  csg::Schedule s;
+  std::string err = csg::make_grouped_schedule(world, rank, n_groups, counts_host, &s);
+  if (!err.empty()) return fail(CSG_ERR_INVALID, "%s", err.c_str());
+  csg_schedule* r = new (std::nothrow) csg_schedule{std::move(s)};
+  if (!r) return fail(CSG_ERR_NOMEM, "out of host memory");
+  *out = r;
+  return CSG_OK;
+}
+
+csg_status csg_schedule_info(const csg_schedule* s, int32_t* n_chunks, int64_t* total_rows) {
+  if (!s) return fail(CSG_ERR_INVALID, "schedule is NULL");
+  if (n_chunks) *n_chunks = static_cast<int32_t>(s->s.chunks.size());
+  if (total_rows) *total_rows = s->s.total_rows;
+  return CSG_OK;
+}
+
+csg_status csg_schedule_get(const csg_schedule* s, csg_chunk* chunks_host, int32_t* order_host) {
+  if (!s) return fail(CSG_ERR_INVALID, "schedule is NULL");
+  for (size_t i = 0; i < s->s.chunks.size(); ++i) {
+    const csg::ChunkDesc& c = s->s.chunks[i];
+    if (chunks_host) chunks_host[i] = csg_chunk{c.row_begin, c.row_end, c.src_rank, c.group, c.is_local, 0};
+    if (order_host) order_host[i] = s->s.order[i];
+  }
+  return CSG_OK;
+}
+
+void csg_schedule_destroy(csg_schedule* s) { delete s; }
+
+csg_status csg_plan_create(csg_op op, int64_t M, int64_t N, int64_t K, csg_dtype in_dtype, csg_dtype out_dtype,
+                           const csg_schedule* s, const int64_t* group_rows_host, int32_t n_groups,
+                           const csg_plan_cfg* cfg, int device, csg_plan** out) {
+  if (!out) return fail(CSG_ERR_INVALID, "out is NULL");
+  *out = nullptr;
+  if (!s) return fail(CSG_ERR_INVALID, "schedule is NULL");
+  if (op < CSG_AG_GEMM || op > CSG_GROUPED_GEMM) return fail(CSG_ERR_INVALID, "unknown op");
+  if ((in_dtype != CSG_BF16 && in_dtype != CSG_F32) || (out_dtype != CSG_BF16 && out_dtype != CSG_F32))
+    return fail(CSG_ERR_INVALID, "unknown dtype");
+  if (M < 1 || N < 1 || K < 1 || M > 0x7fffffff || N > 0x7fffffff || K > (1 << 22))
+    return fail(CSG_ERR_INVALID, "shape out of range");
+  std::vector<int64_t> groups;
+  if (op == CSG_GROUPED_GEMM) {
+    if (!group_rows_host || n_groups < 1) return fail(CSG_ERR_INVALID, "grouped GEMM needs group rows");
+    groups.assign(group_rows_host, group_rows_host + n_groups);
+  } else if (group_rows_host || n_groups) {
+    return fail(CSG_ERR_INVALID, "group rows are only for the grouped GEMM");
+  }
+  csg_plan_cfg c = cfg ? *cfg : csg_plan_cfg{};
+  const bool bf16 = in_dtype == CSG_BF16;
+  if (c.bm == 0) c.bm = bf16 ? 256 : 64;
+  if (c.bn == 0) c.bn = bf16 ? 256 : 64;
+  if (c.bk == 0) c.bk = bf16 ? 64 : 16;
+  if (c.timeout_ms == 0) c.timeout_ms = 2000;
+  if (c.bm < 1 || c.bn < 1 || c.bk < 1 || c.copy_engines < 0 || c.copy_engines > 32 || c.timeout_ms < 1 ||
+      c.num_workgroups < 0 || c.tile_dispatch < 0 || c.tile_dispatch > 2 || c.intra_order != 0)
+    return fail(CSG_ERR_INVALID, "bad plan configuration");
+
+  csg_plan* p = new (std::nothrow) csg_plan;
+  if (!p) return fail(CSG_ERR_NOMEM, "out of host memory");
+  p->op = op;
+  p->M = M;
+  p->N = N;
+  p->K = K;
+  p->in_dtype = in_dtype;
+  p->out_dtype = out_dtype;
+  p->sched = s->s;
+  p->group_rows = groups;
+  p->cfg = c;
+  std::string err = csg::build_tile_map(p->sched, M, N, c.bm, c.bn, op == CSG_GEMM_RS, groups, &p->map);
+  if (!err.empty()) {
+    delete p;
+    return fail(CSG_ERR_INVALID, "%s", err.c_str());
+  }
+  for (int32_t c_id : p->sched.order)
+    if (!p->sched.chunks[c_id].is_local) p->remote_order.push_back(c_id);
+
+  if (device >= 0) {
+    p->key = csg::KernelKey{bf16 ? csg::InType::BF16 : csg::InType::F32, out_dtype == CSG_BF16, op == CSG_GEMM_RS,
+                            c.bm, c.bn, c.bk};
+    if (!csg::kernel_supported(p->key)) {
+      delete p;
+      return fail(CSG_ERR_UNSUPPORTED, "no kernel for dtype %d->%d tile %dx%dx%d", in_dtype, out_dtype, c.bm, c.bn,
+                  c.bk);
+    }
+    if (K % c.bk != 0 || N % 4 != 0) {
+      delete p;
+      return fail(CSG_ERR_UNSUPPORTED, "K must be a multiple of %d and N a multiple of 4", c.bk);
+    }
+    if (p->consumer() && p->n_chunks() > csg::kernel_max_chunks()) {
+      delete p;
+      return fail(CSG_ERR_UNSUPPORTED, "at most %d chunks", csg::kernel_max_chunks());
+    }
+    char arch[64];
+    csg_status st = csg_device_check(device, arch, sizeof arch);
+    if (st != CSG_OK) {
+      delete p;
+      return st;
+    }
+    p->device = device;
+    {
+      DeviceGuard g(device);
+      hipError_t e = g.err != hipSuccess ? g.err : csg::kernel_grid(p->key, device, &p->grid);
+      if (e != hipSuccess) {
+        p->device = -1;
+        delete p;
+        return hip_fail(e, "occupancy query");
+      }
+    }
+    if (c.num_workgroups > 0) p->grid = c.num_workgroups;
+    st = setup_device(p);
+    if (st != CSG_OK) {
+      std::string msg = g_last_error;
+      free_plan_device(p);
+      delete p;
+      g_last_error = msg;
+      return st;
+    }
+  }
+  *out = p;
+  return CSG_OK;
+}
+
+csg_status csg_plan_info_get(const csg_plan* p, csg_plan_info* info) {
+  if (!p || !info) return fail(CSG_ERR_INVALID, "NULL argument");
+  info->n_tiles = p->map.n_tiles();
+  info->n_chunks = p->n_chunks();
+  info->nnz = static_cast<int32_t>(p->map.tile_chunks.size());
+  info->n_tiles_n = p->map.n_tiles_n;
+  info->num_workgroups = p->device >= 0 ? p->grid : 0;
+  info->bm = p->cfg.bm;
+  info->bn = p->cfg.bn;
+  info->bk = p->cfg.bk;
+  return CSG_OK;
+}
+
+csg_status csg_plan_get_map(const csg_plan* p, int32_t* tile_ptr, int32_t* tile_chunks, int32_t* chunk_ptr,
+                            int32_t* chunk_tiles, int32_t* tile_order) {
+  if (!p) return fail(CSG_ERR_INVALID, "plan is NULL");
+  const csg::TileMap& m = p->map;
+  auto cp = [](int32_t* dst, const std::vector<int32_t>& v) {
+    if (dst && !v.empty()) std::memcpy(dst, v.data(), v.size() * sizeof(int32_t));
+  };
+  cp(tile_ptr, m.tile_ptr);
+  cp(tile_chunks, m.tile_chunks);
+  cp(chunk_ptr, m.chunk_ptr);
+  cp(chunk_tiles, m.chunk_tiles);
+  cp(tile_order, m.order);
+  return CSG_OK;
+}
+
+csg_status csg_plan_set_copy_delays(csg_plan* p, const float* delay_us_host, int32_t n) {
+  if (!p) return fail(CSG_ERR_INVALID, "plan is NULL");
+  if (!delay_us_host) {
+    p->delays_us.clear();
+    return CSG_OK;
+  }
+  if (n != static_cast<int32_t>(p->remote_order.size()))
+    return fail(CSG_ERR_INVALID, "need %zu delays (one per remote chunk), got %d", p->remote_order.size(), n);
+  for (int32_t i = 0; i < n; ++i)
+    if (!(delay_us_host[i] >= 0.0f) || delay_us_host[i] > 1e6f) return fail(CSG_ERR_INVALID, "bad delay %d", i);
+  p->delays_us.assign(delay_us_host, delay_us_host + n);
+  return CSG_OK;
+}
+
+csg_status csg_ag_gemm(csg_plan* p, void* a_landing, const void* a_staging, const void* b_nk, void* c, csg_mode mode,
+                       void* compute_stream, void* copy_stream) {
+  if (!p) return fail(CSG_ERR_INVALID, "plan is NULL");
+  if (p->op != CSG_AG_GEMM) return fail(CSG_ERR_INVALID, "plan is not an all-gather GEMM plan");
+  return consumer_call(p, a_landing, a_staging, b_nk, c, mode, compute_stream, copy_stream);
+}
+
+csg_status csg_grouped_gemm(csg_plan* p, void* x_landing, const void* x_staging, const void* b_enk, void* c,
+                            csg_mode mode, void* compute_stream, void* copy_stream) {
+  if (!p) return fail(CSG_ERR_INVALID, "plan is NULL");
+  if (p->op != CSG_GROUPED_GEMM) return fail(CSG_ERR_INVALID, "plan is not a grouped GEMM plan");
+  return consumer_call(p, x_landing, x_staging, b_enk, c, mode, compute_stream, copy_stream);
+}
+
+csg_status csg_gemm_rs(csg_plan* p, const void* a, const void* b_nk, void* c, void* c_outgoing, csg_mode mode,
+                       void* compute_stream, void* copy_stream) {
+  if (!p) return fail(CSG_ERR_INVALID, "plan is NULL");
+  if (p->op != CSG_GEMM_RS) return fail(CSG_ERR_INVALID, "plan is not a GEMM + reduce-scatter plan");
+  if (p->device < 0) return fail(CSG_ERR_STATE, "host-only plan (created with device < 0) cannot run");
+  if (!a || !b_nk || !c || (mode != CSG_MODE_COMPUTE_ONLY && !c_outgoing && !p->remote_order.empty()))
+    return fail(CSG_ERR_INVALID, "NULL buffer");
+  if (!aligned16(a) || !aligned16(b_nk) || !aligned16(c) || !aligned16(c_outgoing))
+    return fail(CSG_ERR_INVALID, "buffers must be 16-byte aligned");
+  hipStream_t compute = static_cast<hipStream_t>(compute_stream), copy = static_cast<hipStream_t>(copy_stream);
+  DeviceGuard g(p->device);
+  if (g.err != hipSuccess) return hip_fail(g.err, "hipSetDevice");
+  CallState cs;
+  csg_status st = begin_call(p, mode, compute, &cs);
+  if (st != CSG_OK) return st;
+  if (mode != CSG_MODE_COPY_ONLY && (st = launch_gemm(p, a, b_nk, c, compute)) != CSG_OK) return st;
+  if (mode == CSG_MODE_COMPUTE_ONLY || p->remote_order.empty()) return CSG_OK;
+  // copy-only reads the C a previous kernel wrote: that kernel must have finished
+  if ((st = ready_copies(p, copy, cs, mode == CSG_MODE_COPY_ONLY)) != CSG_OK) return st;
+  const int64_t row_bytes = p->N * out_bytes(p);
+  const auto budget = std::chrono::milliseconds(p->cfg.timeout_ms) * 4;
+  const Clock::time_point t0 = Clock::now();
+  for (size_t i = 0; i < p->remote_order.size(); ++i) {
+    const int32_t cid = p->remote_order[i];
+    if (mode == CSG_MODE_OVERLAP) {
+      const volatile uint32_t* f = p->h_out_flags + cid;
+      while (*f < p->epoch) {
+        if (Clock::now() - t0 > budget) {
+          (void)finish_copies(p, i, false);
+          p->host_diag = csg_diag{1, cid, -1, *f, p->epoch, 0};
+          return fail(CSG_ERR_TIMEOUT, "output chunk %d was not completed in time", cid);
+        }
+      }
+    }
+    const csg::ChunkDesc& ch = p->sched.chunks[cid];
+    const int64_t off = ch.row_begin * row_bytes;
+    hsa_signal_store_relaxed(p->sig_data[i], 1);
+    const hsa_status_t hs =
+        p->sdma.copy(static_cast<char*>(c_outgoing) + off, static_cast<const char*>(c) + off,
+                     static_cast<size_t>((ch.row_end - ch.row_begin) * row_bytes), static_cast<int>(i % p->sdma.count()),
+                     nullptr, p->sig_data[i]);
+    if (hs != HSA_STATUS_SUCCESS) {
+      hsa_signal_store_relaxed(p->sig_data[i], 0);
+      (void)finish_copies(p, i, false);
+      return fail(CSG_ERR_HIP, "SDMA copy: %s", csg::hsa_error(hs).c_str());
+    }
+  }
+  return finish_copies(p, p->remote_order.size(), false);
+}
+
+csg_status csg_plan_check(csg_plan* p, csg_diag* out) {
+  if (!p) return fail(CSG_ERR_INVALID, "plan is NULL");
+  csg_diag d = p->host_diag;
+  if (p->device >= 0 && p->epoch > 0) {
+    DeviceGuard g(p->device);
+    if (g.err != hipSuccess) return hip_fail(g.err, "hipSetDevice");
+    CSG_HIP(hipEventSynchronize(p->ev_prologue));
+    if (p->kernel_pending[p->epoch & 1]) CSG_HIP(hipEventSynchronize(p->ev_kernel_done[p->epoch & 1]));
+    csg_status st = drain_copies(p);
+    if (st != CSG_OK) return st;
+    csg::DeviceDiag dd{};
+    CSG_HIP(hipMemcpyAsync(&dd, p->d_diag, sizeof dd, hipMemcpyDeviceToHost, p->aux));
+    CSG_HIP(hipStreamSynchronize(p->aux));
+    if (dd.timed_out && !d.timed_out) d = csg_diag{1, dd.chunk, dd.tile, dd.observed, dd.epoch, 0};
+  }
+  if (out) *out = d;
+  if (d.timed_out)
+    return fail(CSG_ERR_TIMEOUT, "chunk %d (tile %d) never became ready: flag %u < epoch %u", d.chunk, d.tile,
+                d.observed, d.epoch);
+  return CSG_OK;
+}
+
+void csg_plan_destroy(csg_plan* p) {
+  if (!p) return;
+  free_plan_device(p);
+  delete p;
+}
+
+}  // extern "C"

@@ -1,0 +1,74 @@
+// Interface between the host runtime and the HIP kernels of the chunk-scheduled GEMM.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace csg {
+
+// Written by the kernel when a bounded flag wait gives up; read back by csg_plan_check.
+struct DeviceDiag {
+  uint32_t timed_out;
+  int32_t chunk;
+  int32_t tile;
+  uint32_t observed;
+  uint32_t epoch;
+  uint32_t abort;     // set once any workgroup gave up; the others stop taking tiles
+  uint32_t pad[2];
+};
+
+// One entry of the execution-ordered tile list.
+struct TileDesc {
+  int32_t row_begin;  // first output row (global)
+  int32_t row_end;    // one past the last valid output row
+  int32_t n_tile;     // tile index along N
+  int32_t group;      // expert index (grouped GEMM), else 0
+};
+
+struct GemmArgs {
+  const void* A;             // rows of A (AG: landing buffer; grouped: routed X), K contiguous
+  const void* B;             // N x K, or E x N x K
+  void* C;                   // M x N
+  int64_t M, N, K;
+  int64_t b_group_stride;    // elements between consecutive experts' weights
+  const TileDesc* tiles;     // [n_tiles] in execution order
+  const int32_t* list_ptr;   // [n_tiles + 1]: per execution position, its chunks
+  const int32_t* list_ids;   // consumer: remote chunks to wait for; producer: chunks written
+  const int32_t* raster;     // [n_tiles] raster id per execution position (diagnostics)
+  uint32_t* flags;           // consumer: per-chunk ready flags
+  uint32_t* counters;        // producer: finished tiles per chunk
+  const int32_t* need;       // producer: tiles per chunk
+  uint32_t* out_flags;       // producer: per-chunk completion flags (host-visible memory)
+  uint32_t* ticket;          // dynamic tile ticket
+  DeviceDiag* diag;
+  uint64_t timeout_ticks;    // bound of one flag wait, in 100 MHz wall-clock ticks
+  uint32_t epoch;            // a flag is ready when it is >= epoch
+  int32_t n_tiles;
+  int32_t n_chunks;
+  int32_t dynamic_ticket;
+};
+
+enum class InType : int32_t { BF16 = 0, F32 = 1 };
+
+struct KernelKey {
+  InType in;
+  bool out_bf16;
+  bool producer;
+  int32_t bm, bn, bk;
+};
+
+// Kernel variants compiled into this library; false if `key` has none.
+bool kernel_supported(const KernelKey& key);
+// Largest chunk count the per-workgroup ready cache holds.
+int32_t kernel_max_chunks();
+// Persistent grid size: co-resident workgroups on the device.
+hipError_t kernel_grid(const KernelKey& key, int device, int32_t* grid);
+hipError_t launch_chunk_gemm(const KernelKey& key, const GemmArgs& args, int32_t grid, hipStream_t stream);
+
+// Per-call set-up on the compute stream: clears counters, the ticket and the
+// diagnostics, and pre-sets (compute-only) or clears (epoch wrap) the ready flags.
+hipError_t launch_prologue(uint32_t* flags, int32_t n_chunks, uint32_t epoch, int32_t preset_all, int32_t clear_flags,
+                           uint32_t* counters, uint32_t* ticket, DeviceDiag* diag, hipStream_t stream);
+
+}  // namespace csg

@@ -1,0 +1,53 @@
+// SDMA copy-engine driver: device-to-device copies issued straight to chosen SDMA
+// engines through the HSA runtime (hsa_amd_memory_async_copy_on_engine), with HSA
+// signals for completion and for ordering one copy after another.
+//
+// Copies issued here never occupy a compute unit and never enter a HIP stream, so
+// they progress while a persistent kernel holds every CU and polls the flags they
+// raise. Spreading consecutive chunks over all engines multiplies the copy
+// bandwidth (one engine moves about 48 GB/s device-to-device on MI355X).
+#pragma once
+
+#include <hsa/hsa.h>
+#include <hsa/hsa_ext_amd.h>
+
+#include <cstddef>
+#include <string>
+#include <vector>
+
+namespace csg {
+
+class SdmaEngines {
+ public:
+  SdmaEngines() = default;
+  SdmaEngines(const SdmaEngines&) = delete;
+  SdmaEngines& operator=(const SdmaEngines&) = delete;
+  ~SdmaEngines() { close(); }
+
+  // Finds the HSA agent of HIP device `hip_device` (by PCI location), lists the SDMA
+  // engines usable for its device-to-device copies and keeps at most `max_engines`
+  // (0 = all). Every engine is warmed up with one small copy. "" on success.
+  std::string open(int hip_device, int max_engines, void* scratch_dst, const void* scratch_src);
+  void close();
+
+  int count() const { return static_cast<int>(engines_.size()); }
+  bool is_open() const { return opened_; }
+
+  // Copy `bytes` from src to dst on engine `engine % count()`. The copy starts once
+  // `dep` (if non-null) reads 0 and decrements `done` when it has completed.
+  hsa_status_t copy(void* dst, const void* src, size_t bytes, int engine, const hsa_signal_t* dep,
+                    hsa_signal_t done) const;
+
+ private:
+  bool opened_ = false;
+  bool hsa_inited_ = false;
+  hsa_agent_t agent_{0};
+  std::vector<hsa_amd_sdma_engine_id_t> engines_;
+};
+
+// Polls `s` until it reads `value` or `budget_ms` pass. Returns the last value read.
+hsa_signal_value_t sdma_wait(hsa_signal_t s, hsa_signal_value_t value, int budget_ms);
+
+std::string hsa_error(hsa_status_t s);
+
+}  // namespace csg

@@ -1,0 +1,161 @@
+"""The C-ABI library on the host (no GPU): it loads, exports every declared symbol,
+and its schedules, dependence maps and tile orders equal the oracle's bit for bit.
+No compute call is made here; device work is covered by the -m gpu tests."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2601_20595_amd as csg
+import seeded_inputs as si
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_library_exports_every_declared_symbol():
+    header = open(os.path.join(ROOT, "include", "csg.h")).read()
+    declared = set(re.findall(r"\b(csg_[a-z_0-9]+)\s*\(", header))
+    assert declared == set(csg.ABI_FUNCTIONS)
+    lib = csg._lib()
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert csg.csg_version().startswith("csg")
+    assert csg.csg_status_str(csg.CSG_ERR_TIMEOUT) == "CSG_ERR_TIMEOUT"
+
+
+def _oracle_chunks_tuple(chunks):
+    return [(c.row_begin, c.row_end, c.src_rank, c.group, int(c.is_local)) for c in chunks]
+
+
+@pytest.mark.parametrize("kind", ["ring", "swizzle1d", "rs_ring", "permutation"])
+@pytest.mark.parametrize("W,r,S,Q", [(1, 0, 64, 1), (2, 1, 128, 2), (8, 0, 1024, 4), (8, 5, 2048, 16), (3, 2, 96, 3)])
+def test_uniform_schedule_matches_oracle(kind, W, r, S, Q):
+    perm = si.draw_permutation(7, W * 100 + r, (W - 1) * Q) if kind == "permutation" else None
+    ch, od = oracle.uniform_schedule(W, r, S, Q, kind, perm)
+    s = csg.Schedule.uniform(W, r, S, Q, kind, perm)
+    chunks, order = s.get()
+    assert chunks == _oracle_chunks_tuple(ch)
+    assert order == od
+
+
+@pytest.mark.parametrize("rep", [0, 1, 2])
+def test_grouped_schedule_matches_oracle(rep):
+    w = si.WORKLOADS[5]
+    routing = si.draw_topk_routing(5, rep, 4096, 8, 2, 1.2)
+    _, counts = si.grouped_layout(routing, 8, 8)
+    counts[3, 7] = 0                               # force an empty segment
+    for r in (0, 5):
+        ch, od, gr = oracle.grouped_schedule(8, r, counts)
+        s = csg.Schedule.grouped(8, r, counts)
+        chunks, order = s.get()
+        assert chunks == _oracle_chunks_tuple(ch)
+        assert order == od
+
+
+MAP_CASES = [
+    # (op, W, r, S, Q, kind, N, BM, BN)
+    ("ag", 2, 0, 128, 2, "permutation", 256, 64, 64),
+    ("ag", 8, 0, 1024, 4, "ring", 1792, 256, 256),
+    ("ag", 8, 3, 1024, 4, "swizzle1d", 1792, 256, 224),
+    ("rs", 8, 0, 1024, 4, "rs_ring", 4096, 256, 256),
+    ("rs", 4, 1, 96, 2, "rs_ring", 100, 64, 48),            # straddling, ragged N
+    ("ag", 8, 0, 2048, 16, "permutation", 3584, 256, 256),  # 2 chunks per tile
+    ("ag", 3, 2, 160, 2, "permutation", 600, 256, 256),     # straddling, ragged M and N
+    ("ag", 4, 1, 64, 4, "ring", 64, 96, 32),                # tiles spanning 6 chunks
+]
+
+
+@pytest.mark.parametrize("case", MAP_CASES, ids=lambda c: "-".join(map(str, c)))
+def test_plan_map_matches_oracle_bit_exact(case):
+    op, W, r, S, Q, kind, N, BM, BN = case
+    perm = si.draw_permutation(11, W + r, (W - 1) * Q) if kind == "permutation" else None
+    ch, od = oracle.uniform_schedule(W, r, S, Q, kind, perm)
+    dm = oracle.dep_map(ch, od, W * S, N, BM, BN, producer=(op == "rs"))
+    s = csg.Schedule.uniform(W, r, S, Q, kind, perm)
+    p = csg.Plan(op, W * S, N, 64, "bf16", "bf16", s, cfg={"bm": BM, "bn": BN}, device=-1)
+    m = p.get_map()
+    assert np.array_equal(m["tile_ptr"], dm.tile_ptr)
+    assert np.array_equal(m["tile_chunks"], dm.tile_chunks)
+    assert np.array_equal(m["chunk_ptr"], dm.chunk_ptr)
+    assert np.array_equal(m["chunk_tiles"], dm.chunk_tiles)
+    assert np.array_equal(m["tile_order"], dm.order)
+
+
+@pytest.mark.parametrize("BM,BN", [(256, 256), (128, 64), (96, 128)])
+def test_grouped_plan_map_matches_oracle(BM, BN):
+    routing = si.draw_topk_routing(5, 3, 2048, 8, 2, 1.2)
+    _, counts = si.grouped_layout(routing, 8, 8)
+    ch, od, gr = oracle.grouped_schedule(8, 2, counts)
+    M = sum(gr)
+    dm = oracle.dep_map(ch, od, M, 1792, BM, BN, group_rows=gr)
+    s = csg.Schedule.grouped(8, 2, counts)
+    p = csg.Plan("grouped", M, 1792, 4096, "bf16", "bf16", s, group_rows=gr, cfg={"bm": BM, "bn": BN}, device=-1)
+    m = p.get_map()
+    assert np.array_equal(m["tile_ptr"], dm.tile_ptr)
+    assert np.array_equal(m["tile_chunks"], dm.tile_chunks)
+    assert np.array_equal(m["chunk_tiles"], dm.chunk_tiles)
+    assert np.array_equal(m["tile_order"], dm.order)
+
+
+def test_general_schedule_and_order_invariance_of_map_shape():
+    chunks = [(0, 40, 0, 0, 1), (40, 100, 1, 0, 0), (100, 128, 1, 0, 0)]
+    for order in ([0, 1, 2], [0, 2, 1], [2, 1, 0]):
+        s = csg.Schedule.create(chunks, order)
+        p = csg.Plan("ag", 128, 64, 64, "bf16", "bf16", s, cfg={"bm": 32, "bn": 64}, device=-1)
+        och = [oracle.Chunk(*c[:4], bool(c[4])) for c in chunks]
+        dm = oracle.dep_map(och, order, 128, 64, 32, 64)
+        m = p.get_map()
+        assert np.array_equal(m["tile_chunks"], dm.tile_chunks)
+        assert np.array_equal(m["tile_order"], dm.order)
+
+
+def _status(fn, *a, **k):
+    try:
+        fn(*a, **k)
+    except csg.CsgError as e:
+        return e.status
+    return csg.CSG_OK
+
+
+def test_validation_errors():
+    bad = [
+        ([(0, 4, 0, 0, 1), (5, 8, 1, 0, 0)], [0, 1]),   # gap
+        ([(0, 5, 0, 0, 1), (4, 8, 1, 0, 0)], [0, 1]),   # overlap
+        ([(0, 4, 0, 0, 1), (4, 8, 1, 0, 0)], [0, 0]),   # not a permutation
+        ([(0, 0, 0, 0, 1), (0, 8, 1, 0, 0)], [0, 1]),   # empty chunk
+        ([(0, 4, 0, 0, 1), (4, 8, 1, 0, 0)], [0, 2]),   # id out of range
+    ]
+    for chunks, order in bad:
+        assert _status(csg.csg_schedule_create, chunks, order) == csg.CSG_ERR_INVALID
+    assert _status(csg.csg_schedule_uniform, 2, 2, 64, 2, "ring") == csg.CSG_ERR_INVALID      # rank >= world
+    assert _status(csg.csg_schedule_uniform, 2, 0, 10, 3, "ring") == csg.CSG_ERR_INVALID      # S % Q
+    assert _status(csg.csg_schedule_uniform, 2, 0, 64, 2, "permutation", [0, 0]) == csg.CSG_ERR_INVALID
+    assert _status(csg.csg_schedule_uniform, 2, 0, 64, 2, "permutation", [0, 5]) == csg.CSG_ERR_INVALID
+    assert _status(csg.csg_schedule_grouped, 2, 0, np.zeros((2, 3))) == csg.CSG_ERR_INVALID   # all empty
+    s = csg.Schedule.uniform(2, 0, 64, 2, "ring")
+    # M must equal the rows the chunks cover
+    assert _status(csg.Plan, "ag", 100, 64, 64, "bf16", "bf16", s, device=-1) == csg.CSG_ERR_INVALID
+    assert _status(csg.Plan, "ag", 128, 0, 64, "bf16", "bf16", s, device=-1) == csg.CSG_ERR_INVALID
+    # group rows only for the grouped op, and must sum to M
+    assert _status(csg.Plan, "ag", 128, 64, 64, "bf16", "bf16", s, group_rows=[128], device=-1) == csg.CSG_ERR_INVALID
+    g = csg.Schedule.grouped(2, 0, [[3, 1], [2, 0]])
+    assert _status(csg.Plan, "grouped", 6, 64, 64, "bf16", "bf16", g, group_rows=[4, 2], device=-1) \
+        == csg.CSG_ERR_INVALID
+    assert _status(csg.Plan, "grouped", 6, 64, 64, "bf16", "bf16", g, group_rows=[5, 1], device=-1) == csg.CSG_OK
+    # bad configuration
+    assert _status(csg.Plan, "ag", 128, 64, 64, "bf16", "bf16", s, cfg={"copy_engines": 99}, device=-1) \
+        == csg.CSG_ERR_INVALID
+
+
+def test_host_only_plan_cannot_run_and_delays_are_checked():
+    s = csg.Schedule.uniform(4, 0, 64, 2, "ring")
+    p = csg.Plan("ag", 256, 64, 64, "bf16", "bf16", s, device=-1)
+    assert _status(p.ag_gemm, 16, 16, 16, 16) == csg.CSG_ERR_STATE
+    assert _status(p.gemm_rs, 16, 16, 16, 16) == csg.CSG_ERR_INVALID      # wrong op for this plan
+    assert _status(p.set_copy_delays, [1.0] * 5) == csg.CSG_ERR_INVALID   # needs 6 (remote chunks)
+    assert _status(p.set_copy_delays, [1.0] * 6) == csg.CSG_OK
+    assert _status(p.set_copy_delays, [-1.0] * 6) == csg.CSG_ERR_INVALID
+    assert _status(p.set_copy_delays, None) == csg.CSG_OK
+    assert p.info.num_workgroups == 0

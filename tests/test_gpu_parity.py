@@ -1,0 +1,245 @@
+"""GPU parity: the HIP path (called through the C ABI) against the CPU oracle.
+
+Small cases span several tiles, chunks that straddle tiles, and ragged M / N
+tails; they are compared element by element. The benchmark's full-size workloads
+are compared on sampled output rows the oracle computes one by one, in the launch
+configuration the benchmark times. Tolerances: max relative error (metric of
+oracle.max_rel_error) <= 2e-2 with bf16, <= 1e-4 for fp32 end to end; integer-
+valued inputs are compared bit for bit.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2601_20595_amd as csg
+import seeded_inputs as si
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    from gpu_util import (DEV, assert_close, bf16_rne_of_f64, out_to_f64, run_ag, run_rs, sample_rows, streams,
+                          to_dev, tol_for, empty_out, nan_fill_)
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def _small_ag(W, r, S, Q, kind, N, K, dtype, out_dtype, dist="normal", rep=0, cfg_id=101):
+    w = si.Workload(cfg_id, "small", "ag", M=W * S, N=N, K=K, dtype=dtype, out_dtype=out_dtype, dist=dist,
+                    world=W, rank=r, shard_rows=S, chunks_per_shard=Q, order=kind)
+    d = si.draw(w, rep=rep)
+    perm = si.draw_permutation(cfg_id, rep, (W - 1) * Q) if kind == "permutation" else None
+    chunks, order = oracle.uniform_schedule(W, r, S, Q, kind, perm)
+    return w, d, perm, chunks, order
+
+
+def test_device_is_gfx950():
+    assert csg.csg_device_check(0).startswith("gfx950")
+
+
+AG_SMALL = [
+    # W, r, S, Q, kind, N, K, dtype, out
+    (2, 0, 128, 2, "permutation", 256, 256, "f32", "f32"),      # the 256^3 fp32 workload itself
+    (3, 1, 100, 2, "ring", 200, 96, "f32", "f32"),              # ragged M and N, straddling tiles
+    (4, 0, 300, 2, "ring", 600, 512, "bf16", "bf16"),           # ragged M (1200) and N (600), h = 150
+    (4, 3, 256, 4, "swizzle1d", 520, 320, "bf16", "bf16"),      # 4 chunks per 256-row tile
+    (2, 1, 512, 1, "permutation", 256, 1024, "bf16", "f32"),    # bf16 in, fp32 out
+]
+
+
+@pytest.mark.parametrize("case", AG_SMALL, ids=lambda c: "W%d-r%d-S%d-Q%d-%s-N%d-K%d-%s-%s" % c)
+@pytest.mark.parametrize("mode", ["overlap", "compute_only"])
+def test_ag_small_parity(case, mode):
+    W, r, S, Q, kind, N, K, dtype, out_dtype = case
+    _say("ag small %s mode=%s" % (case, mode))
+    w, d, perm, chunks, order = _small_ag(W, r, S, Q, kind, N, K, dtype, out_dtype)
+    s = csg.Schedule.uniform(W, r, S, Q, kind, perm)
+    plan = csg.Plan("ag", W * S, N, K, dtype, out_dtype, s, cfg={"timeout_ms": 1000})
+    c, landing = run_ag(plan, chunks, d.A, d.B, out_dtype, mode=mode)
+    G = out_to_f64(c, out_dtype)
+    R = oracle.ag_gemm(d.A.device_array, d.B.device_array, chunks, order)
+    assert_close(G, R, tol_for(out_dtype, dtype), "ag small")
+    if mode == "overlap":
+        # every remote chunk landed: landing == A
+        assert torch.equal(landing.cpu(), to_dev(d.A.device_array).cpu())
+
+
+@pytest.mark.parametrize("out_dtype", ["f32", "bf16"])
+def test_integer_inputs_bit_exact(out_dtype):
+    W, r, S, Q, N, K = 4, 2, 192, 3, 384, 640
+    _say("integer bit-exact out=%s" % out_dtype)
+    w, d, perm, chunks, order = _small_ag(W, r, S, Q, "permutation", N, K, "bf16", out_dtype, dist="int")
+    s = csg.Schedule.uniform(W, r, S, Q, "permutation", perm)
+    plan = csg.Plan("ag", W * S, N, K, "bf16", out_dtype, s, cfg={"timeout_ms": 1000})
+    c, _ = run_ag(plan, chunks, d.A, d.B, out_dtype)
+    G = out_to_f64(c, out_dtype)
+    R = oracle.ag_gemm(d.A.device_array, d.B.device_array, chunks, order)     # exact integers
+    expect = R if out_dtype == "f32" else bf16_rne_of_f64(R)
+    assert np.array_equal(G, expect)
+
+
+def test_arrival_order_does_not_change_a_bit():
+    W, r, S, Q, N, K = 4, 1, 256, 2, 512, 512
+    _say("order determinism")
+    results = []
+    for kind, rep in (("ring", 0), ("swizzle1d", 0), ("permutation", 0), ("permutation", 1)):
+        w, d, perm, chunks, order = _small_ag(W, r, S, Q, kind, N, K, "bf16", "bf16", rep=0)
+        if kind == "permutation":
+            perm = si.draw_permutation(77, rep, (W - 1) * Q)
+        s = csg.Schedule.uniform(W, r, S, Q, kind, perm)
+        plan = csg.Plan("ag", W * S, N, K, "bf16", "bf16", s, cfg={"timeout_ms": 1000})
+        c, _ = run_ag(plan, oracle.uniform_schedule(W, r, S, Q, kind, perm)[0], d.A, d.B, "bf16")
+        results.append(c.cpu())
+    for c in results[1:]:
+        assert torch.equal(c, results[0])
+
+
+def test_identity_weight_copies_every_chunk():
+    W, r, S, Q, K = 4, 0, 128, 2, 256
+    _say("identity")
+    w, d, perm, chunks, order = _small_ag(W, r, S, Q, "ring", K, K, "bf16", "bf16")
+    eye = si.Matrix(values=np.eye(K, dtype=np.float32), dtype="bf16",
+                    bits=si.f32_to_bf16_bits(np.eye(K, dtype=np.float32)))
+    s = csg.Schedule.uniform(W, r, S, Q, "ring")
+    plan = csg.Plan("ag", W * S, K, K, "bf16", "bf16", s, cfg={"timeout_ms": 1000})
+    c, _ = run_ag(plan, chunks, d.A, eye, "bf16")
+    assert np.array_equal(c.cpu().numpy().view(np.uint16), d.A.bits)
+
+
+def test_poisoned_landing_in_cache_never_reaches_output():
+    """Remote rows of the landing buffer hold NaN and were just read (so their lines sit
+    in the caches); a tile that read them before its flag, or through a stale line,
+    would put NaN into C."""
+    W, r, S, Q, N, K = 4, 0, 256, 4, 768, 512
+    _say("poison through cache")
+    w, d, perm, chunks, order = _small_ag(W, r, S, Q, "ring", N, K, "bf16", "bf16")
+    s = csg.Schedule.uniform(W, r, S, Q, "ring")
+    plan = csg.Plan("ag", W * S, N, K, "bf16", "bf16", s, cfg={"timeout_ms": 1000})
+    R = oracle.ag_gemm(d.A.device_array, d.B.device_array, chunks, order)
+    for it in range(3):
+        c, _ = run_ag(plan, chunks, d.A, d.B, "bf16", poison_remote=True, touch_remote=True)
+        assert_close(out_to_f64(c, "bf16"), R, 2e-2, "poison iteration %d" % it)
+
+
+def test_repeated_calls_reuse_the_plan():
+    W, r, S, Q, N, K = 4, 2, 256, 2, 512, 256
+    _say("repeated calls")
+    w, d, perm, chunks, order = _small_ag(W, r, S, Q, "swizzle1d", N, K, "bf16", "bf16")
+    s = csg.Schedule.uniform(W, r, S, Q, "swizzle1d")
+    plan = csg.Plan("ag", W * S, N, K, "bf16", "bf16", s, cfg={"timeout_ms": 1000})
+    R = oracle.ag_gemm(d.A.device_array, d.B.device_array, chunks, order)
+    c, _ = run_ag(plan, chunks, d.A, d.B, "bf16", repeats=5)
+    assert_close(out_to_f64(c, "bf16"), R, 2e-2, "after 5 calls")
+
+
+RS_SMALL = [
+    (4, 1, 256, 2, 512, 320, "bf16", "bf16"),
+    (3, 0, 100, 2, 200, 96, "f32", "f32"),        # ragged, straddling
+    (8, 5, 64, 1, 256, 128, "bf16", "bf16"),      # 4 chunks per tile row: tiles signal several chunks
+]
+
+
+@pytest.mark.parametrize("case", RS_SMALL, ids=lambda c: "W%d-r%d-S%d-Q%d-N%d-K%d-%s-%s" % c)
+@pytest.mark.parametrize("mode", ["overlap", "compute_only"])
+def test_rs_small_parity(case, mode):
+    W, r, S, Q, N, K, dtype, out_dtype = case
+    _say("rs small %s mode=%s" % (case, mode))
+    w = si.Workload(103, "rs", "rs", M=W * S, N=N, K=K, dtype=dtype, out_dtype=out_dtype, dist="normal", world=W,
+                    rank=r, shard_rows=S, chunks_per_shard=Q, order="rs_ring")
+    d = si.draw(w)
+    chunks, order = oracle.uniform_schedule(W, r, S, Q, "rs_ring")
+    s = csg.Schedule.uniform(W, r, S, Q, "rs_ring")
+    plan = csg.Plan("rs", W * S, N, K, dtype, out_dtype, s, cfg={"timeout_ms": 1000})
+    c, out = run_rs(plan, d.A, d.B, out_dtype, mode=mode)
+    R, Rout, log = oracle.gemm_rs(d.A.device_array, d.B.device_array, chunks, order)
+    G = out_to_f64(c, out_dtype)
+    assert_close(G, R, tol_for(out_dtype, dtype), "rs C")
+    O = out_to_f64(out, out_dtype)
+    for ch in chunks:
+        rows = slice(ch.row_begin, ch.row_end)
+        if ch.is_local or mode == "compute_only":
+            assert (O[rows] == 0).all()                  # never sent
+        else:
+            assert np.array_equal(O[rows], G[rows])      # copy-out of the finished C rows (C was NaN before)
+
+
+def test_grouped_small_parity_with_empty_segments_and_partial_tiles():
+    _say("grouped small")
+    W, E, N, K = 4, 3, 264, 256
+    counts = np.array([[70, 0, 5], [0, 3, 1], [130, 0, 0], [1, 2, 300]], dtype=np.int64)
+    chunks, order, gr = oracle.grouped_schedule(W, 1, counts)
+    M = int(sum(gr))
+    X = si.draw_matrix(104, 0, 0, (M, K), "normal", "bf16")
+    B = si.draw_matrix(104, 1, 0, (E, N, K), "normal", "bf16")
+    s = csg.Schedule.grouped(W, 1, counts)
+    plan = csg.Plan("grouped", M, N, K, "bf16", "bf16", s, group_rows=gr, cfg={"timeout_ms": 1000})
+    c, _ = run_ag(plan, chunks, X, B, "bf16")
+    R = oracle.grouped_gemm(X.device_array, B.device_array, chunks, order)
+    assert_close(out_to_f64(c, "bf16"), R, 2e-2, "grouped small")
+
+
+def test_withheld_chunk_times_out_and_plan_recovers():
+    """The host releases the last remote chunk long after the kernel's (tiny) wait bound,
+    so the kernel must give up with a timeout that names that chunk, and exit normally."""
+    W, r, S, Q, N, K = 2, 0, 256, 2, 256, 128
+    _say("withheld chunk")
+    w, d, perm, chunks, order = _small_ag(W, r, S, Q, "ring", N, K, "bf16", "bf16")
+    s = csg.Schedule.uniform(W, r, S, Q, "ring")
+    plan = csg.Plan("ag", W * S, N, K, "bf16", "bf16", s, cfg={"timeout_ms": 20})
+    plan.set_copy_delays([0.0, 300000.0])            # second remote chunk 300 ms late
+    with pytest.raises(csg.CsgError) as ei:
+        run_ag(plan, chunks, d.A, d.B, "bf16")
+    assert ei.value.status == csg.CSG_ERR_TIMEOUT
+    assert ei.value.diag.chunk == order[-1]
+    torch.cuda.synchronize()
+    plan.set_copy_delays(None)
+    c, _ = run_ag(plan, chunks, d.A, d.B, "bf16")
+    R = oracle.ag_gemm(d.A.device_array, d.B.device_array, chunks, order)
+    assert_close(out_to_f64(c, "bf16"), R, 2e-2, "after recovery")
+
+
+# ---------------------------------------------------------------------------------
+# Full-size workloads, sampled rows, in the benchmark's launch configuration
+# ---------------------------------------------------------------------------------
+def _full(cfg_id):
+    w = si.WORKLOADS[cfg_id]
+    d = si.draw(w)
+    if w.op == "grouped":
+        chunks, order, gr = oracle.grouped_schedule(w.world, w.rank, d.counts)
+        s = csg.Schedule.grouped(w.world, w.rank, d.counts)
+        return w, d, chunks, order, s, gr
+    chunks, order = oracle.uniform_schedule(w.world, w.rank, w.shard_rows, w.chunks_per_shard, w.order, d.perm)
+    s = csg.Schedule.uniform(w.world, w.rank, w.shard_rows, w.chunks_per_shard, w.order, d.perm)
+    return w, d, chunks, order, s, None
+
+
+@pytest.mark.parametrize("cfg_id", [1, 2, 3, 4, 5])
+def test_full_size_workload_sampled(cfg_id):
+    w, d, chunks, order, s, gr = _full(cfg_id)
+    _say("full size %s" % w.name)
+    plan = csg.Plan(w.op, w.M, w.N, w.K, w.dtype, w.out_dtype, s, group_rows=gr)
+    if d.delays_us is not None:
+        plan.set_copy_delays(d.delays_us)
+    rows = sample_rows(chunks, extra=24, seed=cfg_id, M=w.M) if w.M > 256 else list(range(w.M))
+    tol = tol_for(w.out_dtype, w.dtype)
+    if w.op == "rs":
+        c, out = run_rs(plan, d.A, d.B, w.out_dtype)
+        R, _, _ = oracle.gemm_rs(d.A.device_array, d.B.device_array, chunks, order, row_subset=rows)
+        G = out_to_f64(c[rows], w.out_dtype)
+        assert_close(G, R[rows], tol, w.name)
+        O = out_to_f64(out[rows], w.out_dtype)
+        remote = np.array([not chunks[next(i for i, ch in enumerate(chunks) if ch.row_begin <= r < ch.row_end)].is_local
+                           for r in rows])
+        assert np.array_equal(O[remote], G[remote])
+        return
+    c, _ = run_ag(plan, chunks, d.A, d.B, w.out_dtype)
+    if w.op == "grouped":
+        R = oracle.grouped_gemm(d.A.device_array, d.B.device_array, chunks, order, row_subset=rows)
+    else:
+        R = oracle.ag_gemm(d.A.device_array, d.B.device_array, chunks, order, row_subset=rows)
+    assert_close(out_to_f64(c[rows], w.out_dtype), R[rows], tol, w.name)
