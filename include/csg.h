@@ -88,7 +88,11 @@ typedef struct {
  *   num_workgroups  persistent grid size G (0 = one per co-resident slot)
  *   copy_engines    SDMA engines the chunk copies are spread over (0 = every engine the
  *                   device offers for device-to-device copies)
- *   timeout_ms      bound on every wait (kernel flag polls, host waits); 0 = 2000 */
+ *   timeout_ms      bound on every wait (kernel flag polls, host waits); 0 = 2000
+ *   split_k         K-slices per tile (0 or 1 = none): the slices of a tile run on different
+ *                   workgroups and the last one to finish adds the fp32 partial sums in slice
+ *                   order, so the result depends on split_k but not on timing; a larger value
+ *                   shortens the work left after the last chunk lands (and the first emission) */
 typedef struct {
     int32_t bm, bn, bk;
     int32_t intra_order;
@@ -96,6 +100,7 @@ typedef struct {
     int32_t num_workgroups;
     int32_t copy_engines;
     int32_t timeout_ms;
+    int32_t split_k;
 } csg_plan_cfg;
 
 typedef struct csg_schedule csg_schedule;

@@ -66,7 +66,8 @@ class csg_chunk(ctypes.Structure):
 class csg_plan_cfg(ctypes.Structure):
     _fields_ = [("bm", ctypes.c_int32), ("bn", ctypes.c_int32), ("bk", ctypes.c_int32),
                 ("intra_order", ctypes.c_int32), ("tile_dispatch", ctypes.c_int32),
-                ("num_workgroups", ctypes.c_int32), ("copy_engines", ctypes.c_int32), ("timeout_ms", ctypes.c_int32)]
+                ("num_workgroups", ctypes.c_int32), ("copy_engines", ctypes.c_int32), ("timeout_ms", ctypes.c_int32),
+                ("split_k", ctypes.c_int32)]
 
 
 class csg_plan_info(ctypes.Structure):

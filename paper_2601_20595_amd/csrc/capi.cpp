@@ -107,6 +107,11 @@ struct csg_plan {
   int32_t* d_list_ids = nullptr;
   int32_t* d_raster = nullptr;
   int32_t* d_need = nullptr;
+  int32_t* d_list_begin = nullptr;     // [kXcdLists + 1] per-die sub-list bounds (in units)
+  float* d_ws = nullptr;               // split-K partial sums
+  uint32_t* d_slot_count = nullptr;    // split-K finished slices per tile
+  int32_t split = 1;                   // K-slices per tile
+  int32_t n_units = 0;                 // entries of the execution list
   uint32_t* d_flags = nullptr;         // fine-grained device memory: [n_chunks] ready flags
   uint32_t* d_epoch_table = nullptr;   // [kEpochTable], entry i == i: source of the flag copies
   uint32_t* d_counters = nullptr;
@@ -149,6 +154,8 @@ void free_plan_device(csg_plan* p) {
     if (e) (void)hipEventSynchronize(e);
   for (void* ptr : {static_cast<void*>(p->d_tiles), static_cast<void*>(p->d_list_ptr),
                     static_cast<void*>(p->d_list_ids), static_cast<void*>(p->d_raster), static_cast<void*>(p->d_need),
+                    static_cast<void*>(p->d_list_begin), static_cast<void*>(p->d_ws),
+                    static_cast<void*>(p->d_slot_count),
                     static_cast<void*>(p->d_flags), static_cast<void*>(p->d_epoch_table),
                     static_cast<void*>(p->d_counters), static_cast<void*>(p->d_ticket), static_cast<void*>(p->d_diag),
                     static_cast<void*>(p->d_scratch)})
@@ -173,20 +180,52 @@ csg_status setup_device(csg_plan* p) {
   const csg::TileMap& m = p->map;
   const int32_t n_tiles = m.n_tiles();
   const int32_t nN = m.n_tiles_n;
-  std::vector<csg::TileDesc> tiles(n_tiles);
-  std::vector<int32_t> lptr(n_tiles + 1, 0), lids, raster(n_tiles);
-  for (int32_t i = 0; i < n_tiles; ++i) {
-    const int32_t t = m.order[i];
-    const csg::RowTile& rt = m.row_tiles[t / nN];
-    tiles[i] = {static_cast<int32_t>(rt.row_begin), static_cast<int32_t>(rt.row_end), t % nN, rt.group};
-    raster[i] = t;
-    for (int32_t q = m.tile_ptr[t]; q < m.tile_ptr[t + 1]; ++q) {
-      const int32_t c = m.tile_chunks[q];
-      // consumers wait only for chunks that have to arrive; producers signal every chunk
-      if (!p->consumer() || !p->sched.chunks[c].is_local) lids.push_back(c);
+  // execution list: the chunk-ordered tile list split into one sub-list per die, a
+  // tile going to die (row-tile index mod dies) so that tiles sharing A rows share
+  // an L2; each sub-list keeps the chunk order (static dispatch uses the plain list)
+  std::vector<int32_t> exec_order;
+  std::vector<int32_t> list_begin(csg::kXcdLists + 1, 0);
+  if (p->cfg.tile_dispatch == 2) {
+    exec_order = m.order;
+    list_begin.assign(csg::kXcdLists + 1, n_tiles);
+    list_begin[0] = 0;
+  } else {
+    for (int x = 0; x < csg::kXcdLists; ++x) {
+      list_begin[x] = static_cast<int32_t>(exec_order.size());
+      for (int32_t t : m.order)
+        if ((t / nN) % csg::kXcdLists == x) exec_order.push_back(t);
     }
-    lptr[i + 1] = static_cast<int32_t>(lids.size());
+    list_begin[csg::kXcdLists] = static_cast<int32_t>(exec_order.size());
   }
+  // work units: every tile, split into `split` K-slices (consecutive units of one tile)
+  const int32_t KT = static_cast<int32_t>(p->K / p->cfg.bk);
+  const int32_t split = std::max(1, std::min(p->cfg.split_k, KT));
+  p->split = split;
+  const int32_t n_units = n_tiles * split;
+  std::vector<csg::TileDesc> tiles;
+  tiles.reserve(n_units);
+  std::vector<int32_t> lptr(1, 0), lids, raster;
+  std::vector<int32_t> unit_begin(csg::kXcdLists + 1, 0);
+  for (int x = 0; x <= csg::kXcdLists; ++x) unit_begin[x] = list_begin[x] * split;  // tiles -> units
+  for (int32_t i = 0; i < n_tiles; ++i) {
+    const int32_t t = exec_order[i];
+    const csg::RowTile& rt = m.row_tiles[t / nN];
+    for (int32_t sl = 0; sl < split; ++sl) {
+      const int32_t k0 = static_cast<int32_t>(static_cast<int64_t>(KT) * sl / split);
+      const int32_t k1 = static_cast<int32_t>(static_cast<int64_t>(KT) * (sl + 1) / split);
+      tiles.push_back({static_cast<int32_t>(rt.row_begin), static_cast<int32_t>(rt.row_end), t % nN, rt.group, k0, k1,
+                       split > 1 ? t : -1, sl | (split << 16)});
+      raster.push_back(t);
+      for (int32_t q = m.tile_ptr[t]; q < m.tile_ptr[t + 1]; ++q) {
+        const int32_t c = m.tile_chunks[q];
+        // consumers wait only for chunks that have to arrive; producers signal every chunk
+        if (!p->consumer() || !p->sched.chunks[c].is_local) lids.push_back(c);
+      }
+      lptr.push_back(static_cast<int32_t>(lids.size()));
+    }
+  }
+  list_begin = unit_begin;
+  p->n_units = n_units;
   std::vector<int32_t> need(p->n_chunks());
   for (int32_t c = 0; c < p->n_chunks(); ++c) need[c] = m.chunk_ptr[c + 1] - m.chunk_ptr[c];
   std::vector<uint32_t> table(kEpochTable);
@@ -198,12 +237,19 @@ csg_status setup_device(csg_plan* p) {
   if ((st = upload(&p->d_raster, raster)) != CSG_OK) return st;
   if ((st = upload(&p->d_need, need)) != CSG_OK) return st;
   if ((st = upload(&p->d_epoch_table, table)) != CSG_OK) return st;
+  if ((st = upload(&p->d_list_begin, list_begin)) != CSG_OK) return st;
   const size_t nflag = static_cast<size_t>(std::max(p->n_chunks(), 1));
   CSG_HIP(hipExtMallocWithFlags(reinterpret_cast<void**>(&p->d_flags), nflag * 4, hipDeviceMallocFinegrained));
   CSG_HIP(hipMemset(p->d_flags, 0, nflag * 4));
   CSG_HIP(hipMalloc(&p->d_counters, nflag * 4));
   CSG_HIP(hipMemset(p->d_counters, 0, nflag * 4));
-  CSG_HIP(hipMalloc(&p->d_ticket, 4));
+  CSG_HIP(hipMalloc(&p->d_ticket, csg::kXcdLists * 4));
+  if (split > 1) {
+    const size_t ws_bytes = static_cast<size_t>(n_tiles) * split * p->cfg.bm * p->cfg.bn * sizeof(float);
+    CSG_HIP(hipMalloc(&p->d_ws, ws_bytes));
+    CSG_HIP(hipMalloc(&p->d_slot_count, static_cast<size_t>(n_tiles) * 4));
+    CSG_HIP(hipMemset(p->d_slot_count, 0, static_cast<size_t>(n_tiles) * 4));
+  }
   CSG_HIP(hipMalloc(&p->d_diag, sizeof(csg::DeviceDiag)));
   CSG_HIP(hipMemset(p->d_diag, 0, sizeof(csg::DeviceDiag)));
   CSG_HIP(hipHostMalloc(&p->h_out_flags, nflag * 4, hipHostMallocMapped | hipHostMallocCoherent));
@@ -287,7 +333,7 @@ csg_status begin_call(csg_plan* p, csg_mode mode, hipStream_t compute, CallState
   p->host_diag = csg_diag{0, -1, -1, 0, p->epoch, 0};
   CSG_HIP(csg::launch_prologue(p->d_flags, p->n_chunks(), p->epoch, mode == CSG_MODE_COMPUTE_ONLY ? 1 : 0,
                                cs->wrapped ? 1 : 0, p->consumer() ? nullptr : p->d_counters, p->d_ticket, p->d_diag,
-                               compute));
+                               p->d_slot_count, p->split > 1 ? p->map.n_tiles() : 0, compute));
   CSG_HIP(hipEventRecord(p->ev_prologue, compute));
   p->kernel_pending[p->epoch & 1] = false;
   return CSG_OK;
@@ -342,10 +388,13 @@ csg_status launch_gemm(csg_plan* p, const void* A, const void* B, void* C, hipSt
   a.need = p->d_need;
   a.out_flags = p->h_out_flags_dev;
   a.ticket = p->d_ticket;
+  a.list_begin = p->d_list_begin;
   a.diag = p->d_diag;
   a.timeout_ticks = static_cast<uint64_t>(p->cfg.timeout_ms) * 100000ull;  // 100 MHz wall clock
   a.epoch = p->epoch;
-  a.n_tiles = p->map.n_tiles();
+  a.n_tiles = p->n_units;
+  a.ws = p->d_ws;
+  a.slot_count = p->d_slot_count;
   a.n_chunks = p->n_chunks();
   a.dynamic_ticket = p->cfg.tile_dispatch == 2 ? 0 : 1;
   CSG_HIP(csg::launch_chunk_gemm(p->key, a, p->grid, compute));
@@ -539,7 +588,9 @@ csg_status csg_plan_create(csg_op op, int64_t M, int64_t N, int64_t K, csg_dtype
   if (c.bn == 0) c.bn = bf16 ? 256 : 64;
   if (c.bk == 0) c.bk = bf16 ? 64 : 16;
   if (c.timeout_ms == 0) c.timeout_ms = 2000;
+  if (c.split_k == 0) c.split_k = 1;
   if (c.bm < 1 || c.bn < 1 || c.bk < 1 || c.copy_engines < 0 || c.copy_engines > 32 || c.timeout_ms < 1 ||
+      c.split_k < 1 || c.split_k > 64 ||
       c.num_workgroups < 0 || c.tile_dispatch < 0 || c.tile_dispatch > 2 || c.intra_order != 0)
     return fail(CSG_ERR_INVALID, "bad plan configuration");
 

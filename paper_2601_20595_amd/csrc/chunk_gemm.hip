@@ -15,10 +15,9 @@
 // Main loops (256 threads = 2 x 2 waves, each wave a (BM/2) x (BN/2) sub-tile of
 // 32 x 32 MFMA blocks):
 //   bf16: v_mfma_f32_32x32x16_bf16; tiles stream HBM -> LDS with buffer_load ... lds
-//         (no register staging), double-buffered; LDS rows are 128 bytes and the
-//         16-byte vectors of row r are stored at vector index (v ^ (r & 7)), which
-//         keeps both the DMA writes and the ds_read_b128 fragment reads free of bank
-//         conflicts.
+//         (no register staging), double-buffered; LDS rows are 128 bytes with an XOR
+//         swizzle of their 16-byte vectors that keeps both the DMA writes and the
+//         ds_read_b128 fragment reads free of bank conflicts.
 //   fp32: v_mfma_f32_32x32x2_f32 with register-staged, padded LDS tiles.
 // The MFMA takes the B fragment as its first operand, so each lane ends up with
 // four runs of four consecutive output columns of one output row, which the
@@ -47,10 +46,16 @@ __device__ __forceinline__ uint32_t load_flag(const uint32_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
+// Buffer resource over [base, base + bytes). Callers pass workgroup-uniform values;
+// readfirstlane keeps the resource in SGPRs, where buffer instructions need it.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
   const int64_t cap = 0x7fffffff;
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, static_cast<int>(bytes < cap ? bytes : cap),
-                                           kBufferDword3);
+  const uint64_t p = reinterpret_cast<uint64_t>(base);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(p));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(p >> 32));
+  const int n = __builtin_amdgcn_readfirstlane(static_cast<int>(bytes < cap ? bytes : cap));
+  void* ub = reinterpret_cast<void*>((static_cast<uint64_t>(hi) << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(ub, 0, n, kBufferDword3);
 }
 
 // Waits (thread 0 only) until every listed chunk is ready. Returns 1 if a chunk was
@@ -85,87 +90,162 @@ __device__ int wait_chunks(const GemmArgs& a, int pos, uint32_t* ready_bits) {
   return fresh;
 }
 
+// Next execution position for a workgroup on die `xcd` (thread 0 only): the next
+// entry of that die's sub-list, else of the following dies' sub-lists; n_tiles when
+// every sub-list is exhausted.
+__device__ int next_tile(const GemmArgs& a, uint32_t xcd) {
+  for (int d = 0; d < kXcdLists; ++d) {
+    const int x = static_cast<int>((xcd + d) % kXcdLists);
+    const int len = a.list_begin[x + 1] - a.list_begin[x];
+    if (len <= 0) continue;
+    if (__hip_atomic_load(a.ticket + x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= static_cast<uint32_t>(len))
+      continue;
+    const uint32_t t = atomicAdd(a.ticket + x, 1u);
+    if (t < static_cast<uint32_t>(len)) return a.list_begin[x] + static_cast<int>(t);
+  }
+  return a.n_tiles;
+}
+
 // Geometry of one output tile as seen by the main loops.
+// Ab and Bb point at the unit's first K element of the tile's first row, so a main
+// loop reads K steps 0 .. nk-1 of its own unit; the byte ranges end at the last valid
+// row's end and bound every load.
 struct TileGeom {
-  const void* Ab;     // first row of the tile in A
-  const void* Bb;     // first row (output column) of the tile in B
-  int64_t K;
+  const void* Ab;     // A[row_begin][kt_begin * BK]
+  const void* Bb;     // B[col0][kt_begin * BK] (of the tile's group)
+  int64_t K;          // row pitch of A and B in elements
+  int64_t abytes;     // readable bytes from Ab
+  int64_t bbytes;     // readable bytes from Bb
   int arows;          // valid A rows (output rows) of the tile
   int brows;          // valid B rows (output columns) of the tile
+  int nk;             // K steps of this unit
 };
 
 // ---------------------------------------------------------------------------------
 // bf16 main loop: LDS DMA, XOR-swizzled 128-byte rows, BK = 64
 // ---------------------------------------------------------------------------------
+// One 16-byte-per-lane DMA from a buffer resource into LDS at lds_off + 16 * lane,
+// reading byte offset vbase + sadd (vbase per lane, sadd uniform). Issued as inline
+// asm so the compiler neither inserts a wait for it in front of every LDS read (it
+// cannot tell that the reads target the other stage) nor hoists one offset register
+// per load out of the tile loop; the whole offset sits in the VGPR operand, which the
+// buffer range check covers. M0 is saved and restored around the load.
+__device__ __forceinline__ void dma16(const __amdgpu_buffer_rsrc_t& rs, uint32_t lds_off, int vbase, int sadd) {
+  uint32_t saved;
+  int voff;
+  asm volatile(
+      "v_add_u32 %1, %3, %4\n\t"
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "buffer_load_dwordx4 %1, %5, 0 offen lds\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved), "=&v"(voff)
+      : "s"(lds_off), "s"(sadd), "v"(vbase), "s"(rs)
+      : "memory");
+}
+
+__device__ __forceinline__ void wait_dma_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
 template <int BM_, int BN_>
 struct Bf16Loop {
   static constexpr int BM = BM_, BN = BN_, BK = 64;
   static constexpr int WTM = BM / 2, WTN = BN / 2, MI = WTM / 32, NI = WTN / 32;
   static constexpr int ROWB = 128;                           // bytes per LDS row (64 bf16)
   static constexpr int STAGE_A = BM * ROWB, STAGE_B = BN * ROWB;
-  static constexpr int LDS_BYTES = 2 * (STAGE_A + STAGE_B);
+  static constexpr int STAGE = STAGE_A + STAGE_B;
+  static constexpr int LDS_BYTES = 2 * STAGE;
   static constexpr int A_LOADS = BM / 32, B_LOADS = BN / 32;  // wave DMA issues per stage (8 rows each)
   static_assert(BM % 64 == 0 && BN % 64 == 0, "bf16 tiles are multiples of 64");
 
-  // Issue one stage: wave w fills rows [w*BM/4, (w+1)*BM/4) of A and likewise of B.
-  __device__ static void issue(unsigned char* lds, int buf, int kt, const __amdgpu_buffer_rsrc_t& rsA,
-                               const __amdgpu_buffer_rsrc_t& rsB, int64_t K, int wave, int lane) {
-    const int lr = lane >> 3;                       // row inside the 8-row group
-    const int logical = (lane & 7) ^ lr;            // logical vector stored at physical slot lane & 7
-    const int kbyte = kt * BK * 2 + logical * 16;
-    unsigned char* la = lds + buf * (STAGE_A + STAGE_B);
-    unsigned char* lb = la + STAGE_A;
+  // LDS swizzle: logical 16-byte vector v of tile row r sits at physical vector
+  // v ^ swz(r), swz(r) = (r & 7) ^ ((r >> 3) & 1). Any 8 consecutive aligned rows,
+  // and the even and the odd rows of any 16 consecutive aligned rows, get distinct
+  // swizzles, so a ds_read_b128 of one logical vector by 16 lanes on 16 consecutive
+  // rows touches 16 distinct 4-bank groups whether LDS is 32 or 64 banks wide.
+  __device__ static int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
+  // Issue one stage (the BK columns starting at byte kbase of every row): wave w
+  // fills rows [w*BM/4, (w+1)*BM/4) of A and likewise of B. Lane l of an 8-row group
+  // writes LDS slot l (row l/8, physical vector l%8), so it fetches logical vector
+  // (l%8) ^ swz(row) of that row.
+  __device__ static void issue(uint32_t lds_base, int buf, int kbase, const __amdgpu_buffer_rsrc_t& rsA,
+                               const __amdgpu_buffer_rsrc_t& rsB, int K, int wave, int lane) {
+    const int lr = lane >> 3;
+    const int wrow_a = wave * (BM / 4), wrow_b = wave * (BN / 4);
+    const uint32_t la = __builtin_amdgcn_readfirstlane(lds_base + buf * STAGE + wrow_a * ROWB);
+    const uint32_t lb = __builtin_amdgcn_readfirstlane(lds_base + buf * STAGE + STAGE_A + wrow_b * ROWB);
+    // row = group base (a multiple of 8) + lr, so swz(row) = lr ^ ((row >> 3) & 1): the
+    // lane part of the offset only depends on the parity of the 8-row group
+    const int v_even = lr * K * 2 + (((lane & 7) ^ lr) * 16);
+    const int v_odd = lr * K * 2 + (((lane & 7) ^ lr ^ 1) * 16);
 #pragma unroll
     for (int q = 0; q < A_LOADS; ++q) {
-      const int row = wave * (BM / 4) + q * 8;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, (lds_ptr_t)(la + row * ROWB),
-                                               16, static_cast<int>((row + lr) * K * 2) + kbyte, 0, 0, 0);
+      const int g8 = wrow_a + q * 8;
+      dma16(rsA, la + q * 8 * ROWB, ((g8 >> 3) & 1) ? v_odd : v_even, g8 * K * 2 + kbase);
     }
 #pragma unroll
     for (int q = 0; q < B_LOADS; ++q) {
-      const int row = wave * (BN / 4) + q * 8;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsB, (lds_ptr_t)(lb + row * ROWB),
-                                               16, static_cast<int>((row + lr) * K * 2) + kbyte, 0, 0, 0);
+      const int g8 = wrow_b + q * 8;
+      dma16(rsB, lb + q * 8 * ROWB, ((g8 >> 3) & 1) ? v_odd : v_even, g8 * K * 2 + kbase);
     }
   }
 
   __device__ static void run(unsigned char* lds, const TileGeom& g, f32x16 (&acc)[MI][NI], int wave, int lane) {
     const int wm = wave >> 1, wn = wave & 1;
-    const __amdgpu_buffer_rsrc_t rsA = make_rsrc(g.Ab, static_cast<int64_t>(g.arows) * g.K * 2);
-    const __amdgpu_buffer_rsrc_t rsB = make_rsrc(g.Bb, static_cast<int64_t>(g.brows) * g.K * 2);
-    const int KT = static_cast<int>(g.K / BK);
+    const __amdgpu_buffer_rsrc_t rsA = make_rsrc(g.Ab, g.abytes);
+    const __amdgpu_buffer_rsrc_t rsB = make_rsrc(g.Bb, g.bbytes);
+    const int K = static_cast<int>(g.K);
+    const int nk = g.nk;
+    const uint32_t lds_base =
+        __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_ptr_t)lds)));
     const int lrow = lane & 31, lhalf = lane >> 5;
-    // byte offset of this lane's fragment row inside a stage; the vector index is
-    // XORed with (row & 7) == (lane & 7) because every block starts on a multiple of 8
+    // byte offset of this lane's fragment row inside a stage; every fragment block
+    // starts on a multiple of 32 rows, so the row's swizzle is swz(lane % 32)
     const int a_off = (wm * WTM + lrow) * ROWB;
     const int b_off = STAGE_A + (wn * WTN + lrow) * ROWB;
-    const int sw = lane & 7;
+    const int sw = swz(lrow);
 
-    issue(lds, 0, 0, rsA, rsB, g.K, wave, lane);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    bf16x8 fa[2][MI], fb[2][NI];  // fragments of two consecutive k sub-steps
+    auto load_frags = [&](int set, int buf, int ks) {
+      const unsigned char* st = lds + buf * STAGE;
+      const int vec = ((ks * 2 + lhalf) ^ sw) * 16;
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+        fa[set][i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(st + a_off + i * 32 * ROWB + vec));
+#pragma unroll
+      for (int j = 0; j < NI; ++j)
+        fb[set][j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(st + b_off + j * 32 * ROWB + vec));
+    };
+
+    issue(lds_base, 0, 0, rsA, rsB, K, wave, lane);
+    wait_dma_all();
     __syncthreads();
-    for (int kt = 0; kt < KT; ++kt) {
-      const int buf = kt & 1;
-      if (kt + 1 < KT) issue(lds, buf ^ 1, kt + 1, rsA, rsB, g.K, wave, lane);
-      const unsigned char* st = lds + buf * (STAGE_A + STAGE_B);
+    load_frags(0, 0, 0);
+    for (int t = 0; t < nk; ++t) {
+      const int buf = t & 1;
+      if (t + 1 < nk) issue(lds_base, buf ^ 1, (t + 1) * BK * 2, rsA, rsB, K, wave, lane);
 #pragma unroll
       for (int ks = 0; ks < BK / 16; ++ks) {
-        const int vec = ((ks * 2 + lhalf) ^ sw) * 16;
-        bf16x8 af[MI], bfr[NI];
-#pragma unroll
-        for (int i = 0; i < MI; ++i)
-          af[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(st + a_off + i * 32 * ROWB + vec));
-#pragma unroll
-        for (int j = 0; j < NI; ++j)
-          bfr[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(st + b_off + j * 32 * ROWB + vec));
+        const int cur = ks & 1;
+        if (ks + 1 < BK / 16) load_frags(cur ^ 1, buf, ks + 1);  // next sub-step's fragments in flight
 #pragma unroll
         for (int i = 0; i < MI; ++i)
 #pragma unroll
           for (int j = 0; j < NI; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[cur][j], fa[cur][i], acc[i][j], 0, 0, 0);
+        if (ks + 1 < BK / 16) {
+          // interleave the next sub-step's LDS reads with this sub-step's MFMAs
+#pragma unroll
+          for (int q = 0; q < MI + NI; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+          }
+          __builtin_amdgcn_sched_group_barrier(0x008, MI * NI - (MI + NI), 0);
+        }
       }
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      __syncthreads();
+      wait_dma_all();   // the next stage has landed in LDS
+      __syncthreads();  // and every wave is done with this stage
+      if (t + 1 < nk) load_frags(0, buf ^ 1, 0);
     }
   }
 };
@@ -187,9 +267,9 @@ struct F32Loop {
   __device__ static void run(unsigned char* lds, const TileGeom& g, f32x16 (&acc)[MI][NI], int wave, int lane) {
     const int tid = wave * 64 + lane;
     const int wm = wave >> 1, wn = wave & 1;
-    const __amdgpu_buffer_rsrc_t rsA = make_rsrc(g.Ab, static_cast<int64_t>(g.arows) * g.K * 4);
-    const __amdgpu_buffer_rsrc_t rsB = make_rsrc(g.Bb, static_cast<int64_t>(g.brows) * g.K * 4);
-    const int KT = static_cast<int>(g.K / BK);
+    const __amdgpu_buffer_rsrc_t rsA = make_rsrc(g.Ab, g.abytes);
+    const __amdgpu_buffer_rsrc_t rsB = make_rsrc(g.Bb, g.bbytes);
+    const int nk = g.nk;
     const int vrow = tid / (BK / 4), vcol = (tid % (BK / 4)) * 4;
     const int voff = (vrow * static_cast<int>(g.K) + vcol) * 4;
     const int pass_bytes = RPP * static_cast<int>(g.K) * 4;
@@ -214,9 +294,9 @@ struct F32Loop {
     load(0);
     store(0);
     __syncthreads();
-    for (int kt = 0; kt < KT; ++kt) {
-      const int buf = kt & 1;
-      if (kt + 1 < KT) load(kt + 1);
+    for (int t = 0; t < nk; ++t) {
+      const int buf = t & 1;
+      if (t + 1 < nk) load(t + 1);
       const float* sa = reinterpret_cast<const float*>(lds + buf * (STAGE_A + STAGE_B));
       const float* sb = reinterpret_cast<const float*>(lds + buf * (STAGE_A + STAGE_B) + STAGE_A);
 #pragma unroll
@@ -232,7 +312,7 @@ struct F32Loop {
           for (int j = 0; j < NI; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(bfr[j], af[i], acc[i][j], 0, 0, 0);
       }
-      if (kt + 1 < KT) store(buf ^ 1);
+      if (t + 1 < nk) store(buf ^ 1);
       __syncthreads();
     }
   }
@@ -256,11 +336,14 @@ __global__ __launch_bounds__(kThreads, 1) void chunk_gemm(GemmArgs a) {
   const int wm = wave >> 1, wn = wave & 1;
   for (int i = tid; i < kMaxChunks / 32; i += kThreads) ready_bits[i] = 0;
   const int in_bytes = (Loop::BK == 64) ? 2 : 4;
+  uint32_t xcd;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID, 0, 4)" : "=s"(xcd));
+  xcd %= kXcdLists;
 
   for (int iter = 0;; ++iter) {
     __syncthreads();  // everyone is done with s_pos / s_state / LDS of the previous tile
     if (tid == 0) {
-      const int pos = a.dynamic_ticket ? static_cast<int>(atomicAdd(a.ticket, 1u))
+      const int pos = a.dynamic_ticket ? next_tile(a, xcd)
                                        : static_cast<int>(blockIdx.x) + iter * static_cast<int>(gridDim.x);
       int state = 0;
       if (pos < a.n_tiles) {
@@ -271,7 +354,8 @@ __global__ __launch_bounds__(kThreads, 1) void chunk_gemm(GemmArgs a) {
       s_state = state;
     }
     __syncthreads();
-    const int pos = s_pos;
+    // uniform across the workgroup; readfirstlane lets everything derived from it live in SGPRs
+    const int pos = __builtin_amdgcn_readfirstlane(s_pos);
     if (pos >= a.n_tiles || s_state < 0) break;
     // a chunk seen ready for the first time: every wave drops possibly stale cache lines
     if (!kProducer && s_state > 0) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
@@ -283,9 +367,13 @@ __global__ __launch_bounds__(kThreads, 1) void chunk_gemm(GemmArgs a) {
     g.K = a.K;
     g.arows = td.row_end - td.row_begin;
     g.brows = static_cast<int>(bvalid < BN ? bvalid : BN);
-    g.Ab = static_cast<const unsigned char*>(a.A) + static_cast<int64_t>(td.row_begin) * a.K * in_bytes;
+    const int64_t k0 = static_cast<int64_t>(td.kt_begin) * Loop::BK;
+    g.nk = td.kt_end - td.kt_begin;
+    g.Ab = static_cast<const unsigned char*>(a.A) + (static_cast<int64_t>(td.row_begin) * a.K + k0) * in_bytes;
     g.Bb = static_cast<const unsigned char*>(a.B) +
-           (static_cast<int64_t>(td.group) * a.b_group_stride + col0 * a.K) * in_bytes;
+           (static_cast<int64_t>(td.group) * a.b_group_stride + col0 * a.K + k0) * in_bytes;
+    g.abytes = (static_cast<int64_t>(g.arows) * a.K - k0) * in_bytes;
+    g.bbytes = (static_cast<int64_t>(g.brows) * a.K - k0) * in_bytes;
 
     f32x16 acc[MI][NI];
 #pragma unroll
@@ -294,41 +382,79 @@ __global__ __launch_bounds__(kThreads, 1) void chunk_gemm(GemmArgs a) {
       for (int j = 0; j < NI; ++j) acc[i][j] = f32x16{};
     Loop::run(lds, g, acc, wave, lane);
 
-    // epilogue: accumulator element r = 4 * q + t of block (i, j) is output row
-    // (i * 32 + lane % 32) and column (j * 32 + 8 * q + 4 * (lane / 32) + t) of the
-    // wave's sub-tile
-    {
-      const int N32 = static_cast<int>(a.N);
-      const int lrow = lane & 31, lhalf = lane >> 5;
-      const int64_t cbase = static_cast<int64_t>(td.row_begin) * a.N + col0;
+    // Output run (i, j, q) of this thread: accumulator elements 4q..4q+3 of block
+    // (i, j), i.e. output row (i * 32 + lane % 32) and columns (j * 32 + 8q +
+    // 4 * (lane / 32) + 0..3) of the wave's sub-tile.
+    const int N32 = static_cast<int>(a.N);
+    const int lrow = lane & 31, lhalf = lane >> 5;
+    const int64_t cbase = static_cast<int64_t>(td.row_begin) * a.N + col0;
+    auto store_run = [&](int i, int j, int q, const f32x4& f) {
+      const int lr = wm * Loop::WTM + i * 32 + lrow;
+      const int lc = wn * Loop::WTN + j * 32 + 8 * q + 4 * lhalf;
+      if (lr >= g.arows || lc >= g.brows) return;  // N is a multiple of 4: a run is all in or all out
+      const int off = lr * N32 + lc;
+      if constexpr (kOutBf16)  // v_cvt_pk_bf16_f32: round to nearest even (the default rounding mode)
+        *reinterpret_cast<bf16x4*>(static_cast<unsigned short*>(a.C) + cbase + off) = __builtin_convertvector(f, bf16x4);
+      else
+        *reinterpret_cast<f32x4*>(static_cast<float*>(a.C) + cbase + off) = f;
+    };
+
+    const int nslices = td.slice >> 16;
+    if (nslices > 1) {
+      // Split along K: store this slice's partial sums; the slice that finishes its
+      // tile last adds all of them in slice order (so the result does not depend on
+      // which slice finished when) and writes the output from those sums.
+      constexpr int kVecs = MI * NI * 4;                  // 16-byte vectors per thread
+      constexpr int kSliceBytes = kVecs * kThreads * 16;  // one slice of one tile
+      // slice layout: vector v of thread t at byte (v * kThreads + t) * 16; addressed
+      // through a buffer resource so the per-vector offset is a scalar operand
+      const __amdgpu_buffer_rsrc_t rsW =
+          make_rsrc(a.ws + static_cast<int64_t>(td.slot) * nslices * (kSliceBytes / 4),
+                    static_cast<int64_t>(nslices) * kSliceBytes);
+      const int toff = tid * 16;
+      const int mine = (td.slice & 0xffff) * kSliceBytes;
 #pragma unroll
-      for (int i = 0; i < MI; ++i) {
-        const int lr = wm * Loop::WTM + i * 32 + lrow;
-        if (lr >= g.arows) continue;
+      for (int i = 0; i < MI; ++i)
 #pragma unroll
         for (int j = 0; j < NI; ++j)
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            const int lc = wn * Loop::WTN + j * 32 + 8 * q + 4 * lhalf;
-            if (lc >= g.brows) continue;  // N is a multiple of 4: a run is all in or all out
-            const int off = lr * N32 + lc;
-            const f32x16& v = acc[i][j];
-            if constexpr (kOutBf16) {
-              // v_cvt_pk_bf16_f32: round to nearest even (the default rounding mode)
-              const f32x4 f = {v[4 * q + 0], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
-              *reinterpret_cast<bf16x4*>(static_cast<unsigned short*>(a.C) + cbase + off) =
-                  __builtin_convertvector(f, bf16x4);
-            } else {
-              u32x4 pk;
-              pk.x = __float_as_uint(v[4 * q + 0]);
-              pk.y = __float_as_uint(v[4 * q + 1]);
-              pk.z = __float_as_uint(v[4 * q + 2]);
-              pk.w = __float_as_uint(v[4 * q + 3]);
-              *reinterpret_cast<u32x4*>(static_cast<float*>(a.C) + cbase + off) = pk;
-            }
+            const f32x4 f = {acc[i][j][4 * q + 0], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, f), rsW, toff,
+                                                   mine + ((i * NI + j) * 4 + q) * kThreads * 16, 0);
+          }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");  // partials leave this die's L2
+      __syncthreads();
+      if (tid == 0)
+        s_state = (__hip_atomic_fetch_add(a.slot_count + td.slot, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) ==
+                   static_cast<uint32_t>(nslices - 1));
+      __syncthreads();
+      if (!s_state) continue;
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");  // see the other dies' partials
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NI; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int v = ((i * NI + j) * 4 + q) * kThreads * 16;
+            f32x4 sum = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rsW, toff, v, 0));
+            for (int sl = 1; sl < nslices; ++sl)
+              sum += __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rsW, toff, sl * kSliceBytes + v, 0));
+            store_run(i, j, q, sum);
+            __builtin_amdgcn_sched_barrier(0);  // one run at a time keeps register use flat
+          }
+    } else {
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NI; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const f32x4 f = {acc[i][j][4 * q + 0], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+            store_run(i, j, q, f);
             __builtin_amdgcn_sched_barrier(0);  // convert-and-store one run at a time
           }
-      }
     }
 
     if constexpr (kProducer) {
@@ -349,15 +475,17 @@ __global__ __launch_bounds__(kThreads, 1) void chunk_gemm(GemmArgs a) {
 
 __global__ __launch_bounds__(kThreads) void chunk_prologue(uint32_t* flags, int32_t n_chunks, uint32_t epoch,
                                                             int32_t preset_all, int32_t clear_flags, uint32_t* counters,
-                                                            uint32_t* ticket, DeviceDiag* diag) {
+                                                            uint32_t* ticket, DeviceDiag* diag, uint32_t* slot_count,
+                                                            int32_t n_slots) {
   const int tid = threadIdx.x;
+  for (int i = tid; i < n_slots; i += blockDim.x) slot_count[i] = 0u;
   for (int c = tid; c < n_chunks; c += blockDim.x) {
     if (clear_flags || preset_all)
       __hip_atomic_store(flags + c, preset_all ? epoch : 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
     if (counters) counters[c] = 0u;
   }
+  if (tid < kXcdLists) ticket[tid] = 0u;
   if (tid == 0) {
-    *ticket = 0u;
     diag->timed_out = 0u;
     diag->chunk = -1;
     diag->tile = -1;
@@ -437,9 +565,10 @@ hipError_t launch_chunk_gemm(const KernelKey& key, const GemmArgs& args, int32_t
 }
 
 hipError_t launch_prologue(uint32_t* flags, int32_t n_chunks, uint32_t epoch, int32_t preset_all, int32_t clear_flags,
-                           uint32_t* counters, uint32_t* ticket, DeviceDiag* diag, hipStream_t stream) {
+                           uint32_t* counters, uint32_t* ticket, DeviceDiag* diag, uint32_t* slot_count,
+                           int32_t n_slots, hipStream_t stream) {
   hipLaunchKernelGGL(chunk_prologue, dim3(1), dim3(kThreads), 0, stream, flags, n_chunks, epoch, preset_all,
-                     clear_flags, counters, ticket, diag);
+                     clear_flags, counters, ticket, diag, slot_count, n_slots);
   return hipGetLastError();
 }
 

@@ -19,11 +19,16 @@ struct DeviceDiag {
 };
 
 // One entry of the execution-ordered tile list.
+// One work unit of the execution list: a tile, or one K-slice of a tile split along K.
 struct TileDesc {
   int32_t row_begin;  // first output row (global)
   int32_t row_end;    // one past the last valid output row
   int32_t n_tile;     // tile index along N
   int32_t group;      // expert index (grouped GEMM), else 0
+  int32_t kt_begin;   // first K step (units of the tile's BK)
+  int32_t kt_end;     // one past the last K step
+  int32_t slot;       // split tiles: workspace slot (the tile's raster id); -1 if not split
+  int32_t slice;      // split tiles: slice index | (number of slices << 16)
 };
 
 struct GemmArgs {
@@ -40,8 +45,11 @@ struct GemmArgs {
   uint32_t* counters;        // producer: finished tiles per chunk
   const int32_t* need;       // producer: tiles per chunk
   uint32_t* out_flags;       // producer: per-chunk completion flags (host-visible memory)
-  uint32_t* ticket;          // dynamic tile ticket
+  uint32_t* ticket;          // [kXcdLists] tickets, one per tile sub-list
+  const int32_t* list_begin; // [kXcdLists + 1]: sub-list x is positions [list_begin[x], list_begin[x+1])
   DeviceDiag* diag;
+  float* ws;                 // split-K partial sums: [slot][slice][BM * BN] fp32, thread-major
+  uint32_t* slot_count;      // split-K: finished slices per slot
   uint64_t timeout_ticks;    // bound of one flag wait, in 100 MHz wall-clock ticks
   uint32_t epoch;            // a flag is ready when it is >= epoch
   int32_t n_tiles;
@@ -50,6 +58,11 @@ struct GemmArgs {
 };
 
 enum class InType : int32_t { BF16 = 0, F32 = 1 };
+
+// The tile list is split into one sub-list per XCD (accelerator complex die, each
+// with its own L2); a workgroup takes tiles from the sub-list of the die it runs on
+// and steals from the others once its own is exhausted.
+constexpr int kXcdLists = 8;
 
 struct KernelKey {
   InType in;
@@ -66,9 +79,11 @@ int32_t kernel_max_chunks();
 hipError_t kernel_grid(const KernelKey& key, int device, int32_t* grid);
 hipError_t launch_chunk_gemm(const KernelKey& key, const GemmArgs& args, int32_t grid, hipStream_t stream);
 
-// Per-call set-up on the compute stream: clears counters, the ticket and the
-// diagnostics, and pre-sets (compute-only) or clears (epoch wrap) the ready flags.
+// Per-call set-up on the compute stream: clears counters, the tickets, the split-K
+// slot counts and the diagnostics, and pre-sets (compute-only) or clears (epoch
+// wrap) the ready flags.
 hipError_t launch_prologue(uint32_t* flags, int32_t n_chunks, uint32_t epoch, int32_t preset_all, int32_t clear_flags,
-                           uint32_t* counters, uint32_t* ticket, DeviceDiag* diag, hipStream_t stream);
+                           uint32_t* counters, uint32_t* ticket, DeviceDiag* diag, uint32_t* slot_count,
+                           int32_t n_slots, hipStream_t stream);
 
 }  // namespace csg

@@ -204,6 +204,87 @@ def test_withheld_chunk_times_out_and_plan_recovers():
 
 
 # ---------------------------------------------------------------------------------
+# Split-K and static dispatch: the same results, to the same bar
+# ---------------------------------------------------------------------------------
+SPLIT_AG = [
+    # W, r, S, Q, kind, N, K, dtype, out, split, dispatch
+    (4, 0, 300, 2, "ring", 600, 512, "bf16", "bf16", 2, 0),          # 8 K steps, 2 slices, ragged M and N
+    (4, 3, 256, 4, "swizzle1d", 520, 640, "bf16", "f32", 3, 0),      # 10 K steps in 3 uneven slices
+    (3, 1, 100, 2, "ring", 200, 96, "f32", "f32", 4, 0),             # fp32, 6 K steps in 4 slices
+    (2, 1, 512, 1, "permutation", 256, 256, "bf16", "bf16", 8, 0),   # 4 K steps: the split is cut to 4
+    (4, 0, 300, 2, "ring", 600, 512, "bf16", "bf16", 1, 2),          # static dispatch, no split
+    (4, 3, 256, 4, "swizzle1d", 520, 640, "bf16", "bf16", 2, 2),     # static dispatch with split
+]
+
+
+@pytest.mark.parametrize("case", SPLIT_AG, ids=lambda c: "W%d-r%d-S%d-Q%d-%s-N%d-K%d-%s-%s-split%d-disp%d" % c)
+def test_ag_split_k_and_dispatch_parity(case):
+    W, r, S, Q, kind, N, K, dtype, out_dtype, split, disp = case
+    _say("ag split/dispatch %s" % (case,))
+    w, d, perm, chunks, order = _small_ag(W, r, S, Q, kind, N, K, dtype, out_dtype)
+    s = csg.Schedule.uniform(W, r, S, Q, kind, perm)
+    plan = csg.Plan("ag", W * S, N, K, dtype, out_dtype, s,
+                    cfg={"timeout_ms": 1000, "split_k": split, "tile_dispatch": disp})
+    R = oracle.ag_gemm(d.A.device_array, d.B.device_array, chunks, order)
+    c, _ = run_ag(plan, chunks, d.A, d.B, out_dtype)
+    assert_close(out_to_f64(c, out_dtype), R, tol_for(out_dtype, dtype), "ag split")
+    # the slices are added in a fixed order: repeated calls give the same bits
+    c2, _ = run_ag(plan, chunks, d.A, d.B, out_dtype, repeats=3)
+    assert torch.equal(c.cpu(), c2.cpu())
+
+
+@pytest.mark.parametrize("split", [2, 5])
+def test_split_k_integer_inputs_bit_exact(split):
+    W, r, S, Q, N, K = 4, 2, 192, 3, 384, 640
+    _say("integer bit-exact split=%d" % split)
+    w, d, perm, chunks, order = _small_ag(W, r, S, Q, "permutation", N, K, "bf16", "f32", dist="int")
+    s = csg.Schedule.uniform(W, r, S, Q, "permutation", perm)
+    plan = csg.Plan("ag", W * S, N, K, "bf16", "f32", s, cfg={"timeout_ms": 1000, "split_k": split})
+    c, _ = run_ag(plan, chunks, d.A, d.B, "f32")
+    R = oracle.ag_gemm(d.A.device_array, d.B.device_array, chunks, order)
+    assert np.array_equal(out_to_f64(c, "f32"), R)
+
+
+@pytest.mark.parametrize("split", [2, 3])
+def test_rs_split_k_parity(split):
+    """A chunk's flag rises only after the last slice of its last tile has written C."""
+    W, r, S, Q, N, K = 4, 1, 256, 2, 512, 640
+    _say("rs split=%d" % split)
+    w = si.Workload(103, "rs", "rs", M=W * S, N=N, K=K, dtype="bf16", out_dtype="bf16", dist="normal", world=W,
+                    rank=r, shard_rows=S, chunks_per_shard=Q, order="rs_ring")
+    d = si.draw(w)
+    chunks, order = oracle.uniform_schedule(W, r, S, Q, "rs_ring")
+    s = csg.Schedule.uniform(W, r, S, Q, "rs_ring")
+    plan = csg.Plan("rs", W * S, N, K, "bf16", "bf16", s, cfg={"timeout_ms": 1000, "split_k": split})
+    c, out = run_rs(plan, d.A, d.B, "bf16")
+    R, _, _ = oracle.gemm_rs(d.A.device_array, d.B.device_array, chunks, order)
+    G = out_to_f64(c, "bf16")
+    assert_close(G, R, 2e-2, "rs split C")
+    O = out_to_f64(out, "bf16")
+    for ch in chunks:
+        rows = slice(ch.row_begin, ch.row_end)
+        if ch.is_local:
+            assert (O[rows] == 0).all()
+        else:
+            assert np.array_equal(O[rows], G[rows])
+
+
+def test_grouped_split_k_parity():
+    _say("grouped split")
+    W, E, N, K = 4, 3, 264, 512
+    counts = np.array([[70, 0, 5], [0, 3, 1], [130, 0, 0], [1, 2, 300]], dtype=np.int64)
+    chunks, order, gr = oracle.grouped_schedule(W, 2, counts)
+    M = int(sum(gr))
+    X = si.draw_matrix(105, 0, 0, (M, K), "normal", "bf16")
+    B = si.draw_matrix(105, 1, 0, (E, N, K), "normal", "bf16")
+    s = csg.Schedule.grouped(W, 2, counts)
+    plan = csg.Plan("grouped", M, N, K, "bf16", "bf16", s, group_rows=gr, cfg={"timeout_ms": 1000, "split_k": 3})
+    c, _ = run_ag(plan, chunks, X, B, "bf16")
+    R = oracle.grouped_gemm(X.device_array, B.device_array, chunks, order)
+    assert_close(out_to_f64(c, "bf16"), R, 2e-2, "grouped split")
+
+
+# ---------------------------------------------------------------------------------
 # Full-size workloads, sampled rows, in the benchmark's launch configuration
 # ---------------------------------------------------------------------------------
 def _full(cfg_id):
