@@ -242,6 +242,16 @@ csg_status csg_grouped_gemm(csg_plan* p, void* x_landing, const void* x_staging,
  * CSG_ERR_TIMEOUT if a wait expired (details in *out), CSG_OK otherwise. */
 csg_status csg_plan_check(csg_plan* p, csg_diag* out);
 
+/* Durations of the plan's most recent GEMM kernel launches, oldest first: the time
+ * between two timing events the library records on the compute stream right
+ * before and right after each kernel (so it covers the kernel only, not the
+ * prologue or host launch latency; in overlap mode it includes the kernel's
+ * waits for chunks). Up to n values (at most the last 256 launches) are written to
+ * ms_host; *n_out receives how many. Waits for those launches to complete.
+ * CSG_ERR_STATE on a host-only plan, CSG_ERR_INVALID for n < 0 or NULL
+ * pointers. */
+csg_status csg_plan_kernel_times(csg_plan* p, float* ms_host, int32_t n, int32_t* n_out);
+
 /* Waits for the plan's last call, then frees everything the plan owns. */
 void csg_plan_destroy(csg_plan* p);
 

@@ -44,7 +44,8 @@ ABI_FUNCTIONS = (
     "csg_schedule_create", "csg_schedule_uniform", "csg_schedule_grouped", "csg_schedule_info",
     "csg_schedule_get", "csg_schedule_destroy",
     "csg_plan_create", "csg_plan_info_get", "csg_plan_get_map", "csg_plan_set_copy_delays",
-    "csg_ag_gemm", "csg_gemm_rs", "csg_grouped_gemm", "csg_plan_check", "csg_plan_destroy",
+    "csg_ag_gemm", "csg_gemm_rs", "csg_grouped_gemm", "csg_plan_check", "csg_plan_kernel_times",
+    "csg_plan_destroy",
 )
 
 
@@ -113,6 +114,7 @@ def _lib():
         "csg_gemm_rs": ([vp, vp, vp, vp, vp, st, vp, vp], st),
         "csg_grouped_gemm": ([vp, vp, vp, vp, vp, st, vp, vp], st),
         "csg_plan_check": ([vp, P(csg_diag)], st),
+        "csg_plan_kernel_times": ([vp, P(ctypes.c_float), i32, P(i32)], st),
         "csg_plan_destroy": ([vp], None),
     }
     for name, (args, res) in sig.items():
@@ -310,6 +312,15 @@ def csg_plan_check(plan: int) -> csg_diag:
     return d
 
 
+def csg_plan_kernel_times(plan: int, n: int = 256) -> np.ndarray:
+    """Durations (ms) of the plan's last n kernel launches, oldest first."""
+    buf = np.zeros(max(n, 1), dtype=np.float32)
+    got = ctypes.c_int32(0)
+    _check(_lib().csg_plan_kernel_times(plan, buf.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), n,
+                                        ctypes.byref(got)), "csg_plan_kernel_times")
+    return buf[:got.value].copy()
+
+
 def csg_plan_destroy(plan: int) -> None:
     _lib().csg_plan_destroy(plan)
 
@@ -379,6 +390,9 @@ class Plan:
 
     def check(self) -> csg_diag:
         return csg_plan_check(self.handle)
+
+    def kernel_times(self, n: int = 256) -> np.ndarray:
+        return csg_plan_kernel_times(self.handle, n)
 
     def close(self):
         if self.handle:

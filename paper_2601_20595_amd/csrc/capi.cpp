@@ -78,6 +78,7 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 // Epochs run 1 .. kEpochTable - 1; the flag copy of epoch e reads table entry e.
 constexpr uint32_t kEpochTable = 1u << 16;
+constexpr int kTimingRing = 256;  // kernel launches whose durations a plan keeps
 
 }  // namespace
 
@@ -127,6 +128,9 @@ struct csg_plan {
   hipEvent_t ev_copy_in = nullptr;     // the caller's copy stream reached the call
   hipEvent_t ev_prologue = nullptr;    // the prologue finished (waited for on an epoch wrap)
   hipEvent_t ev_kernel_done[2] = {nullptr, nullptr};  // by epoch parity
+  hipEvent_t ev_k0[kTimingRing] = {};  // timing events around each kernel launch (ring)
+  hipEvent_t ev_k1[kTimingRing] = {};
+  uint64_t n_launches = 0;
   hipStream_t aux = nullptr;           // plan-internal transfers (diagnostics)
   csg_diag host_diag{};                // host-side wait failures of the last call
 
@@ -163,6 +167,10 @@ void free_plan_device(csg_plan* p) {
   if (p->h_out_flags) (void)hipHostFree(p->h_out_flags);
   for (hipEvent_t e : {p->ev_copy_in, p->ev_prologue, p->ev_kernel_done[0], p->ev_kernel_done[1]})
     if (e) (void)hipEventDestroy(e);
+  for (int i = 0; i < kTimingRing; ++i) {
+    if (p->ev_k0[i]) (void)hipEventDestroy(p->ev_k0[i]);
+    if (p->ev_k1[i]) (void)hipEventDestroy(p->ev_k1[i]);
+  }
   if (p->aux) (void)hipStreamDestroy(p->aux);
 }
 
@@ -269,6 +277,10 @@ csg_status setup_device(csg_plan* p) {
   CSG_HIP(hipEventCreateWithFlags(&p->ev_copy_in, hipEventDisableTiming));
   CSG_HIP(hipEventCreateWithFlags(&p->ev_prologue, hipEventDisableTiming));
   for (hipEvent_t& e : p->ev_kernel_done) CSG_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+  for (int i = 0; i < kTimingRing; ++i) {
+    CSG_HIP(hipEventCreate(&p->ev_k0[i]));
+    CSG_HIP(hipEventCreate(&p->ev_k1[i]));
+  }
   CSG_HIP(hipStreamCreateWithFlags(&p->aux, hipStreamNonBlocking));
   CSG_HIP(hipDeviceSynchronize());
   return CSG_OK;
@@ -397,7 +409,11 @@ csg_status launch_gemm(csg_plan* p, const void* A, const void* B, void* C, hipSt
   a.slot_count = p->d_slot_count;
   a.n_chunks = p->n_chunks();
   a.dynamic_ticket = p->cfg.tile_dispatch == 2 ? 0 : 1;
+  const int slot = static_cast<int>(p->n_launches % kTimingRing);
+  CSG_HIP(hipEventRecord(p->ev_k0[slot], compute));
   CSG_HIP(csg::launch_chunk_gemm(p->key, a, p->grid, compute));
+  CSG_HIP(hipEventRecord(p->ev_k1[slot], compute));
+  ++p->n_launches;
   CSG_HIP(hipEventRecord(p->ev_kernel_done[p->epoch & 1], compute));
   p->kernel_pending[p->epoch & 1] = true;
   return CSG_OK;
@@ -784,6 +800,23 @@ csg_status csg_plan_check(csg_plan* p, csg_diag* out) {
   if (d.timed_out)
     return fail(CSG_ERR_TIMEOUT, "chunk %d (tile %d) never became ready: flag %u < epoch %u", d.chunk, d.tile,
                 d.observed, d.epoch);
+  return CSG_OK;
+}
+
+csg_status csg_plan_kernel_times(csg_plan* p, float* ms_host, int32_t n, int32_t* n_out) {
+  if (!p || !ms_host || !n_out || n < 0) return fail(CSG_ERR_INVALID, "NULL argument or n < 0");
+  *n_out = 0;
+  if (p->device < 0) return fail(CSG_ERR_STATE, "host-only plan has no kernel launches");
+  DeviceGuard g(p->device);
+  if (g.err != hipSuccess) return hip_fail(g.err, "hipSetDevice");
+  const uint64_t avail = std::min<uint64_t>(p->n_launches, kTimingRing);
+  const int32_t m = static_cast<int32_t>(std::min<uint64_t>(avail, static_cast<uint64_t>(n)));
+  for (int32_t i = 0; i < m; ++i) {
+    const int slot = static_cast<int>((p->n_launches - m + i) % kTimingRing);
+    CSG_HIP(hipEventSynchronize(p->ev_k1[slot]));
+    CSG_HIP(hipEventElapsedTime(&ms_host[i], p->ev_k0[slot], p->ev_k1[slot]));
+  }
+  *n_out = m;
   return CSG_OK;
 }
 

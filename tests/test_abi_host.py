@@ -159,3 +159,5 @@ def test_host_only_plan_cannot_run_and_delays_are_checked():
     assert _status(p.set_copy_delays, [-1.0] * 6) == csg.CSG_ERR_INVALID
     assert _status(p.set_copy_delays, None) == csg.CSG_OK
     assert p.info.num_workgroups == 0
+    assert _status(p.kernel_times, 4) == csg.CSG_ERR_STATE               # nothing ever ran
+    assert _status(p.kernel_times, -1) == csg.CSG_ERR_INVALID
