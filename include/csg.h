@@ -92,7 +92,15 @@ typedef struct {
  *   split_k         K-slices per tile (0 or 1 = none): the slices of a tile run on different
  *                   workgroups and the last one to finish adds the fp32 partial sums in slice
  *                   order, so the result depends on split_k but not on timing; a larger value
- *                   shortens the work left after the last chunk lands (and the first emission) */
+ *                   shortens the work left after the last chunk lands (and the first emission)
+ *   tail_split      K-slices for the tiles on the overlap's critical path: the tiles that
+ *   tail_chunks     read one of the tail_chunks last-arriving chunks (AG, grouped) or write
+ *                   one of the tail_chunks first-emitted chunks (RS); 0 = none. Slices are
+ *                   added as for split_k. A plan with split tiles keeps each tile's slices
+ *                   on one die (they exchange partial sums through its L2), so its
+ *                   num_workgroups, if given, must be a multiple of 8
+ *   trace           1 = the kernel records when each work unit was taken, started and
+ *                   finished (read back with csg_plan_trace); 0 = off */
 typedef struct {
     int32_t bm, bn, bk;
     int32_t intra_order;
@@ -101,6 +109,9 @@ typedef struct {
     int32_t copy_engines;
     int32_t timeout_ms;
     int32_t split_k;
+    int32_t tail_split;
+    int32_t tail_chunks;
+    int32_t trace;
 } csg_plan_cfg;
 
 typedef struct csg_schedule csg_schedule;
@@ -113,15 +124,32 @@ typedef struct {
     int32_t n_tiles_n;      /* tiles along N */
     int32_t num_workgroups; /* persistent grid actually used (0 on a host-only plan) */
     int32_t bm, bn, bk;     /* tile shape actually used */
+    int32_t n_units;        /* work units of the execution list (0 on a host-only plan) */
 } csg_plan_info;
+
+/* One work unit (a tile, or one K-slice of a split tile) of the last kernel run of a
+ * plan with tracing on, in execution-list order. Times are device wall-clock ticks
+ * (100 MHz): when a workgroup took the unit, when the unit's chunk waits were over,
+ * and when the unit finished (its output stored, or its partial sums for a slice
+ * that was not the last). */
+typedef struct {
+    int32_t raster;         /* raster id of the tile */
+    int32_t slice;          /* K-slice index */
+    int32_t n_slices;       /* K-slices of the tile (1 = not split) */
+    int32_t xcd;            /* die the workgroup ran on */
+    int32_t workgroup;      /* workgroup id */
+    int32_t reserved;
+    uint64_t t_take, t_start, t_end;
+} csg_trace_unit;
 
 /* Diagnostics of the last call on a plan (filled by csg_plan_check). */
 typedef struct {
     int32_t timed_out;      /* 1 if a kernel flag wait or a host wait expired */
     int32_t chunk;          /* chunk id waited on, -1 if none */
     int32_t tile;           /* raster id of the tile that waited, -1 if none */
-    uint32_t observed;      /* flag value seen when the wait gave up */
-    uint32_t epoch;         /* epoch the wait needed */
+    uint32_t observed;      /* value seen when the wait gave up (the chunk copy's completion
+                               signal: 1 = not landed) */
+    uint32_t epoch;         /* call number of the plan */
     int32_t reserved;
 } csg_diag;
 
@@ -213,8 +241,8 @@ csg_status csg_plan_set_copy_delays(csg_plan* p, const float* delay_us_host, int
  * simulated peers' shards). The prologue and the persistent kernel are queued on
  * `compute`; then, once the work queued earlier on `copy` and the plan's previous
  * kernel have completed, the calling thread issues, for each remote chunk in
- * arrival order, an SDMA copy staging -> landing followed by an SDMA copy that
- * raises the chunk's flag, and returns when all of them have completed. The
+ * arrival order, an SDMA copy staging -> landing whose completion signal is the
+ * chunk's ready flag, and returns when all of them have completed. The
  * kernel runs tiles in chunk order, each waiting for its chunks. Work queued on
  * `compute` afterwards is ordered after the kernel. Asynchronous failures (a flag
  * wait that timed out) surface through csg_plan_check. CSG_ERR_TIMEOUT if a host
@@ -239,7 +267,9 @@ csg_status csg_grouped_gemm(csg_plan* p, void* x_landing, const void* x_staging,
                             void* copy_stream);
 
 /* Waits for the plan's last call to complete and reports its diagnostics.
- * CSG_ERR_TIMEOUT if a wait expired (details in *out), CSG_OK otherwise. */
+ * CSG_ERR_TIMEOUT if a wait expired (details in *out); CSG_ERR_STATE if the kernel
+ * finished without running every work unit (which only a grid that leaves a die
+ * without workgroups can cause); CSG_OK otherwise. */
 csg_status csg_plan_check(csg_plan* p, csg_diag* out);
 
 /* Durations of the plan's most recent GEMM kernel launches, oldest first: the time
@@ -251,6 +281,12 @@ csg_status csg_plan_check(csg_plan* p, csg_diag* out);
  * CSG_ERR_STATE on a host-only plan, CSG_ERR_INVALID for n < 0 or NULL
  * pointers. */
 csg_status csg_plan_kernel_times(csg_plan* p, float* ms_host, int32_t n, int32_t* n_out);
+
+/* Copies the trace of the plan's last kernel run (plan created with cfg.trace = 1)
+ * into units_host[0..n): at most n units, *n_out receives how many. Waits for the
+ * kernel. CSG_ERR_STATE if the plan does not trace or never ran a kernel,
+ * CSG_ERR_INVALID for NULL pointers or n < 0. */
+csg_status csg_plan_trace(csg_plan* p, csg_trace_unit* units_host, int32_t n, int32_t* n_out);
 
 /* Waits for the plan's last call, then frees everything the plan owns. */
 void csg_plan_destroy(csg_plan* p);

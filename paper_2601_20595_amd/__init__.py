@@ -45,7 +45,7 @@ ABI_FUNCTIONS = (
     "csg_schedule_get", "csg_schedule_destroy",
     "csg_plan_create", "csg_plan_info_get", "csg_plan_get_map", "csg_plan_set_copy_delays",
     "csg_ag_gemm", "csg_gemm_rs", "csg_grouped_gemm", "csg_plan_check", "csg_plan_kernel_times",
-    "csg_plan_destroy",
+    "csg_plan_trace", "csg_plan_destroy",
 )
 
 
@@ -68,13 +68,20 @@ class csg_plan_cfg(ctypes.Structure):
     _fields_ = [("bm", ctypes.c_int32), ("bn", ctypes.c_int32), ("bk", ctypes.c_int32),
                 ("intra_order", ctypes.c_int32), ("tile_dispatch", ctypes.c_int32),
                 ("num_workgroups", ctypes.c_int32), ("copy_engines", ctypes.c_int32), ("timeout_ms", ctypes.c_int32),
-                ("split_k", ctypes.c_int32)]
+                ("split_k", ctypes.c_int32), ("tail_split", ctypes.c_int32), ("tail_chunks", ctypes.c_int32),
+                ("trace", ctypes.c_int32)]
 
 
 class csg_plan_info(ctypes.Structure):
     _fields_ = [("n_tiles", ctypes.c_int32), ("n_chunks", ctypes.c_int32), ("nnz", ctypes.c_int32),
                 ("n_tiles_n", ctypes.c_int32), ("num_workgroups", ctypes.c_int32), ("bm", ctypes.c_int32),
-                ("bn", ctypes.c_int32), ("bk", ctypes.c_int32)]
+                ("bn", ctypes.c_int32), ("bk", ctypes.c_int32), ("n_units", ctypes.c_int32)]
+
+
+class csg_trace_unit(ctypes.Structure):
+    _fields_ = [("raster", ctypes.c_int32), ("slice", ctypes.c_int32), ("n_slices", ctypes.c_int32),
+                ("xcd", ctypes.c_int32), ("workgroup", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("t_take", ctypes.c_uint64), ("t_start", ctypes.c_uint64), ("t_end", ctypes.c_uint64)]
 
 
 class csg_diag(ctypes.Structure):
@@ -115,6 +122,7 @@ def _lib():
         "csg_grouped_gemm": ([vp, vp, vp, vp, vp, st, vp, vp], st),
         "csg_plan_check": ([vp, P(csg_diag)], st),
         "csg_plan_kernel_times": ([vp, P(ctypes.c_float), i32, P(i32)], st),
+        "csg_plan_trace": ([vp, P(csg_trace_unit), i32, P(i32)], st),
         "csg_plan_destroy": ([vp], None),
     }
     for name, (args, res) in sig.items():
@@ -321,6 +329,18 @@ def csg_plan_kernel_times(plan: int, n: int = 256) -> np.ndarray:
     return buf[:got.value].copy()
 
 
+def csg_plan_trace(plan: int, n: int) -> np.ndarray:
+    """Trace of the plan's last kernel run: a structured array with fields raster,
+    slice, n_slices, xcd, workgroup, t_take, t_start, t_end (100 MHz ticks)."""
+    buf = (csg_trace_unit * max(n, 1))()
+    got = ctypes.c_int32(0)
+    _check(_lib().csg_plan_trace(plan, buf, n, ctypes.byref(got)), "csg_plan_trace")
+    dt = np.dtype([("raster", np.int32), ("slice", np.int32), ("n_slices", np.int32), ("xcd", np.int32),
+                   ("workgroup", np.int32), ("reserved", np.int32), ("t_take", np.uint64), ("t_start", np.uint64),
+                   ("t_end", np.uint64)])
+    return np.frombuffer(bytes(buf), dtype=dt, count=got.value).copy()
+
+
 def csg_plan_destroy(plan: int) -> None:
     _lib().csg_plan_destroy(plan)
 
@@ -393,6 +413,9 @@ class Plan:
 
     def kernel_times(self, n: int = 256) -> np.ndarray:
         return csg_plan_kernel_times(self.handle, n)
+
+    def trace(self) -> np.ndarray:
+        return csg_plan_trace(self.handle, self.info.n_units)
 
     def close(self):
         if self.handle:

@@ -4,11 +4,12 @@
 //
 // Copy-engine realization (Section 5.2, realization (1): copy engine with
 // global-memory signals). Every chunk copy goes straight to an SDMA engine through
-// the HSA runtime (sdma.cpp), consecutive chunks on consecutive engines; a chunk's
-// ready flag is raised by a second 4-byte SDMA copy on the same engine that starts
-// once the chunk's copy has completed (HSA signal dependency). Its source is entry
-// `epoch` of a static table holding 0, 1, 2, ..., so the flag copy depends on
-// nothing but the chunk copy. No copy enters a HIP stream: on this platform a
+// the HSA runtime (sdma.cpp), consecutive chunks on consecutive engines. A chunk's
+// ready flag is the completion signal of its copy: a GPU-only HSA signal whose value
+// the host sets to 1 before the call's kernel is launched and the engine brings to 0
+// when the copy has landed; the kernel polls that value in memory. Signals come in
+// two sets used by alternate calls, so a kernel still finishing the previous call
+// never sees its signals reset. No copy enters a HIP stream: on this platform a
 // stream wait (and the stream write/wait-value operations, which run as kernels)
 // can end up behind the persistent kernel in a shared hardware queue, and a copy
 // behind it could not progress until the kernel that waits for its flag ends.
@@ -23,6 +24,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <chrono>
 #include <cstdarg>
 #include <cstdio>
@@ -76,8 +78,8 @@ struct DeviceGuard {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-// Epochs run 1 .. kEpochTable - 1; the flag copy of epoch e reads table entry e.
-constexpr uint32_t kEpochTable = 1u << 16;
+// Epochs run 1 .. kEpochWrap - 1; on reaching it the emitted-flag words are cleared.
+constexpr uint32_t kEpochWrap = 1u << 30;
 constexpr int kTimingRing = 256;  // kernel launches whose durations a plan keeps
 
 }  // namespace
@@ -111,10 +113,14 @@ struct csg_plan {
   int32_t* d_list_begin = nullptr;     // [kXcdLists + 1] per-die sub-list bounds (in units)
   float* d_ws = nullptr;               // split-K partial sums
   uint32_t* d_slot_count = nullptr;    // split-K finished slices per tile
-  int32_t split = 1;                   // K-slices per tile
+  int32_t ws_slices = 0;               // partial-sum buffers of split tiles (0: nothing is split)
+  uint64_t* d_trace = nullptr;         // per-unit trace words (cfg.trace)
+  std::vector<csg::TileDesc> units;    // host copy of the execution list
+  std::vector<int32_t> unit_raster;    // raster id per execution position
+  bool lines_aligned = false;          // every chunk of A starts on a 128-byte line
   int32_t n_units = 0;                 // entries of the execution list
-  uint32_t* d_flags = nullptr;         // fine-grained device memory: [n_chunks] ready flags
-  uint32_t* d_epoch_table = nullptr;   // [kEpochTable], entry i == i: source of the flag copies
+  const int64_t** d_ready[2] = {nullptr, nullptr};  // per signal set: [n_chunks] ready-value pointers
+  int64_t* d_zero = nullptr;           // the "ready" value local chunks point at
   uint32_t* d_counters = nullptr;
   uint32_t* d_ticket = nullptr;
   csg::DeviceDiag* d_diag = nullptr;
@@ -122,9 +128,10 @@ struct csg_plan {
   uint32_t* h_out_flags_dev = nullptr; // its device address
   uint32_t* d_scratch = nullptr;       // target of the engines' warm-up copies
   csg::SdmaEngines sdma;
-  std::vector<hsa_signal_t> sig_data;  // per remote chunk position: chunk copy done
-  std::vector<hsa_signal_t> sig_flag;  // per remote chunk position: flag copy done
+  std::vector<hsa_signal_t> sig_ready[2];  // consumers: per signal set, per remote chunk position
+  std::vector<hsa_signal_t> sig_data;  // producer: per remote chunk position, copy-out done
   bool copies_in_flight = false;       // a call returned before its copies completed (error path)
+  int copies_set = 0;                  // signal set of those copies (consumers)
   hipEvent_t ev_copy_in = nullptr;     // the caller's copy stream reached the call
   hipEvent_t ev_prologue = nullptr;    // the prologue finished (waited for on an epoch wrap)
   hipEvent_t ev_kernel_done[2] = {nullptr, nullptr};  // by epoch parity
@@ -143,24 +150,25 @@ namespace {
 void free_plan_device(csg_plan* p) {
   if (p->device < 0) return;
   DeviceGuard g(p->device);
-  for (size_t i = 0; i < p->sig_flag.size(); ++i) {
-    if (p->copies_in_flight) {
-      (void)csg::sdma_wait(p->sig_data[i], 0, 10000);
-      (void)csg::sdma_wait(p->sig_flag[i], 0, 10000);
-    }
+  if (p->copies_in_flight) {
+    const std::vector<hsa_signal_t>& sigs = p->consumer() ? p->sig_ready[p->copies_set] : p->sig_data;
+    for (hsa_signal_t sgn : sigs)
+      if (sgn.handle) (void)csg::sdma_wait(sgn, 0, 10000);
   }
   for (hsa_signal_t sgn : p->sig_data)
     if (sgn.handle) hsa_signal_destroy(sgn);
-  for (hsa_signal_t sgn : p->sig_flag)
-    if (sgn.handle) hsa_signal_destroy(sgn);
+  for (auto& set : p->sig_ready)
+    for (hsa_signal_t sgn : set)
+      if (sgn.handle) hsa_signal_destroy(sgn);
   p->sdma.close();
   for (hipEvent_t e : p->ev_kernel_done)
     if (e) (void)hipEventSynchronize(e);
   for (void* ptr : {static_cast<void*>(p->d_tiles), static_cast<void*>(p->d_list_ptr),
                     static_cast<void*>(p->d_list_ids), static_cast<void*>(p->d_raster), static_cast<void*>(p->d_need),
                     static_cast<void*>(p->d_list_begin), static_cast<void*>(p->d_ws),
-                    static_cast<void*>(p->d_slot_count),
-                    static_cast<void*>(p->d_flags), static_cast<void*>(p->d_epoch_table),
+                    static_cast<void*>(p->d_slot_count), static_cast<void*>(p->d_trace),
+                    static_cast<void*>(p->d_ready[0]), static_cast<void*>(p->d_ready[1]),
+                    static_cast<void*>(p->d_zero),
                     static_cast<void*>(p->d_counters), static_cast<void*>(p->d_ticket), static_cast<void*>(p->d_diag),
                     static_cast<void*>(p->d_scratch)})
     if (ptr) (void)hipFree(ptr);
@@ -181,6 +189,9 @@ csg_status upload(T** dst, const std::vector<T>& src) {
   if (!src.empty()) CSG_HIP(hipMemcpy(*dst, src.data(), src.size() * sizeof(T), hipMemcpyHostToDevice));
   return CSG_OK;
 }
+
+int64_t in_bytes(const csg_plan* p) { return p->in_dtype == CSG_BF16 ? 2 : 4; }
+int64_t out_bytes(const csg_plan* p) { return p->out_dtype == CSG_BF16 ? 2 : 4; }
 
 csg_status setup_device(csg_plan* p) {
   DeviceGuard g(p->device);
@@ -205,24 +216,42 @@ csg_status setup_device(csg_plan* p) {
     }
     list_begin[csg::kXcdLists] = static_cast<int32_t>(exec_order.size());
   }
-  // work units: every tile, split into `split` K-slices (consecutive units of one tile)
+  // K-slices per tile: split_k for every tile; tail_split for the tiles on the
+  // critical path of the overlap, i.e. those reading one of the tail_chunks
+  // last-arriving chunks (consumers), or writing one of the tail_chunks first-emitted
+  // chunks (producer)
   const int32_t KT = static_cast<int32_t>(p->K / p->cfg.bk);
-  const int32_t split = std::max(1, std::min(p->cfg.split_k, KT));
-  p->split = split;
-  const int32_t n_units = n_tiles * split;
+  std::vector<int32_t> tile_split(n_tiles, std::max(1, p->cfg.split_k));
+  if (p->cfg.tail_split > 1 && p->cfg.tail_chunks > 0) {
+    std::vector<int32_t> pos(p->n_chunks());
+    for (int32_t i = 0; i < p->n_chunks(); ++i) pos[p->sched.order[i]] = i;
+    for (int32_t t = 0; t < n_tiles; ++t) {
+      int32_t lo = p->n_chunks(), hi = -1;
+      for (int32_t q = m.tile_ptr[t]; q < m.tile_ptr[t + 1]; ++q) {
+        lo = std::min(lo, pos[m.tile_chunks[q]]);
+        hi = std::max(hi, pos[m.tile_chunks[q]]);
+      }
+      const bool critical = p->consumer() ? hi >= p->n_chunks() - p->cfg.tail_chunks : lo < p->cfg.tail_chunks;
+      if (critical) tile_split[t] = std::max(tile_split[t], p->cfg.tail_split);
+    }
+  }
+  for (int32_t& sp : tile_split) sp = std::min(sp, KT);
+  // work units: every tile, as tile_split[t] consecutive K-slices; the slices of a
+  // split tile own consecutive partial-sum buffers of the workspace
   std::vector<csg::TileDesc> tiles;
-  tiles.reserve(n_units);
   std::vector<int32_t> lptr(1, 0), lids, raster;
   std::vector<int32_t> unit_begin(csg::kXcdLists + 1, 0);
-  for (int x = 0; x <= csg::kXcdLists; ++x) unit_begin[x] = list_begin[x] * split;  // tiles -> units
-  for (int32_t i = 0; i < n_tiles; ++i) {
+  int32_t ws_slices = 0;
+  for (int32_t i = 0, x = 0; i < n_tiles; ++i) {
+    while (x <= csg::kXcdLists && list_begin[x] == i) unit_begin[x++] = static_cast<int32_t>(tiles.size());
     const int32_t t = exec_order[i];
     const csg::RowTile& rt = m.row_tiles[t / nN];
+    const int32_t split = tile_split[t];
     for (int32_t sl = 0; sl < split; ++sl) {
       const int32_t k0 = static_cast<int32_t>(static_cast<int64_t>(KT) * sl / split);
       const int32_t k1 = static_cast<int32_t>(static_cast<int64_t>(KT) * (sl + 1) / split);
       tiles.push_back({static_cast<int32_t>(rt.row_begin), static_cast<int32_t>(rt.row_end), t % nN, rt.group, k0, k1,
-                       split > 1 ? t : -1, sl | (split << 16)});
+                       split > 1 ? ws_slices : -1, sl | (split << 16)});
       raster.push_back(t);
       for (int32_t q = m.tile_ptr[t]; q < m.tile_ptr[t + 1]; ++q) {
         const int32_t c = m.tile_chunks[q];
@@ -231,32 +260,43 @@ csg_status setup_device(csg_plan* p) {
       }
       lptr.push_back(static_cast<int32_t>(lids.size()));
     }
+    if (split > 1) ws_slices += split;
   }
+  for (int x = 0; x <= csg::kXcdLists; ++x)
+    if (list_begin[x] == n_tiles) unit_begin[x] = static_cast<int32_t>(tiles.size());
+  const int32_t n_units = static_cast<int32_t>(tiles.size());
+  p->ws_slices = ws_slices;
+  p->units = tiles;
+  p->unit_raster = raster;
   list_begin = unit_begin;
   p->n_units = n_units;
+  p->lines_aligned = true;
+  for (const csg::ChunkDesc& c : p->sched.chunks)
+    if ((c.row_begin * p->K * in_bytes(p)) % 128 != 0) p->lines_aligned = false;
   std::vector<int32_t> need(p->n_chunks());
   for (int32_t c = 0; c < p->n_chunks(); ++c) need[c] = m.chunk_ptr[c + 1] - m.chunk_ptr[c];
-  std::vector<uint32_t> table(kEpochTable);
-  for (uint32_t i = 0; i < kEpochTable; ++i) table[i] = i;
   csg_status st;
   if ((st = upload(&p->d_tiles, tiles)) != CSG_OK) return st;
   if ((st = upload(&p->d_list_ptr, lptr)) != CSG_OK) return st;
   if ((st = upload(&p->d_list_ids, lids)) != CSG_OK) return st;
   if ((st = upload(&p->d_raster, raster)) != CSG_OK) return st;
   if ((st = upload(&p->d_need, need)) != CSG_OK) return st;
-  if ((st = upload(&p->d_epoch_table, table)) != CSG_OK) return st;
   if ((st = upload(&p->d_list_begin, list_begin)) != CSG_OK) return st;
   const size_t nflag = static_cast<size_t>(std::max(p->n_chunks(), 1));
-  CSG_HIP(hipExtMallocWithFlags(reinterpret_cast<void**>(&p->d_flags), nflag * 4, hipDeviceMallocFinegrained));
-  CSG_HIP(hipMemset(p->d_flags, 0, nflag * 4));
+  CSG_HIP(hipMalloc(&p->d_zero, 64));
+  CSG_HIP(hipMemset(p->d_zero, 0, 64));
   CSG_HIP(hipMalloc(&p->d_counters, nflag * 4));
   CSG_HIP(hipMemset(p->d_counters, 0, nflag * 4));
   CSG_HIP(hipMalloc(&p->d_ticket, csg::kXcdLists * 4));
-  if (split > 1) {
-    const size_t ws_bytes = static_cast<size_t>(n_tiles) * split * p->cfg.bm * p->cfg.bn * sizeof(float);
+  if (ws_slices > 0) {
+    const size_t ws_bytes = static_cast<size_t>(ws_slices) * p->cfg.bm * p->cfg.bn * sizeof(float);
     CSG_HIP(hipMalloc(&p->d_ws, ws_bytes));
     CSG_HIP(hipMalloc(&p->d_slot_count, static_cast<size_t>(n_tiles) * 4));
     CSG_HIP(hipMemset(p->d_slot_count, 0, static_cast<size_t>(n_tiles) * 4));
+  }
+  if (p->cfg.trace) {
+    CSG_HIP(hipMalloc(&p->d_trace, static_cast<size_t>(std::max(n_units, 1)) * 4 * sizeof(uint64_t)));
+    CSG_HIP(hipMemset(p->d_trace, 0, static_cast<size_t>(std::max(n_units, 1)) * 4 * sizeof(uint64_t)));
   }
   CSG_HIP(hipMalloc(&p->d_diag, sizeof(csg::DeviceDiag)));
   CSG_HIP(hipMemset(p->d_diag, 0, sizeof(csg::DeviceDiag)));
@@ -265,14 +305,28 @@ csg_status setup_device(csg_plan* p) {
   CSG_HIP(hipHostGetDevicePointer(reinterpret_cast<void**>(&p->h_out_flags_dev), p->h_out_flags, 0));
   CSG_HIP(hipMalloc(&p->d_scratch, 64));
   CSG_HIP(hipDeviceSynchronize());
-  std::string err = p->sdma.open(p->device, p->cfg.copy_engines, p->d_scratch, p->d_epoch_table);
+  std::string err = p->sdma.open(p->device, p->cfg.copy_engines, p->d_scratch, p->d_scratch + 8);
   if (!err.empty()) return fail(CSG_ERR_HIP, "copy engines: %s", err.c_str());
-  p->sig_data.assign(p->remote_order.size(), hsa_signal_t{0});
-  p->sig_flag.assign(p->remote_order.size(), hsa_signal_t{0});
-  for (size_t i = 0; i < p->remote_order.size(); ++i) {
-    hsa_status_t hs = hsa_signal_create(0, 0, nullptr, &p->sig_data[i]);
-    if (hs == HSA_STATUS_SUCCESS) hs = hsa_signal_create(0, 0, nullptr, &p->sig_flag[i]);
-    if (hs != HSA_STATUS_SUCCESS) return fail(CSG_ERR_NOMEM, "hsa_signal_create: %s", csg::hsa_error(hs).c_str());
+  const size_t n_remote = p->remote_order.size();
+  if (p->consumer()) {
+    for (int set = 0; set < 2; ++set) {
+      p->sig_ready[set].assign(n_remote, hsa_signal_t{0});
+      std::vector<const int64_t*> ptrs(p->n_chunks(), p->d_zero);
+      for (size_t i = 0; i < n_remote; ++i) {
+        hsa_status_t hs = p->sdma.make_signal(0, &p->sig_ready[set][i]);
+        const int64_t* vp = nullptr;
+        if (hs == HSA_STATUS_SUCCESS) hs = p->sdma.signal_value_ptr(p->sig_ready[set][i], &vp);
+        if (hs != HSA_STATUS_SUCCESS) return fail(CSG_ERR_NOMEM, "copy signal: %s", csg::hsa_error(hs).c_str());
+        ptrs[p->remote_order[i]] = vp;
+      }
+      if ((st = upload(&p->d_ready[set], ptrs)) != CSG_OK) return st;
+    }
+  } else {
+    p->sig_data.assign(n_remote, hsa_signal_t{0});
+    for (size_t i = 0; i < n_remote; ++i) {
+      const hsa_status_t hs = p->sdma.make_signal(0, &p->sig_data[i]);
+      if (hs != HSA_STATUS_SUCCESS) return fail(CSG_ERR_NOMEM, "copy signal: %s", csg::hsa_error(hs).c_str());
+    }
   }
   CSG_HIP(hipEventCreateWithFlags(&p->ev_copy_in, hipEventDisableTiming));
   CSG_HIP(hipEventCreateWithFlags(&p->ev_prologue, hipEventDisableTiming));
@@ -286,8 +340,6 @@ csg_status setup_device(csg_plan* p) {
   return CSG_OK;
 }
 
-int64_t in_bytes(const csg_plan* p) { return p->in_dtype == CSG_BF16 ? 2 : 4; }
-int64_t out_bytes(const csg_plan* p) { return p->out_dtype == CSG_BF16 ? 2 : 4; }
 
 using Clock = std::chrono::steady_clock;
 
@@ -312,24 +364,29 @@ csg_status host_wait(csg_plan* p, hipEvent_t e, const char* what) {
 }
 
 struct CallState {
-  bool wrapped = false;
   int prev_parity = 0;
   bool prev_kernel = false;
 };
+
+// The signals copies of this call complete: one set per call parity (consumers), the
+// copy-out signals (producer).
+std::vector<hsa_signal_t>& call_signals(csg_plan* p) {
+  return p->consumer() ? p->sig_ready[p->epoch & 1] : p->sig_data;
+}
 
 // Waits for the copies a previous call left running (only after an error return).
 csg_status drain_copies(csg_plan* p) {
   if (!p->copies_in_flight) return CSG_OK;
   const int budget = p->cfg.timeout_ms * 4;
-  for (size_t i = 0; i < p->sig_flag.size(); ++i) {
-    if (csg::sdma_wait(p->sig_data[i], 0, budget) != 0 || csg::sdma_wait(p->sig_flag[i], 0, budget) != 0)
-      return fail(CSG_ERR_TIMEOUT, "copies of the previous call did not complete");
-  }
+  const std::vector<hsa_signal_t>& sigs = p->consumer() ? p->sig_ready[p->copies_set] : p->sig_data;
+  for (hsa_signal_t sgn : sigs)
+    if (csg::sdma_wait(sgn, 0, budget) > 0) return fail(CSG_ERR_TIMEOUT, "copies of the previous call did not complete");
   p->copies_in_flight = false;
   return CSG_OK;
 }
 
-// Front half of a call: the prologue is queued on the compute stream.
+// Front half of a call: the call's ready signals are armed and the prologue is
+// queued on the compute stream.
 csg_status begin_call(csg_plan* p, csg_mode mode, hipStream_t compute, CallState* cs) {
   if (mode != CSG_MODE_OVERLAP && mode != CSG_MODE_COMPUTE_ONLY && mode != CSG_MODE_COPY_ONLY)
     return fail(CSG_ERR_INVALID, "unknown mode %d", static_cast<int>(mode));
@@ -337,15 +394,29 @@ csg_status begin_call(csg_plan* p, csg_mode mode, hipStream_t compute, CallState
   if (st != CSG_OK) return st;
   cs->prev_parity = p->epoch & 1;
   cs->prev_kernel = p->kernel_pending[cs->prev_parity];
-  if (p->epoch + 1 >= kEpochTable) {  // wrap (from an odd epoch): clear every flag, restart at 2
-    p->epoch = 1;                     // so the new epoch's parity differs from the last one's
-    cs->wrapped = true;
+  if (p->epoch + 1 >= kEpochWrap) {
+    // the producer's emitted flags hold epochs: once no kernel can still write one,
+    // clear them and restart at 2 (so the new epoch's parity differs from the last one's)
+    for (int par = 0; par < 2; ++par)
+      if (p->kernel_pending[par] && (st = host_wait(p, p->ev_kernel_done[par], "an earlier kernel")) != CSG_OK)
+        return st;
+    std::memset(p->h_out_flags, 0, static_cast<size_t>(std::max(p->n_chunks(), 1)) * 4);
+    p->epoch = 1;
   }
   ++p->epoch;
   p->host_diag = csg_diag{0, -1, -1, 0, p->epoch, 0};
-  CSG_HIP(csg::launch_prologue(p->d_flags, p->n_chunks(), p->epoch, mode == CSG_MODE_COMPUTE_ONLY ? 1 : 0,
-                               cs->wrapped ? 1 : 0, p->consumer() ? nullptr : p->d_counters, p->d_ticket, p->d_diag,
-                               p->d_slot_count, p->split > 1 ? p->map.n_tiles() : 0, compute));
+  if (p->consumer() && !p->remote_order.empty()) {
+    // this call's signal set was last polled by the kernel two calls back, which must
+    // be done before the set is armed again (it normally ended long ago)
+    const int set = p->epoch & 1;
+    if (p->kernel_pending[set] && (st = host_wait(p, p->ev_kernel_done[set], "the kernel two calls back")) != CSG_OK)
+      return st;
+    const hsa_signal_value_t v = mode == CSG_MODE_COMPUTE_ONLY ? 0 : 1;  // compute-only: every chunk ready
+    for (hsa_signal_t sgn : p->sig_ready[set]) hsa_signal_store_relaxed(sgn, v);
+    std::atomic_thread_fence(std::memory_order_seq_cst);  // armed before the kernel launch below
+  }
+  CSG_HIP(csg::launch_prologue(p->consumer() ? nullptr : p->d_counters, p->n_chunks(), p->epoch, p->d_ticket,
+                               p->d_diag, p->d_slot_count, p->ws_slices > 0 ? p->map.n_tiles() : 0, compute));
   CSG_HIP(hipEventRecord(p->ev_prologue, compute));
   p->kernel_pending[p->epoch & 1] = false;
   return CSG_OK;
@@ -360,18 +431,17 @@ csg_status ready_copies(csg_plan* p, hipStream_t copy, const CallState& cs, bool
     st = host_wait(p, p->ev_kernel_done[cs.prev_parity], "the previous call's kernel");
     if (st != CSG_OK) return st;
   }
-  // the prologue clears counters (producer) and, on a wrap, the flags
-  st = host_wait(p, p->ev_prologue, "the call's prologue");
-  if (st != CSG_OK) return st;
   p->copies_in_flight = true;
+  p->copies_set = p->epoch & 1;
   return CSG_OK;
 }
 
-// Waits until every issued copy (and flag copy) of this call has completed.
-csg_status finish_copies(csg_plan* p, size_t issued, bool with_flags) {
+// Waits until every issued copy of this call has completed.
+csg_status finish_copies(csg_plan* p, size_t issued) {
   const int budget = p->cfg.timeout_ms * 4;
+  const std::vector<hsa_signal_t>& sigs = call_signals(p);
   for (size_t i = 0; i < issued; ++i) {
-    hsa_signal_value_t v = csg::sdma_wait(with_flags ? p->sig_flag[i] : p->sig_data[i], 0, budget);
+    hsa_signal_value_t v = csg::sdma_wait(sigs[i], 0, budget);
     if (v < 0) return fail(CSG_ERR_HIP, "SDMA copy %zu reported an error", i);
     if (v != 0) {
       p->host_diag = csg_diag{1, p->remote_order[i], -1, 0, p->epoch, 0};
@@ -395,7 +465,7 @@ csg_status launch_gemm(csg_plan* p, const void* A, const void* B, void* C, hipSt
   a.list_ptr = p->d_list_ptr;
   a.list_ids = p->d_list_ids;
   a.raster = p->d_raster;
-  a.flags = p->d_flags;
+  a.ready = p->d_ready[p->epoch & 1];
   a.counters = p->d_counters;
   a.need = p->d_need;
   a.out_flags = p->h_out_flags_dev;
@@ -409,6 +479,9 @@ csg_status launch_gemm(csg_plan* p, const void* A, const void* B, void* C, hipSt
   a.slot_count = p->d_slot_count;
   a.n_chunks = p->n_chunks();
   a.dynamic_ticket = p->cfg.tile_dispatch == 2 ? 0 : 1;
+  a.steal = (p->ws_slices > 0 && a.dynamic_ticket) ? 0 : 1;
+  a.trace = p->d_trace;
+  a.acquire_fresh = (p->consumer() && (!p->lines_aligned || reinterpret_cast<uintptr_t>(A) % 128 != 0)) ? 1 : 0;
   const int slot = static_cast<int>(p->n_launches % kTimingRing);
   CSG_HIP(hipEventRecord(p->ev_k0[slot], compute));
   CSG_HIP(csg::launch_chunk_gemm(p->key, a, p->grid, compute));
@@ -419,14 +492,15 @@ csg_status launch_gemm(csg_plan* p, const void* A, const void* B, void* C, hipSt
   return CSG_OK;
 }
 
-// Consumer copies: staging -> landing per remote chunk, then the chunk's flag, both
-// on engine (i mod engines) for the i-th remote chunk in arrival order.
+// Consumer copies: staging -> landing per remote chunk, on engine (i mod engines)
+// for the i-th remote chunk in arrival order; each completes the chunk's (armed)
+// ready signal.
 csg_status issue_consumer_copies(csg_plan* p, void* landing, const void* staging) {
   const int64_t row_bytes = p->K * in_bytes(p);
   const bool delayed = !p->delays_us.empty();
   const Clock::time_point t0 = Clock::now();
   double release_us = 0.0;
-  const uint32_t* epoch_src = p->d_epoch_table + p->epoch;
+  const std::vector<hsa_signal_t>& sigs = call_signals(p);
   for (size_t i = 0; i < p->remote_order.size(); ++i) {
     const int32_t cid = p->remote_order[i];
     const csg::ChunkDesc& c = p->sched.chunks[cid];
@@ -436,21 +510,17 @@ csg_status issue_consumer_copies(csg_plan* p, void* landing, const void* staging
     }
     const int64_t off = c.row_begin * row_bytes;
     const int64_t bytes = (c.row_end - c.row_begin) * row_bytes;
-    hsa_signal_store_relaxed(p->sig_data[i], 1);
-    hsa_signal_store_relaxed(p->sig_flag[i], 1);
     const int eng = static_cast<int>(i % p->sdma.count());
-    hsa_status_t hs = p->sdma.copy(static_cast<char*>(landing) + off, static_cast<const char*>(staging) + off,
-                                   static_cast<size_t>(bytes), eng, nullptr, p->sig_data[i]);
-    if (hs == HSA_STATUS_SUCCESS)
-      hs = p->sdma.copy(p->d_flags + cid, epoch_src, 4, eng, &p->sig_data[i], p->sig_flag[i]);
+    const hsa_status_t hs = p->sdma.copy(static_cast<char*>(landing) + off, static_cast<const char*>(staging) + off,
+                                         static_cast<size_t>(bytes), eng, nullptr, sigs[i]);
     if (hs != HSA_STATUS_SUCCESS) {
-      hsa_signal_store_relaxed(p->sig_data[i], 0);
-      hsa_signal_store_relaxed(p->sig_flag[i], 0);
-      (void)finish_copies(p, i, true);
-      return fail(CSG_ERR_HIP, "SDMA copy: %s", csg::hsa_error(hs).c_str());
+      // the chunks not copied keep their signals armed: the kernel's bounded waits for
+      // them expire and it reports them through csg_plan_check
+      (void)finish_copies(p, i);
+      return fail(CSG_ERR_HIP, "SDMA copy of chunk %d: %s", cid, csg::hsa_error(hs).c_str());
     }
   }
-  return finish_copies(p, p->remote_order.size(), true);
+  return finish_copies(p, p->remote_order.size());
 }
 
 csg_status consumer_call(csg_plan* p, void* landing, const void* staging, const void* b, void* c, csg_mode mode,
@@ -606,9 +676,16 @@ csg_status csg_plan_create(csg_op op, int64_t M, int64_t N, int64_t K, csg_dtype
   if (c.timeout_ms == 0) c.timeout_ms = 2000;
   if (c.split_k == 0) c.split_k = 1;
   if (c.bm < 1 || c.bn < 1 || c.bk < 1 || c.copy_engines < 0 || c.copy_engines > 32 || c.timeout_ms < 1 ||
-      c.split_k < 1 || c.split_k > 64 ||
+      c.split_k < 1 || c.split_k > 64 || c.tail_split < 0 || c.tail_split > 64 || c.tail_chunks < 0 ||
+      c.trace < 0 || c.trace > 1 ||
       c.num_workgroups < 0 || c.tile_dispatch < 0 || c.tile_dispatch > 2 || c.intra_order != 0)
     return fail(CSG_ERR_INVALID, "bad plan configuration");
+  // split tiles run every slice on their own die (no stealing): every die needs
+  // workgroups, which the round-robin dispatch of a grid that is a multiple of the die
+  // count guarantees
+  if ((c.split_k > 1 || (c.tail_split > 1 && c.tail_chunks > 0)) && c.tile_dispatch != 2 && c.num_workgroups > 0 &&
+      c.num_workgroups % csg::kXcdLists != 0)
+    return fail(CSG_ERR_INVALID, "with split tiles num_workgroups must be a multiple of %d", csg::kXcdLists);
 
   csg_plan* p = new (std::nothrow) csg_plan;
   if (!p) return fail(CSG_ERR_NOMEM, "out of host memory");
@@ -640,6 +717,14 @@ csg_status csg_plan_create(csg_op op, int64_t M, int64_t N, int64_t K, csg_dtype
     if (K % c.bk != 0 || N % 4 != 0) {
       delete p;
       return fail(CSG_ERR_UNSUPPORTED, "K must be a multiple of %d and N a multiple of 4", c.bk);
+    }
+    // a tile's rows of A, B and C are addressed with 32-bit buffer offsets
+    const int64_t ib = bf16 ? 2 : 4, ob = out_dtype == CSG_BF16 ? 2 : 4;
+    if (static_cast<int64_t>(std::max(c.bm, c.bn)) * K * ib >= (int64_t{1} << 31) ||
+        static_cast<int64_t>(c.bm) * N * ob >= (int64_t{1} << 30)) {
+      delete p;
+      return fail(CSG_ERR_UNSUPPORTED, "a %d-row tile of A/B (K = %lld) or of C (N = %lld) exceeds the 32-bit offset range",
+                  std::max(c.bm, c.bn), static_cast<long long>(K), static_cast<long long>(N));
     }
     if (p->consumer() && p->n_chunks() > csg::kernel_max_chunks()) {
       delete p;
@@ -685,6 +770,7 @@ csg_status csg_plan_info_get(const csg_plan* p, csg_plan_info* info) {
   info->bm = p->cfg.bm;
   info->bn = p->cfg.bn;
   info->bk = p->cfg.bk;
+  info->n_units = p->device >= 0 ? p->n_units : 0;
   return CSG_OK;
 }
 
@@ -759,7 +845,7 @@ csg_status csg_gemm_rs(csg_plan* p, const void* a, const void* b_nk, void* c, vo
       const volatile uint32_t* f = p->h_out_flags + cid;
       while (*f < p->epoch) {
         if (Clock::now() - t0 > budget) {
-          (void)finish_copies(p, i, false);
+          (void)finish_copies(p, i);
           p->host_diag = csg_diag{1, cid, -1, *f, p->epoch, 0};
           return fail(CSG_ERR_TIMEOUT, "output chunk %d was not completed in time", cid);
         }
@@ -774,11 +860,11 @@ csg_status csg_gemm_rs(csg_plan* p, const void* a, const void* b_nk, void* c, vo
                      nullptr, p->sig_data[i]);
     if (hs != HSA_STATUS_SUCCESS) {
       hsa_signal_store_relaxed(p->sig_data[i], 0);
-      (void)finish_copies(p, i, false);
+      (void)finish_copies(p, i);
       return fail(CSG_ERR_HIP, "SDMA copy: %s", csg::hsa_error(hs).c_str());
     }
   }
-  return finish_copies(p, p->remote_order.size(), false);
+  return finish_copies(p, p->remote_order.size());
 }
 
 csg_status csg_plan_check(csg_plan* p, csg_diag* out) {
@@ -795,11 +881,47 @@ csg_status csg_plan_check(csg_plan* p, csg_diag* out) {
     CSG_HIP(hipMemcpyAsync(&dd, p->d_diag, sizeof dd, hipMemcpyDeviceToHost, p->aux));
     CSG_HIP(hipStreamSynchronize(p->aux));
     if (dd.timed_out && !d.timed_out) d = csg_diag{1, dd.chunk, dd.tile, dd.observed, dd.epoch, 0};
+    if (!d.timed_out && p->kernel_pending[p->epoch & 1] && dd.units_done != static_cast<uint32_t>(p->n_units)) {
+      if (out) *out = d;
+      return fail(CSG_ERR_STATE, "the kernel ran %u of %d work units (a die without workgroups?)", dd.units_done,
+                  p->n_units);
+    }
   }
   if (out) *out = d;
   if (d.timed_out)
-    return fail(CSG_ERR_TIMEOUT, "chunk %d (tile %d) never became ready: flag %u < epoch %u", d.chunk, d.tile,
+    return fail(CSG_ERR_TIMEOUT, "chunk %d (tile %d) never became ready (value %u, call %u)", d.chunk, d.tile,
                 d.observed, d.epoch);
+  return CSG_OK;
+}
+
+csg_status csg_plan_trace(csg_plan* p, csg_trace_unit* units_host, int32_t n, int32_t* n_out) {
+  if (!p || !units_host || !n_out || n < 0) return fail(CSG_ERR_INVALID, "NULL argument or n < 0");
+  *n_out = 0;
+  if (p->device < 0 || !p->d_trace) return fail(CSG_ERR_STATE, "plan was not created with tracing");
+  if (p->n_launches == 0) return fail(CSG_ERR_STATE, "plan never ran a kernel");
+  DeviceGuard g(p->device);
+  if (g.err != hipSuccess) return hip_fail(g.err, "hipSetDevice");
+  CSG_HIP(hipEventSynchronize(p->ev_k1[(p->n_launches - 1) % kTimingRing]));
+  const int32_t m = std::min(n, p->n_units);
+  std::vector<uint64_t> words(static_cast<size_t>(m) * 4);
+  if (m > 0) {
+    CSG_HIP(hipMemcpyAsync(words.data(), p->d_trace, words.size() * sizeof(uint64_t), hipMemcpyDeviceToHost, p->aux));
+    CSG_HIP(hipStreamSynchronize(p->aux));
+  }
+  for (int32_t i = 0; i < m; ++i) {
+    const csg::TileDesc& u = p->units[i];
+    csg_trace_unit& r = units_host[i];
+    r.raster = p->unit_raster[i];
+    r.slice = u.slice & 0xffff;
+    r.n_slices = u.slice >> 16;
+    r.xcd = static_cast<int32_t>(words[4 * i + 3] >> 32);
+    r.workgroup = static_cast<int32_t>(words[4 * i + 3] & 0xffffffffu);
+    r.reserved = 0;
+    r.t_take = words[4 * i + 0];
+    r.t_start = words[4 * i + 1];
+    r.t_end = words[4 * i + 2];
+  }
+  *n_out = m;
   return CSG_OK;
 }
 

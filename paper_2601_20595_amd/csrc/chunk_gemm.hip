@@ -5,20 +5,22 @@
 // (consumer ops: all-gather + GEMM, all-to-all + grouped GEMM) or emission
 // (producer op: GEMM + reduce-scatter), following the tile-scheduler swizzle of
 // Section 5.2:
-//   consumer: before a tile, wait until every remote chunk its rows read has a
-//             ready flag >= epoch (the copy engine raises it after the chunk's
-//             copy). A workgroup remembers the chunks it has seen ready, so it
-//             waits at most once per chunk (Section 5.2, minimal synchronization);
+//   consumer: before a tile, wait until every remote chunk its rows read is ready
+//             (its copy's completion signal, which the copy engine brings to 0).
+//             A workgroup remembers the chunks it has seen ready, so it waits at
+//             most once per chunk (Section 5.2, minimal synchronization);
 //   producer: after a tile, count it against every chunk it wrote; the tile that
 //             completes a chunk releases the chunk's flag for the copy engine.
 //
-// Main loops (256 threads = 2 x 2 waves, each wave a (BM/2) x (BN/2) sub-tile of
-// 32 x 32 MFMA blocks):
-//   bf16: v_mfma_f32_32x32x16_bf16; tiles stream HBM -> LDS with buffer_load ... lds
-//         (no register staging), double-buffered; LDS rows are 128 bytes with an XOR
-//         swizzle of their 16-byte vectors that keeps both the DMA writes and the
-//         ds_read_b128 fragment reads free of bank conflicts.
-//   fp32: v_mfma_f32_32x32x2_f32 with register-staged, padded LDS tiles.
+// Main loops (each wave owns a sub-tile of 32 x 32 MFMA blocks):
+//   bf16: 512 threads = 2 (M) x 4 (N) waves, two per SIMD, so one wave's MFMAs issue
+//         while the other waits on LDS or issues its loads; v_mfma_f32_32x32x16_bf16;
+//         tiles stream HBM -> LDS with buffer_load ... lds (no register staging),
+//         double-buffered; LDS rows are 128 bytes with an XOR swizzle of their 16-byte
+//         vectors that keeps both the DMA writes and the ds_read_b128 fragment reads
+//         free of bank conflicts.
+//   fp32: 256 threads = 2 x 2 waves; v_mfma_f32_32x32x2_f32 with register-staged,
+//         padded LDS tiles.
 // The MFMA takes the B fragment as its first operand, so each lane ends up with
 // four runs of four consecutive output columns of one output row, which the
 // epilogue writes as 8-byte (bf16) or 16-byte (fp32) stores.
@@ -39,10 +41,15 @@ typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
 // Buffer resource word 3 for raw (unswizzled, unformatted) buffers on gfx9-family targets.
 constexpr int kBufferDword3 = 0x00020000;
-constexpr int kThreads = 256;
+constexpr int kPrologueThreads = 256;
 constexpr int kMaxChunks = 4096;  // per-workgroup ready cache: one bit per chunk
 
 __device__ __forceinline__ uint32_t load_flag(const uint32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+// A chunk's ready value: its copy's completion signal, 0 once the chunk has landed.
+__device__ __forceinline__ int64_t load_ready(const int64_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
@@ -68,21 +75,22 @@ __device__ int wait_chunks(const GemmArgs& a, int pos, uint32_t* ready_bits) {
     const uint32_t bit = 1u << (c & 31);
     if (ready_bits[c >> 5] & bit) continue;
     const uint64_t t0 = wall_clock64();
-    uint32_t v = load_flag(a.flags + c);
-    while (v < a.epoch) {
+    const int64_t* rp = a.ready[c];
+    int64_t v = load_ready(rp);
+    while (v != 0) {
       if (load_flag(&a.diag->abort)) return -1;
       if (wall_clock64() - t0 > a.timeout_ticks) {
         if (atomicCAS(&a.diag->timed_out, 0u, 1u) == 0u) {
           a.diag->chunk = c;
           a.diag->tile = a.raster[pos];
-          a.diag->observed = v;
+          a.diag->observed = static_cast<uint32_t>(v);
           a.diag->epoch = a.epoch;
         }
         __hip_atomic_store(&a.diag->abort, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
         return -1;
       }
       __builtin_amdgcn_s_sleep(2);
-      v = load_flag(a.flags + c);
+      v = load_ready(rp);
     }
     ready_bits[c >> 5] |= bit;
     fresh = 1;
@@ -91,10 +99,11 @@ __device__ int wait_chunks(const GemmArgs& a, int pos, uint32_t* ready_bits) {
 }
 
 // Next execution position for a workgroup on die `xcd` (thread 0 only): the next
-// entry of that die's sub-list, else of the following dies' sub-lists; n_tiles when
-// every sub-list is exhausted.
+// entry of that die's sub-list, else (when stealing is on) of the following dies'
+// sub-lists; n_tiles when no list it may take from has entries left.
 __device__ int next_tile(const GemmArgs& a, uint32_t xcd) {
-  for (int d = 0; d < kXcdLists; ++d) {
+  const int dies = a.steal ? kXcdLists : 1;
+  for (int d = 0; d < dies; ++d) {
     const int x = static_cast<int>((xcd + d) % kXcdLists);
     const int len = a.list_begin[x + 1] - a.list_begin[x];
     if (len <= 0) continue;
@@ -144,18 +153,24 @@ __device__ __forceinline__ void dma16(const __amdgpu_buffer_rsrc_t& rs, uint32_t
       : "memory");
 }
 
+// Waits until every vector-memory operation of this wave has completed (loads landed,
+// stores acknowledged).
 __device__ __forceinline__ void wait_dma_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 template <int BM_, int BN_>
 struct Bf16Loop {
   static constexpr int BM = BM_, BN = BN_, BK = 64;
-  static constexpr int WTM = BM / 2, WTN = BN / 2, MI = WTM / 32, NI = WTN / 32;
+  // 8 waves, two per SIMD: while one wave of a SIMD waits on LDS or issues its DMA,
+  // the other keeps the matrix core busy. Waves are laid out 2 (M) x 4 (N).
+  static constexpr int WAVES_M = 2, WAVES_N = 4, WAVES = WAVES_M * WAVES_N, THREADS = WAVES * 64;
+  static constexpr int WTM = BM / WAVES_M, WTN = BN / WAVES_N, MI = WTM / 32, NI = WTN / 32;
   static constexpr int ROWB = 128;                           // bytes per LDS row (64 bf16)
   static constexpr int STAGE_A = BM * ROWB, STAGE_B = BN * ROWB;
   static constexpr int STAGE = STAGE_A + STAGE_B;
   static constexpr int LDS_BYTES = 2 * STAGE;
-  static constexpr int A_LOADS = BM / 32, B_LOADS = BN / 32;  // wave DMA issues per stage (8 rows each)
-  static_assert(BM % 64 == 0 && BN % 64 == 0, "bf16 tiles are multiples of 64");
+  static constexpr int A_ROWS_W = BM / WAVES, B_ROWS_W = BN / WAVES;  // rows each wave loads per stage
+  static constexpr int A_LOADS = A_ROWS_W / 8, B_LOADS = B_ROWS_W / 8; // DMA issues (8 rows each)
+  static_assert(A_ROWS_W % 8 == 0 && B_ROWS_W % 8 == 0 && WTM % 32 == 0 && WTN % 32 == 0, "bf16 tile shape");
 
   // LDS swizzle: logical 16-byte vector v of tile row r sits at physical vector
   // v ^ swz(r), swz(r) = (r & 7) ^ ((r >> 3) & 1). Any 8 consecutive aligned rows,
@@ -165,13 +180,13 @@ struct Bf16Loop {
   __device__ static int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
   // Issue one stage (the BK columns starting at byte kbase of every row): wave w
-  // fills rows [w*BM/4, (w+1)*BM/4) of A and likewise of B. Lane l of an 8-row group
+  // fills rows [w*BM/8, (w+1)*BM/8) of A and likewise of B. Lane l of an 8-row group
   // writes LDS slot l (row l/8, physical vector l%8), so it fetches logical vector
   // (l%8) ^ swz(row) of that row.
   __device__ static void issue(uint32_t lds_base, int buf, int kbase, const __amdgpu_buffer_rsrc_t& rsA,
                                const __amdgpu_buffer_rsrc_t& rsB, int K, int wave, int lane) {
     const int lr = lane >> 3;
-    const int wrow_a = wave * (BM / 4), wrow_b = wave * (BN / 4);
+    const int wrow_a = wave * A_ROWS_W, wrow_b = wave * B_ROWS_W;
     const uint32_t la = __builtin_amdgcn_readfirstlane(lds_base + buf * STAGE + wrow_a * ROWB);
     const uint32_t lb = __builtin_amdgcn_readfirstlane(lds_base + buf * STAGE + STAGE_A + wrow_b * ROWB);
     // row = group base (a multiple of 8) + lr, so swz(row) = lr ^ ((row >> 3) & 1): the
@@ -191,7 +206,7 @@ struct Bf16Loop {
   }
 
   __device__ static void run(unsigned char* lds, const TileGeom& g, f32x16 (&acc)[MI][NI], int wave, int lane) {
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave % WAVES_M, wn = wave / WAVES_M;
     const __amdgpu_buffer_rsrc_t rsA = make_rsrc(g.Ab, g.abytes);
     const __amdgpu_buffer_rsrc_t rsB = make_rsrc(g.Bb, g.bbytes);
     const int K = static_cast<int>(g.K);
@@ -256,17 +271,18 @@ struct Bf16Loop {
 template <int BM_, int BN_>
 struct F32Loop {
   static constexpr int BM = BM_, BN = BN_, BK = 16;
+  static constexpr int WAVES_M = 2, WAVES_N = 2, THREADS = 256;
   static constexpr int WTM = BM / 2, WTN = BN / 2, MI = WTM / 32, NI = WTN / 32;
   static constexpr int LDK = BK + 4;                      // floats per LDS row
   static constexpr int STAGE_A = BM * LDK * 4, STAGE_B = BN * LDK * 4;
   static constexpr int LDS_BYTES = 2 * (STAGE_A + STAGE_B);
-  static constexpr int RPP = kThreads / (BK / 4);         // rows per load pass
+  static constexpr int RPP = THREADS / (BK / 4);          // rows per load pass
   static constexpr int A_PASSES = BM / RPP, B_PASSES = BN / RPP;
   static_assert(BM % RPP == 0 && BN % RPP == 0, "fp32 tile rows");
 
   __device__ static void run(unsigned char* lds, const TileGeom& g, f32x16 (&acc)[MI][NI], int wave, int lane) {
     const int tid = wave * 64 + lane;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave % WAVES_M, wn = wave / WAVES_M;
     const __amdgpu_buffer_rsrc_t rsA = make_rsrc(g.Ab, g.abytes);
     const __amdgpu_buffer_rsrc_t rsB = make_rsrc(g.Bb, g.bbytes);
     const int nk = g.nk;
@@ -319,10 +335,67 @@ struct F32Loop {
 };
 
 // ---------------------------------------------------------------------------------
+// Split-K reduction: sum of the S slices' partials of every run, added in slice
+// order (((p0 + p1) + p2) + ...), then stored. Runs are handled in batches of B;
+// the loads of the next batch are issued before the current batch is added and
+// stored, so the reduction pays about one memory latency instead of one per run.
+// ---------------------------------------------------------------------------------
+constexpr int kDropOffset = 0x7ffffff0;  // buffer offset past every C resource: store dropped
+constexpr int kPolicySc0 = 1, kPolicySc1 = 16;  // cache-policy bits of buffer instructions (scope)
+
+template <int S, int kRuns, class Load, class Store>
+__device__ __forceinline__ void reduce_fixed(Load load, Store store) {
+  constexpr int B0 = (8 / S) > 0 ? (8 / S) : 1;
+  constexpr int B = (B0 >= 8 && kRuns % 8 == 0) ? 8 : (B0 >= 4 && kRuns % 4 == 0) ? 4 : (B0 >= 2 && kRuns % 2 == 0) ? 2 : 1;
+  f32x4 v[2][B][S];
+#pragma unroll
+  for (int b = 0; b < B; ++b)
+#pragma unroll
+    for (int s = 0; s < S; ++s) v[0][b][s] = load(s, b);
+#pragma unroll
+  for (int r0 = 0; r0 < kRuns; r0 += B) {
+    const int cur = (r0 / B) & 1;
+    if (r0 + B < kRuns) {
+#pragma unroll
+      for (int b = 0; b < B; ++b)
+#pragma unroll
+        for (int s = 0; s < S; ++s) v[cur ^ 1][b][s] = load(s, r0 + B + b);
+    }
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      f32x4 sum = v[cur][b][0];
+#pragma unroll
+      for (int s = 1; s < S; ++s) sum += v[cur][b][s];
+      store(r0 + b, sum);
+    }
+  }
+}
+
+template <int kRuns, class Load, class Store>
+__device__ void reduce_slices(int n, Load load, Store store) {
+  switch (n) {
+    case 2: reduce_fixed<2, kRuns>(load, store); break;
+    case 3: reduce_fixed<3, kRuns>(load, store); break;
+    case 4: reduce_fixed<4, kRuns>(load, store); break;
+    case 5: reduce_fixed<5, kRuns>(load, store); break;
+    case 6: reduce_fixed<6, kRuns>(load, store); break;
+    case 7: reduce_fixed<7, kRuns>(load, store); break;
+    case 8: reduce_fixed<8, kRuns>(load, store); break;
+    default:
+      for (int r = 0; r < kRuns; ++r) {
+        f32x4 sum = load(0, r);
+        for (int s = 1; s < n; ++s) sum += load(s, r);
+        store(r, sum);
+      }
+  }
+}
+
+// ---------------------------------------------------------------------------------
 // The persistent kernel
 // ---------------------------------------------------------------------------------
 template <class Loop, bool kOutBf16, bool kProducer>
-__global__ __launch_bounds__(kThreads, 1) void chunk_gemm(GemmArgs a) {
+__global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
+  constexpr int kThreads = Loop::THREADS;
   constexpr int BN = Loop::BN;
   constexpr int MI = Loop::MI, NI = Loop::NI;
   __shared__ __attribute__((aligned(16))) unsigned char lds[Loop::LDS_BYTES];
@@ -333,22 +406,30 @@ __global__ __launch_bounds__(kThreads, 1) void chunk_gemm(GemmArgs a) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave % Loop::WAVES_M, wn = wave / Loop::WAVES_M;
   for (int i = tid; i < kMaxChunks / 32; i += kThreads) ready_bits[i] = 0;
   const int in_bytes = (Loop::BK == 64) ? 2 : 4;
   uint32_t xcd;
   asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID, 0, 4)" : "=s"(xcd));
   xcd %= kXcdLists;
+  uint32_t units = 0;  // work units this workgroup executed (the host checks the total)
 
-  for (int iter = 0;; ++iter) {
+  int iter = 0;
+  for (;; ++iter) {
     __syncthreads();  // everyone is done with s_pos / s_state / LDS of the previous tile
     if (tid == 0) {
       const int pos = a.dynamic_ticket ? next_tile(a, xcd)
                                        : static_cast<int>(blockIdx.x) + iter * static_cast<int>(gridDim.x);
       int state = 0;
       if (pos < a.n_tiles) {
+        const uint64_t t_take = a.trace ? wall_clock64() : 0;
         if (load_flag(&a.diag->abort)) state = -1;
         else if (!kProducer) state = wait_chunks(a, pos, ready_bits);
+        if (a.trace) {
+          a.trace[4 * pos + 0] = t_take;
+          a.trace[4 * pos + 1] = wall_clock64();
+          a.trace[4 * pos + 3] = (static_cast<uint64_t>(xcd) << 32) | blockIdx.x;
+        }
       }
       s_pos = pos;
       s_state = state;
@@ -357,8 +438,10 @@ __global__ __launch_bounds__(kThreads, 1) void chunk_gemm(GemmArgs a) {
     // uniform across the workgroup; readfirstlane lets everything derived from it live in SGPRs
     const int pos = __builtin_amdgcn_readfirstlane(s_pos);
     if (pos >= a.n_tiles || s_state < 0) break;
-    // a chunk seen ready for the first time: every wave drops possibly stale cache lines
-    if (!kProducer && s_state > 0) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
+    ++units;
+    // a chunk seen ready for the first time: every wave drops possibly stale cache
+    // lines, unless chunks are line-aligned (then no stale line of a chunk can exist)
+    if (!kProducer && s_state > 0 && a.acquire_fresh) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
 
     const TileDesc td = a.tiles[pos];
     const int64_t col0 = static_cast<int64_t>(td.n_tile) * BN;
@@ -382,21 +465,46 @@ __global__ __launch_bounds__(kThreads, 1) void chunk_gemm(GemmArgs a) {
       for (int j = 0; j < NI; ++j) acc[i][j] = f32x16{};
     Loop::run(lds, g, acc, wave, lane);
 
-    // Output run (i, j, q) of this thread: accumulator elements 4q..4q+3 of block
-    // (i, j), i.e. output row (i * 32 + lane % 32) and columns (j * 32 + 8q +
-    // 4 * (lane / 32) + 0..3) of the wave's sub-tile.
+    // Output run r = (i * NI + j) * 4 + q of this thread: accumulator elements
+    // 4q..4q+3 of block (i, j), i.e. output row (i * 32 + lane % 32) and columns
+    // (j * 32 + 8q + 4 * (lane / 32) + 0..3) of the wave's sub-tile.
+    constexpr int kRuns = MI * NI * 4;
+    constexpr int kOutBytes = kOutBf16 ? 2 : 4;
+    // The producer's C goes straight to memory (system-coherent stores, sc0 sc1): the
+    // copy engine reads memory, and a store that completes is then visible to it, so
+    // releasing a tile needs no write-back of this die's whole L2. Consumers' C stays
+    // in L2 until the kernel's end.
+    constexpr int kCStorePolicy = kProducer ? (kPolicySc0 | kPolicySc1) : 0;
     const int N32 = static_cast<int>(a.N);
     const int lrow = lane & 31, lhalf = lane >> 5;
-    const int64_t cbase = static_cast<int64_t>(td.row_begin) * a.N + col0;
-    auto store_run = [&](int i, int j, int q, const f32x4& f) {
-      const int lr = wm * Loop::WTM + i * 32 + lrow;
-      const int lc = wn * Loop::WTN + j * 32 + 8 * q + 4 * lhalf;
-      if (lr >= g.arows || lc >= g.brows) return;  // N is a multiple of 4: a run is all in or all out
-      const int off = lr * N32 + lc;
+    // C is written through a buffer resource over the tile's rows; a run outside the
+    // valid tile gets a lane offset past the resource's end, and the hardware drops
+    // it (the plan keeps BM * N * out_bytes below that offset). No branch, so the
+    // epilogue stays one block the compiler can schedule as a whole.
+    const __amdgpu_buffer_rsrc_t rsC =
+        make_rsrc(static_cast<unsigned char*>(a.C) + (static_cast<int64_t>(td.row_begin) * a.N + col0) * kOutBytes,
+                  static_cast<int64_t>(g.arows) * a.N * kOutBytes);
+    // the offset of run (i, j, q) is split into a per-lane part (one register), a
+    // per-row-block scalar part (i) and a constant that fits the instruction's
+    // immediate field (j, q), so no per-run offsets stay live across tiles
+    const int vrow = wm * Loop::WTM + lrow;         // row of block i: vrow + 32 i
+    const int vcol = wn * Loop::WTN + 4 * lhalf;    // column of run (j, q): vcol + 32 j + 8 q
+    const int voff_c = (vrow * N32 + vcol) * kOutBytes;
+    auto store_run = [&](int r, const f32x4& f) {
+      const int i = r / (NI * 4), j = (r / 4) % NI, q = r % 4;
+      // N is a multiple of 4: a run is all in or all out
+      const bool ok = (vrow + 32 * i < g.arows) && (vcol + 32 * j + 8 * q < g.brows);
+      const int voff = (ok ? voff_c : kDropOffset) + (32 * j + 8 * q) * kOutBytes;
+      const int soff = __builtin_amdgcn_readfirstlane(32 * i * N32 * kOutBytes);
       if constexpr (kOutBf16)  // v_cvt_pk_bf16_f32: round to nearest even (the default rounding mode)
-        *reinterpret_cast<bf16x4*>(static_cast<unsigned short*>(a.C) + cbase + off) = __builtin_convertvector(f, bf16x4);
+        __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, __builtin_convertvector(f, bf16x4)), rsC, voff,
+                                              soff, kCStorePolicy);
       else
-        *reinterpret_cast<f32x4*>(static_cast<float*>(a.C) + cbase + off) = f;
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, f), rsC, voff, soff, kCStorePolicy);
+    };
+    auto acc_run = [&](int r) -> f32x4 {
+      const int i = r / (NI * 4), j = (r / 4) % NI, q = r % 4;
+      return f32x4{acc[i][j][4 * q + 0], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
     };
 
     const int nslices = td.slice >> 16;
@@ -404,86 +512,79 @@ __global__ __launch_bounds__(kThreads, 1) void chunk_gemm(GemmArgs a) {
       // Split along K: store this slice's partial sums; the slice that finishes its
       // tile last adds all of them in slice order (so the result does not depend on
       // which slice finished when) and writes the output from those sums.
-      constexpr int kVecs = MI * NI * 4;                  // 16-byte vectors per thread
-      constexpr int kSliceBytes = kVecs * kThreads * 16;  // one slice of one tile
-      // slice layout: vector v of thread t at byte (v * kThreads + t) * 16; addressed
-      // through a buffer resource so the per-vector offset is a scalar operand
-      const __amdgpu_buffer_rsrc_t rsW =
-          make_rsrc(a.ws + static_cast<int64_t>(td.slot) * nslices * (kSliceBytes / 4),
-                    static_cast<int64_t>(nslices) * kSliceBytes);
+      constexpr int kSliceBytes = kRuns * kThreads * 16;  // one slice of one tile
+      // slice layout: run r of thread t at byte (r * kThreads + t) * 16; addressed
+      // through a buffer resource so the per-run offset is a scalar operand
+      const __amdgpu_buffer_rsrc_t rsW = make_rsrc(a.ws + static_cast<int64_t>(td.slot) * (kSliceBytes / 4),
+                                                   static_cast<int64_t>(nslices) * kSliceBytes);
       const int toff = tid * 16;
       const int mine = (td.slice & 0xffff) * kSliceBytes;
 #pragma unroll
-      for (int i = 0; i < MI; ++i)
-#pragma unroll
-        for (int j = 0; j < NI; ++j)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const f32x4 f = {acc[i][j][4 * q + 0], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
-            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, f), rsW, toff,
-                                                   mine + ((i * NI + j) * 4 + q) * kThreads * 16, 0);
-          }
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");  // partials leave this die's L2
+      for (int r = 0; r < kRuns; ++r)
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc_run(r)), rsW, toff,
+                                               mine + r * kThreads * 16, 0);
+      // Without stealing all slices of a tile run on one die and meet in its L2 (the
+      // vector L1 is write-through): waiting for the stores to complete is the release,
+      // and the reducer drops only its own L1. Otherwise slices may sit on other dies,
+      // whose L2s are not coherent with each other: write back and invalidate L2.
+      if (a.steal) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+      else wait_dma_all();
       __syncthreads();
       if (tid == 0)
-        s_state = (__hip_atomic_fetch_add(a.slot_count + td.slot, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) ==
-                   static_cast<uint32_t>(nslices - 1));
+        s_state = (__hip_atomic_fetch_add(a.slot_count + a.raster[pos], 1u, __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT) == static_cast<uint32_t>(nslices - 1));
       __syncthreads();
-      if (!s_state) continue;
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");  // see the other dies' partials
-#pragma unroll
-      for (int i = 0; i < MI; ++i)
-#pragma unroll
-        for (int j = 0; j < NI; ++j)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int v = ((i * NI + j) * 4 + q) * kThreads * 16;
-            f32x4 sum = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rsW, toff, v, 0));
-            for (int sl = 1; sl < nslices; ++sl)
-              sum += __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rsW, toff, sl * kSliceBytes + v, 0));
-            store_run(i, j, q, sum);
-            __builtin_amdgcn_sched_barrier(0);  // one run at a time keeps register use flat
-          }
+      if (!s_state) {
+        if (a.trace && tid == 0) a.trace[4 * pos + 2] = wall_clock64();
+        continue;
+      }
+      if (a.steal) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+      else asm volatile("buffer_inv sc0" ::: "memory");
+      auto load_part = [&](int sl, int r) -> f32x4 {
+        return __builtin_bit_cast(f32x4,
+                                  __builtin_amdgcn_raw_buffer_load_b128(rsW, toff, sl * kSliceBytes + r * kThreads * 16, 0));
+      };
+      reduce_slices<kRuns>(nslices, load_part, store_run);
     } else {
 #pragma unroll
-      for (int i = 0; i < MI; ++i)
-#pragma unroll
-        for (int j = 0; j < NI; ++j)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const f32x4 f = {acc[i][j][4 * q + 0], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
-            store_run(i, j, q, f);
-            __builtin_amdgcn_sched_barrier(0);  // convert-and-store one run at a time
-          }
+      for (int r = 0; r < kRuns; ++r) {
+        store_run(r, acc_run(r));
+        __builtin_amdgcn_sched_barrier(0);  // convert-and-store one run at a time
+      }
     }
 
     if constexpr (kProducer) {
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "");  // this wave's C stores reach memory first
+      // This wave's C stores (system-coherent, written through to memory) have
+      // completed before the workgroup counts the tile. The counter and flag updates
+      // are relaxed system-scope atomics, performed at the memory side; they are
+      // ordered after the stores by the wait and the barrier, and the tile completing
+      // a chunk raises its flag only after every other tile of the chunk counted
+      // itself, each after its own stores completed. No cache is written back or
+      // invalidated.
+      wait_dma_all();
       __syncthreads();
       if (tid == 0) {
         for (int p = a.list_ptr[pos]; p < a.list_ptr[pos + 1]; ++p) {
           const int c = a.list_ids[p];
           const uint32_t done =
-              __hip_atomic_fetch_add(a.counters + c, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_SYSTEM) + 1u;
+              __hip_atomic_fetch_add(a.counters + c, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) + 1u;
           if (done == static_cast<uint32_t>(a.need[c]))
-            __hip_atomic_store(a.out_flags + c, a.epoch, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+            __hip_atomic_store(a.out_flags + c, a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
         }
       }
     }
+    if (a.trace && tid == 0) a.trace[4 * pos + 2] = wall_clock64();
   }
+  if (tid == 0) atomicAdd(&a.diag->units_done, units);
 }
 
-__global__ __launch_bounds__(kThreads) void chunk_prologue(uint32_t* flags, int32_t n_chunks, uint32_t epoch,
-                                                            int32_t preset_all, int32_t clear_flags, uint32_t* counters,
-                                                            uint32_t* ticket, DeviceDiag* diag, uint32_t* slot_count,
-                                                            int32_t n_slots) {
+__global__ __launch_bounds__(kPrologueThreads) void chunk_prologue(uint32_t* counters, int32_t n_chunks,
+                                                                    uint32_t epoch, uint32_t* ticket, DeviceDiag* diag,
+                                                                    uint32_t* slot_count, int32_t n_slots) {
   const int tid = threadIdx.x;
   for (int i = tid; i < n_slots; i += blockDim.x) slot_count[i] = 0u;
-  for (int c = tid; c < n_chunks; c += blockDim.x) {
-    if (clear_flags || preset_all)
-      __hip_atomic_store(flags + c, preset_all ? epoch : 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-    if (counters) counters[c] = 0u;
-  }
+  if (counters)
+    for (int c = tid; c < n_chunks; c += blockDim.x) counters[c] = 0u;
   if (tid < kXcdLists) ticket[tid] = 0u;
   if (tid == 0) {
     diag->timed_out = 0u;
@@ -492,6 +593,7 @@ __global__ __launch_bounds__(kThreads) void chunk_prologue(uint32_t* flags, int3
     diag->observed = 0u;
     diag->epoch = epoch;
     diag->abort = 0u;
+    diag->units_done = 0u;
   }
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "");
 }
@@ -504,7 +606,7 @@ using LoopF32_64 = F32Loop<64, 64>;
 
 template <class Loop, bool kOutBf16, bool kProducer>
 static hipError_t launch_one(const GemmArgs& args, int32_t grid, hipStream_t stream) {
-  hipLaunchKernelGGL((chunk_gemm<Loop, kOutBf16, kProducer>), dim3(grid), dim3(kThreads), 0, stream, args);
+  hipLaunchKernelGGL((chunk_gemm<Loop, kOutBf16, kProducer>), dim3(grid), dim3(Loop::THREADS), 0, stream, args);
   return hipGetLastError();
 }
 
@@ -519,12 +621,13 @@ struct Variant {
   bool out_bf16;
   bool producer;
   int bm, bn, bk;
+  int threads;
   hipError_t (*launch)(const GemmArgs&, int32_t, hipStream_t);
   const void* (*func)();
 };
 
 #define CSG_VARIANT(IN, LOOP, OB, PR) \
-  Variant { IN, OB, PR, LOOP::BM, LOOP::BN, LOOP::BK, &launch_one<LOOP, OB, PR>, &kernel_ptr<LOOP, OB, PR> }
+  Variant { IN, OB, PR, LOOP::BM, LOOP::BN, LOOP::BK, LOOP::THREADS, &launch_one<LOOP, OB, PR>, &kernel_ptr<LOOP, OB, PR> }
 
 const Variant kVariants[] = {
     CSG_VARIANT(InType::BF16, LoopBf16_256, true, false),  CSG_VARIANT(InType::BF16, LoopBf16_256, true, true),
@@ -551,7 +654,7 @@ hipError_t kernel_grid(const KernelKey& key, int device, int32_t* grid) {
   int cus = 0, per_cu = 0;
   hipError_t e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device);
   if (e != hipSuccess) return e;
-  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, v->func(), kThreads, 0);
+  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, v->func(), v->threads, 0);
   if (e != hipSuccess) return e;
   if (per_cu < 1) per_cu = 1;
   *grid = cus * per_cu;
@@ -564,11 +667,10 @@ hipError_t launch_chunk_gemm(const KernelKey& key, const GemmArgs& args, int32_t
   return v->launch(args, grid, stream);
 }
 
-hipError_t launch_prologue(uint32_t* flags, int32_t n_chunks, uint32_t epoch, int32_t preset_all, int32_t clear_flags,
-                           uint32_t* counters, uint32_t* ticket, DeviceDiag* diag, uint32_t* slot_count,
-                           int32_t n_slots, hipStream_t stream) {
-  hipLaunchKernelGGL(chunk_prologue, dim3(1), dim3(kThreads), 0, stream, flags, n_chunks, epoch, preset_all,
-                     clear_flags, counters, ticket, diag, slot_count, n_slots);
+hipError_t launch_prologue(uint32_t* counters, int32_t n_chunks, uint32_t epoch, uint32_t* ticket, DeviceDiag* diag,
+                           uint32_t* slot_count, int32_t n_slots, hipStream_t stream) {
+  hipLaunchKernelGGL(chunk_prologue, dim3(1), dim3(kPrologueThreads), 0, stream, counters, n_chunks, epoch, ticket, diag,
+                     slot_count, n_slots);
   return hipGetLastError();
 }
 

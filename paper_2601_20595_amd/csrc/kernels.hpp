@@ -15,7 +15,8 @@ struct DeviceDiag {
   uint32_t observed;
   uint32_t epoch;
   uint32_t abort;     // set once any workgroup gave up; the others stop taking tiles
-  uint32_t pad[2];
+  uint32_t units_done;  // work units executed, summed over workgroups as they exit
+  uint32_t pad;
 };
 
 // One entry of the execution-ordered tile list.
@@ -27,7 +28,8 @@ struct TileDesc {
   int32_t group;      // expert index (grouped GEMM), else 0
   int32_t kt_begin;   // first K step (units of the tile's BK)
   int32_t kt_end;     // one past the last K step
-  int32_t slot;       // split tiles: workspace slot (the tile's raster id); -1 if not split
+  int32_t slot;       // split tiles: workspace index of the tile's first slice (its slices are
+                      // consecutive); -1 if not split
   int32_t slice;      // split tiles: slice index | (number of slices << 16)
 };
 
@@ -41,20 +43,35 @@ struct GemmArgs {
   const int32_t* list_ptr;   // [n_tiles + 1]: per execution position, its chunks
   const int32_t* list_ids;   // consumer: remote chunks to wait for; producer: chunks written
   const int32_t* raster;     // [n_tiles] raster id per execution position (diagnostics)
-  uint32_t* flags;           // consumer: per-chunk ready flags
+  const int64_t* const* ready;  // consumer: per chunk, the value a copy engine brings to 0 once
+                                // the chunk has landed (local chunks point at a 0)
   uint32_t* counters;        // producer: finished tiles per chunk
   const int32_t* need;       // producer: tiles per chunk
   uint32_t* out_flags;       // producer: per-chunk completion flags (host-visible memory)
   uint32_t* ticket;          // [kXcdLists] tickets, one per tile sub-list
   const int32_t* list_begin; // [kXcdLists + 1]: sub-list x is positions [list_begin[x], list_begin[x+1])
   DeviceDiag* diag;
-  float* ws;                 // split-K partial sums: [slot][slice][BM * BN] fp32, thread-major
-  uint32_t* slot_count;      // split-K: finished slices per slot
+  float* ws;                 // split-K partial sums: [slice buffer][BM * BN] fp32, thread-major
+  uint32_t* slot_count;      // split-K: finished slices per tile (by raster id)
   uint64_t timeout_ticks;    // bound of one flag wait, in 100 MHz wall-clock ticks
-  uint32_t epoch;            // a flag is ready when it is >= epoch
+  uint32_t epoch;            // call number: the value the producer's emitted flags take
   int32_t n_tiles;
   int32_t n_chunks;
   int32_t dynamic_ticket;
+  // Consumers: 1 if a cache line of A may hold rows of two chunks (a chunk boundary
+  // or the buffer start not on a 128-byte line), so a line cached while one chunk was
+  // ready could hold stale rows of the next; then a workgroup drops its caches when
+  // it first sees a chunk ready. With line-aligned chunks no line of a chunk is read
+  // before its flag, and lines cached by earlier work are dropped at kernel launch.
+  int32_t acquire_fresh;
+  // 1: a workgroup whose die's sub-list is exhausted takes entries of other dies'
+  // lists. 0: every entry runs on its own die, so the slices of a split tile share
+  // that die's L2 and exchange partial sums through it without L2 maintenance.
+  int32_t steal;
+  // Optional (nullptr = off): per execution position, 4 words written by the
+  // workgroup that ran it: wall-clock ticks (100 MHz) when it took the position,
+  // when its waits were over, when it finished, and (die << 32 | workgroup id).
+  uint64_t* trace;
 };
 
 enum class InType : int32_t { BF16 = 0, F32 = 1 };
@@ -79,11 +96,10 @@ int32_t kernel_max_chunks();
 hipError_t kernel_grid(const KernelKey& key, int device, int32_t* grid);
 hipError_t launch_chunk_gemm(const KernelKey& key, const GemmArgs& args, int32_t grid, hipStream_t stream);
 
-// Per-call set-up on the compute stream: clears counters, the tickets, the split-K
-// slot counts and the diagnostics, and pre-sets (compute-only) or clears (epoch
-// wrap) the ready flags.
-hipError_t launch_prologue(uint32_t* flags, int32_t n_chunks, uint32_t epoch, int32_t preset_all, int32_t clear_flags,
-                           uint32_t* counters, uint32_t* ticket, DeviceDiag* diag, uint32_t* slot_count,
-                           int32_t n_slots, hipStream_t stream);
+// Per-call set-up on the compute stream: clears the producer's per-chunk counters
+// (counters may be nullptr), the tickets, the split-K slot counts and the
+// diagnostics.
+hipError_t launch_prologue(uint32_t* counters, int32_t n_chunks, uint32_t epoch, uint32_t* ticket, DeviceDiag* diag,
+                           uint32_t* slot_count, int32_t n_slots, hipStream_t stream);
 
 }  // namespace csg

@@ -31,6 +31,20 @@ class SdmaEngines {
   void close();
 
   int count() const { return static_cast<int>(engines_.size()); }
+  // Completion signal for copies, consumed by GPU agents only: the runtime makes it
+  // without an interrupt event (which costs the engines several microseconds per
+  // copy), and its value may be read by kernels through signal_value_ptr. The calling
+  // thread polls the value too.
+  hsa_status_t make_signal(hsa_signal_value_t initial, hsa_signal_t* out) const {
+    return hsa_amd_signal_create(initial, 0, nullptr, HSA_AMD_SIGNAL_AMD_GPU_ONLY, out);
+  }
+  // Address of a signal's value, for kernels to poll.
+  static hsa_status_t signal_value_ptr(hsa_signal_t s, const int64_t** out) {
+    volatile hsa_signal_value_t* vp = nullptr;
+    const hsa_status_t st = hsa_amd_signal_value_pointer(s, &vp);
+    *out = const_cast<const int64_t*>(reinterpret_cast<volatile int64_t*>(vp));
+    return st;
+  }
   bool is_open() const { return opened_; }
 
   // Copy `bytes` from src to dst on engine `engine % count()`. The copy starts once

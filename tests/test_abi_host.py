@@ -147,6 +147,13 @@ def test_validation_errors():
     # bad configuration
     assert _status(csg.Plan, "ag", 128, 64, 64, "bf16", "bf16", s, cfg={"copy_engines": 99}, device=-1) \
         == csg.CSG_ERR_INVALID
+    assert _status(csg.Plan, "ag", 128, 64, 64, "bf16", "bf16", s, cfg={"tail_split": -1}, device=-1) \
+        == csg.CSG_ERR_INVALID
+    # split tiles stay on their die: a given grid must cover every die evenly
+    assert _status(csg.Plan, "ag", 128, 64, 64, "bf16", "bf16", s, cfg={"split_k": 2, "num_workgroups": 12},
+                   device=-1) == csg.CSG_ERR_INVALID
+    assert _status(csg.Plan, "ag", 128, 64, 64, "bf16", "bf16", s, cfg={"split_k": 2, "num_workgroups": 16},
+                   device=-1) == csg.CSG_OK
 
 
 def test_host_only_plan_cannot_run_and_delays_are_checked():

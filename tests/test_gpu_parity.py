@@ -126,6 +126,40 @@ def test_poisoned_landing_in_cache_never_reaches_output():
         assert_close(out_to_f64(c, "bf16"), R, 2e-2, "poison iteration %d" % it)
 
 
+@pytest.mark.parametrize("case", [
+    # W, r, S, Q, kind, N, K, dtype, out, split
+    (4, 0, 256, 4, "ring", 768, 512, "bf16", "bf16", 1),     # 128-byte-aligned chunks: no acquire needed
+    (4, 0, 256, 4, "ring", 768, 512, "bf16", "bf16", 2),
+    (2, 1, 50, 2, "ring", 64, 16, "f32", "f32", 1),          # 64-byte rows, 25-row chunks: lines straddle chunks
+], ids=lambda c: "W%d-r%d-S%d-Q%d-%s-N%d-K%d-%s-%s-split%d" % c)
+def test_poisoned_landing_variants(case):
+    W, r, S, Q, kind, N, K, dtype, out_dtype, split = case
+    _say("poison variant %s" % (case,))
+    w, d, perm, chunks, order = _small_ag(W, r, S, Q, kind, N, K, dtype, out_dtype)
+    s = csg.Schedule.uniform(W, r, S, Q, kind)
+    plan = csg.Plan("ag", W * S, N, K, dtype, out_dtype, s, cfg={"timeout_ms": 1000, "split_k": split})
+    R = oracle.ag_gemm(d.A.device_array, d.B.device_array, chunks, order)
+    for it in range(3):
+        c, _ = run_ag(plan, chunks, d.A, d.B, out_dtype, poison_remote=True, touch_remote=True)
+        assert_close(out_to_f64(c, out_dtype), R, tol_for(out_dtype, dtype), "poison iteration %d" % it)
+
+
+@pytest.mark.parametrize("split", [1, 2, 3])
+def test_plan_reuse_with_new_inputs(split):
+    """The same plan, buffers reused, inputs changed between calls: a stale cache line
+    of the landing buffer or of the split-K partial sums would show as a mismatch."""
+    W, r, S, Q, N, K = 4, 1, 256, 2, 512, 640
+    _say("plan reuse split=%d" % split)
+    s = csg.Schedule.uniform(W, r, S, Q, "swizzle1d")
+    plan = csg.Plan("ag", W * S, N, K, "bf16", "bf16", s, cfg={"timeout_ms": 1000, "split_k": split})
+    st = streams()
+    for rep in range(3):
+        w, d, perm, chunks, order = _small_ag(W, r, S, Q, "swizzle1d", N, K, "bf16", "bf16", rep=rep)
+        R = oracle.ag_gemm(d.A.device_array, d.B.device_array, chunks, order)
+        c, _ = run_ag(plan, chunks, d.A, d.B, "bf16", st=st)
+        assert_close(out_to_f64(c, "bf16"), R, 2e-2, "rep %d" % rep)
+
+
 def test_repeated_calls_reuse_the_plan():
     W, r, S, Q, N, K = 4, 2, 256, 2, 512, 256
     _say("repeated calls")
@@ -231,6 +265,62 @@ def test_ag_split_k_and_dispatch_parity(case):
     # the slices are added in a fixed order: repeated calls give the same bits
     c2, _ = run_ag(plan, chunks, d.A, d.B, out_dtype, repeats=3)
     assert torch.equal(c.cpu(), c2.cpu())
+
+
+TAIL_CASES = [
+    # op, W, r, S, Q, kind, N, K, cfg
+    ("ag", 4, 0, 300, 2, "ring", 600, 512, {"tail_split": 2, "tail_chunks": 2}),
+    ("ag", 2, 1, 512, 1, "permutation", 256, 1024, {"tail_split": 4, "tail_chunks": 1}),
+    ("ag", 4, 3, 256, 4, "swizzle1d", 520, 640, {"split_k": 2, "tail_split": 3, "tail_chunks": 5}),
+    ("ag", 4, 0, 256, 4, "ring", 512, 512, {"tail_split": 2, "tail_chunks": 4, "num_workgroups": 8}),
+    ("rs", 4, 1, 256, 2, "rs_ring", 512, 640, {"tail_split": 2, "tail_chunks": 3}),
+]
+
+
+@pytest.mark.parametrize("case", TAIL_CASES, ids=lambda c: "%s-W%d-r%d-S%d-Q%d-%s-N%d-K%d-%s" % (
+    c[:8] + ("_".join("%s%d" % kv for kv in sorted(c[8].items())),)))
+def test_tail_split_parity(case):
+    """Tiles on the critical path split along K (the rest whole): same result, to the
+    same bar, and every work unit ran."""
+    op, W, r, S, Q, kind, N, K, cfg = case
+    _say("tail split %s" % (case,))
+    cfg = dict(cfg, timeout_ms=1000)
+    if op == "rs":
+        w = si.Workload(103, "rs", "rs", M=W * S, N=N, K=K, dtype="bf16", out_dtype="bf16", dist="normal", world=W,
+                        rank=r, shard_rows=S, chunks_per_shard=Q, order="rs_ring")
+        d = si.draw(w)
+        chunks, order = oracle.uniform_schedule(W, r, S, Q, "rs_ring")
+        plan = csg.Plan("rs", W * S, N, K, "bf16", "bf16", csg.Schedule.uniform(W, r, S, Q, "rs_ring"), cfg=cfg)
+        c, out = run_rs(plan, d.A, d.B, "bf16")
+        R, _, _ = oracle.gemm_rs(d.A.device_array, d.B.device_array, chunks, order)
+        G = out_to_f64(c, "bf16")
+        assert_close(G, R, 2e-2, "rs tail")
+        O = out_to_f64(out, "bf16")
+        for ch in chunks:
+            if not ch.is_local:
+                assert np.array_equal(O[ch.row_begin:ch.row_end], G[ch.row_begin:ch.row_end])
+        return
+    w, d, perm, chunks, order = _small_ag(W, r, S, Q, kind, N, K, "bf16", "bf16")
+    plan = csg.Plan("ag", W * S, N, K, "bf16", "bf16", csg.Schedule.uniform(W, r, S, Q, kind, perm), cfg=cfg)
+    R = oracle.ag_gemm(d.A.device_array, d.B.device_array, chunks, order)
+    for mode in ("overlap", "compute_only"):
+        c, _ = run_ag(plan, chunks, d.A, d.B, "bf16", mode=mode)
+        assert_close(out_to_f64(c, "bf16"), R, 2e-2, "ag tail %s" % mode)
+
+
+def test_grouped_tail_split_parity():
+    _say("grouped tail split")
+    W, E, N, K = 4, 3, 264, 512
+    counts = np.array([[70, 0, 5], [0, 3, 1], [130, 0, 0], [1, 2, 300]], dtype=np.int64)
+    chunks, order, gr = oracle.grouped_schedule(W, 3, counts)
+    M = int(sum(gr))
+    X = si.draw_matrix(106, 0, 0, (M, K), "normal", "bf16")
+    B = si.draw_matrix(106, 1, 0, (E, N, K), "normal", "bf16")
+    plan = csg.Plan("grouped", M, N, K, "bf16", "bf16", csg.Schedule.grouped(W, 3, counts), group_rows=gr,
+                    cfg={"timeout_ms": 1000, "tail_split": 4, "tail_chunks": 3})
+    c, _ = run_ag(plan, chunks, X, B, "bf16")
+    R = oracle.grouped_gemm(X.device_array, B.device_array, chunks, order)
+    assert_close(out_to_f64(c, "bf16"), R, 2e-2, "grouped tail")
 
 
 @pytest.mark.parametrize("split", [2, 5])
