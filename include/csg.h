@@ -100,7 +100,10 @@ typedef struct {
  *                   on one die (they exchange partial sums through its L2), so its
  *                   num_workgroups, if given, must be a multiple of 8
  *   trace           1 = the kernel records when each work unit was taken, started and
- *                   finished (read back with csg_plan_trace); 0 = off */
+ *                   finished (read back with csg_plan_trace); 0 = off
+ *   warm_rows       consumers: 0 or 1 = a workgroup that sees a chunk land first loads
+ *                   its share of the tile's A rows into the caches before computing
+ *                   (copy-engine writes leave the rows only in HBM); 2 = off */
 typedef struct {
     int32_t bm, bn, bk;
     int32_t intra_order;
@@ -112,6 +115,7 @@ typedef struct {
     int32_t tail_split;
     int32_t tail_chunks;
     int32_t trace;
+    int32_t warm_rows;
 } csg_plan_cfg;
 
 typedef struct csg_schedule csg_schedule;
@@ -131,7 +135,8 @@ typedef struct {
  * plan with tracing on, in execution-list order. Times are device wall-clock ticks
  * (100 MHz): when a workgroup took the unit, when the unit's chunk waits were over,
  * and when the unit finished (its output stored, or its partial sums for a slice
- * that was not the last). */
+ * that was not the last), and the shader-clock cycles in between, so that
+ * cycles / (t_end - t_start) * 100 MHz is the clock the unit ran at. */
 typedef struct {
     int32_t raster;         /* raster id of the tile */
     int32_t slice;          /* K-slice index */
@@ -140,6 +145,7 @@ typedef struct {
     int32_t workgroup;      /* workgroup id */
     int32_t reserved;
     uint64_t t_take, t_start, t_end;
+    uint64_t cycles;        /* shader-clock cycles from t_start to t_end */
 } csg_trace_unit;
 
 /* Diagnostics of the last call on a plan (filled by csg_plan_check). */

@@ -69,7 +69,7 @@ class csg_plan_cfg(ctypes.Structure):
                 ("intra_order", ctypes.c_int32), ("tile_dispatch", ctypes.c_int32),
                 ("num_workgroups", ctypes.c_int32), ("copy_engines", ctypes.c_int32), ("timeout_ms", ctypes.c_int32),
                 ("split_k", ctypes.c_int32), ("tail_split", ctypes.c_int32), ("tail_chunks", ctypes.c_int32),
-                ("trace", ctypes.c_int32)]
+                ("trace", ctypes.c_int32), ("warm_rows", ctypes.c_int32)]
 
 
 class csg_plan_info(ctypes.Structure):
@@ -81,7 +81,8 @@ class csg_plan_info(ctypes.Structure):
 class csg_trace_unit(ctypes.Structure):
     _fields_ = [("raster", ctypes.c_int32), ("slice", ctypes.c_int32), ("n_slices", ctypes.c_int32),
                 ("xcd", ctypes.c_int32), ("workgroup", ctypes.c_int32), ("reserved", ctypes.c_int32),
-                ("t_take", ctypes.c_uint64), ("t_start", ctypes.c_uint64), ("t_end", ctypes.c_uint64)]
+                ("t_take", ctypes.c_uint64), ("t_start", ctypes.c_uint64), ("t_end", ctypes.c_uint64),
+                ("cycles", ctypes.c_uint64)]
 
 
 class csg_diag(ctypes.Structure):
@@ -331,13 +332,14 @@ def csg_plan_kernel_times(plan: int, n: int = 256) -> np.ndarray:
 
 def csg_plan_trace(plan: int, n: int) -> np.ndarray:
     """Trace of the plan's last kernel run: a structured array with fields raster,
-    slice, n_slices, xcd, workgroup, t_take, t_start, t_end (100 MHz ticks)."""
+    slice, n_slices, xcd, workgroup, t_take, t_start, t_end (100 MHz ticks) and cycles
+    (shader clock, t_start to t_end)."""
     buf = (csg_trace_unit * max(n, 1))()
     got = ctypes.c_int32(0)
     _check(_lib().csg_plan_trace(plan, buf, n, ctypes.byref(got)), "csg_plan_trace")
     dt = np.dtype([("raster", np.int32), ("slice", np.int32), ("n_slices", np.int32), ("xcd", np.int32),
                    ("workgroup", np.int32), ("reserved", np.int32), ("t_take", np.uint64), ("t_start", np.uint64),
-                   ("t_end", np.uint64)])
+                   ("t_end", np.uint64), ("cycles", np.uint64)])
     return np.frombuffer(bytes(buf), dtype=dt, count=got.value).copy()
 
 

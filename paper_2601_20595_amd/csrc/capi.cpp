@@ -295,8 +295,9 @@ csg_status setup_device(csg_plan* p) {
     CSG_HIP(hipMemset(p->d_slot_count, 0, static_cast<size_t>(n_tiles) * 4));
   }
   if (p->cfg.trace) {
-    CSG_HIP(hipMalloc(&p->d_trace, static_cast<size_t>(std::max(n_units, 1)) * 4 * sizeof(uint64_t)));
-    CSG_HIP(hipMemset(p->d_trace, 0, static_cast<size_t>(std::max(n_units, 1)) * 4 * sizeof(uint64_t)));
+    const size_t words = static_cast<size_t>(std::max(n_units, 1)) * csg::kTraceWords;
+    CSG_HIP(hipMalloc(&p->d_trace, words * sizeof(uint64_t)));
+    CSG_HIP(hipMemset(p->d_trace, 0, words * sizeof(uint64_t)));
   }
   CSG_HIP(hipMalloc(&p->d_diag, sizeof(csg::DeviceDiag)));
   CSG_HIP(hipMemset(p->d_diag, 0, sizeof(csg::DeviceDiag)));
@@ -452,7 +453,7 @@ csg_status finish_copies(csg_plan* p, size_t issued) {
   return CSG_OK;
 }
 
-csg_status launch_gemm(csg_plan* p, const void* A, const void* B, void* C, hipStream_t compute) {
+csg_status launch_gemm(csg_plan* p, const void* A, const void* B, void* C, csg_mode mode, hipStream_t compute) {
   csg::GemmArgs a{};
   a.A = A;
   a.B = B;
@@ -481,6 +482,9 @@ csg_status launch_gemm(csg_plan* p, const void* A, const void* B, void* C, hipSt
   a.dynamic_ticket = p->cfg.tile_dispatch == 2 ? 0 : 1;
   a.steal = (p->ws_slices > 0 && a.dynamic_ticket) ? 0 : 1;
   a.trace = p->d_trace;
+  // only copies of this call leave rows fresh in HBM; without them the warm-up loads
+  // would only cost time
+  a.n_tiles_n = (p->consumer() && mode == CSG_MODE_OVERLAP && p->cfg.warm_rows != 2) ? p->map.n_tiles_n : 0;
   a.acquire_fresh = (p->consumer() && (!p->lines_aligned || reinterpret_cast<uintptr_t>(A) % 128 != 0)) ? 1 : 0;
   const int slot = static_cast<int>(p->n_launches % kTimingRing);
   CSG_HIP(hipEventRecord(p->ev_k0[slot], compute));
@@ -538,7 +542,7 @@ csg_status consumer_call(csg_plan* p, void* landing, const void* staging, const 
   if (st != CSG_OK) return st;
   // the kernel is queued first: it starts as soon as the previous kernel ends and
   // waits for its chunks, while the host releases the copies
-  if (mode != CSG_MODE_COPY_ONLY && (st = launch_gemm(p, landing, b, c, compute)) != CSG_OK) return st;
+  if (mode != CSG_MODE_COPY_ONLY && (st = launch_gemm(p, landing, b, c, mode, compute)) != CSG_OK) return st;
   if (mode == CSG_MODE_COMPUTE_ONLY || p->remote_order.empty()) return CSG_OK;
   // the landing rows are rewritten: the previous kernel must be done reading them
   if ((st = ready_copies(p, copy, cs, true)) != CSG_OK) return st;
@@ -677,7 +681,7 @@ csg_status csg_plan_create(csg_op op, int64_t M, int64_t N, int64_t K, csg_dtype
   if (c.split_k == 0) c.split_k = 1;
   if (c.bm < 1 || c.bn < 1 || c.bk < 1 || c.copy_engines < 0 || c.copy_engines > 32 || c.timeout_ms < 1 ||
       c.split_k < 1 || c.split_k > 64 || c.tail_split < 0 || c.tail_split > 64 || c.tail_chunks < 0 ||
-      c.trace < 0 || c.trace > 1 ||
+      c.trace < 0 || c.trace > 1 || c.warm_rows < 0 || c.warm_rows > 2 ||
       c.num_workgroups < 0 || c.tile_dispatch < 0 || c.tile_dispatch > 2 || c.intra_order != 0)
     return fail(CSG_ERR_INVALID, "bad plan configuration");
   // split tiles run every slice on their own die (no stealing): every die needs
@@ -832,7 +836,7 @@ csg_status csg_gemm_rs(csg_plan* p, const void* a, const void* b_nk, void* c, vo
   CallState cs;
   csg_status st = begin_call(p, mode, compute, &cs);
   if (st != CSG_OK) return st;
-  if (mode != CSG_MODE_COPY_ONLY && (st = launch_gemm(p, a, b_nk, c, compute)) != CSG_OK) return st;
+  if (mode != CSG_MODE_COPY_ONLY && (st = launch_gemm(p, a, b_nk, c, mode, compute)) != CSG_OK) return st;
   if (mode == CSG_MODE_COMPUTE_ONLY || p->remote_order.empty()) return CSG_OK;
   // copy-only reads the C a previous kernel wrote: that kernel must have finished
   if ((st = ready_copies(p, copy, cs, mode == CSG_MODE_COPY_ONLY)) != CSG_OK) return st;
@@ -903,7 +907,8 @@ csg_status csg_plan_trace(csg_plan* p, csg_trace_unit* units_host, int32_t n, in
   if (g.err != hipSuccess) return hip_fail(g.err, "hipSetDevice");
   CSG_HIP(hipEventSynchronize(p->ev_k1[(p->n_launches - 1) % kTimingRing]));
   const int32_t m = std::min(n, p->n_units);
-  std::vector<uint64_t> words(static_cast<size_t>(m) * 4);
+  constexpr int W = csg::kTraceWords;
+  std::vector<uint64_t> words(static_cast<size_t>(m) * W);
   if (m > 0) {
     CSG_HIP(hipMemcpyAsync(words.data(), p->d_trace, words.size() * sizeof(uint64_t), hipMemcpyDeviceToHost, p->aux));
     CSG_HIP(hipStreamSynchronize(p->aux));
@@ -914,12 +919,13 @@ csg_status csg_plan_trace(csg_plan* p, csg_trace_unit* units_host, int32_t n, in
     r.raster = p->unit_raster[i];
     r.slice = u.slice & 0xffff;
     r.n_slices = u.slice >> 16;
-    r.xcd = static_cast<int32_t>(words[4 * i + 3] >> 32);
-    r.workgroup = static_cast<int32_t>(words[4 * i + 3] & 0xffffffffu);
+    r.xcd = static_cast<int32_t>(words[W * i + 3] >> 32);
+    r.workgroup = static_cast<int32_t>(words[W * i + 3] & 0xffffffffu);
     r.reserved = 0;
-    r.t_take = words[4 * i + 0];
-    r.t_start = words[4 * i + 1];
-    r.t_end = words[4 * i + 2];
+    r.t_take = words[W * i + 0];
+    r.t_start = words[W * i + 1];
+    r.t_end = words[W * i + 2];
+    r.cycles = words[W * i + 5] - words[W * i + 4];
   }
   *n_out = m;
   return CSG_OK;

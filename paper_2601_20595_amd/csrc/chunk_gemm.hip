@@ -89,7 +89,9 @@ __device__ int wait_chunks(const GemmArgs& a, int pos, uint32_t* ready_bits) {
         __hip_atomic_store(&a.diag->abort, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
         return -1;
       }
-      __builtin_amdgcn_s_sleep(2);
+      // about 1 us between polls: every waiting workgroup polls words of one page,
+      // and faster polling loads that memory channel for no gain
+      __builtin_amdgcn_s_sleep(32);
       v = load_ready(rp);
     }
     ready_bits[c >> 5] |= bit;
@@ -156,6 +158,31 @@ __device__ __forceinline__ void dma16(const __amdgpu_buffer_rsrc_t& rs, uint32_t
 // Waits until every vector-memory operation of this wave has completed (loads landed,
 // stores acknowledged).
 __device__ __forceinline__ void wait_dma_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Pulls part `part` of `parts` of [0, bytes) of a buffer into the caches: one 4-byte
+// load per 128-byte line, written to this wave's 256-byte scratch area of LDS (so no
+// register waits for it; the next wait for the wave's loads covers it). Rows that a
+// copy engine has just written are not in any cache, and a main loop that finds them
+// only in HBM stalls on every K step; the tiles that consume a fresh chunk together
+// (one per column tile) each warm one part of its rows first.
+template <int kThreads>
+__device__ __forceinline__ void warm_lines(const __amdgpu_buffer_rsrc_t& rs, int64_t bytes, int part, int parts,
+                                           uint32_t lds_scratch, int tid) {
+  const int lines = static_cast<int>(bytes >> 7);
+  const int lo = static_cast<int>(static_cast<int64_t>(lines) * part / parts);
+  const int hi = static_cast<int>(static_cast<int64_t>(lines) * (part + 1) / parts);
+  for (int i = lo + tid; i < hi; i += kThreads) {
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %1\n\t"
+        "buffer_load_dword %2, %3, 0 offen lds\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "s"(lds_scratch), "v"(i << 7), "s"(rs)
+        : "memory");
+  }
+}
 
 template <int BM_, int BN_>
 struct Bf16Loop {
@@ -400,6 +427,7 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
   constexpr int MI = Loop::MI, NI = Loop::NI;
   __shared__ __attribute__((aligned(16))) unsigned char lds[Loop::LDS_BYTES];
   __shared__ uint32_t ready_bits[kMaxChunks / 32];
+  __shared__ __attribute__((aligned(16))) uint32_t warm_scratch[kThreads];  // target of warm_lines
   __shared__ int s_pos;
   __shared__ int s_state;
 
@@ -426,9 +454,10 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
         if (load_flag(&a.diag->abort)) state = -1;
         else if (!kProducer) state = wait_chunks(a, pos, ready_bits);
         if (a.trace) {
-          a.trace[4 * pos + 0] = t_take;
-          a.trace[4 * pos + 1] = wall_clock64();
-          a.trace[4 * pos + 3] = (static_cast<uint64_t>(xcd) << 32) | blockIdx.x;
+          a.trace[kTraceWords * pos + 0] = t_take;
+          a.trace[kTraceWords * pos + 1] = wall_clock64();
+          a.trace[kTraceWords * pos + 3] = (static_cast<uint64_t>(xcd) << 32) | blockIdx.x;
+          a.trace[kTraceWords * pos + 4] = clock64();
         }
       }
       s_pos = pos;
@@ -457,6 +486,20 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
            (static_cast<int64_t>(td.group) * a.b_group_stride + col0 * a.K + k0) * in_bytes;
     g.abytes = (static_cast<int64_t>(g.arows) * a.K - k0) * in_bytes;
     g.bbytes = (static_cast<int64_t>(g.brows) * a.K - k0) * in_bytes;
+
+    if (!kProducer && s_state > 0 && a.n_tiles_n > 0) {
+      // this workgroup saw one of the tile's chunks land just now: warm its share of
+      // the tile's A rows (all K columns), shared with the other column tiles and
+      // K-slices
+      const int64_t panel = static_cast<int64_t>(g.arows) * a.K * in_bytes;
+      const __amdgpu_buffer_rsrc_t rsP =
+          make_rsrc(static_cast<const unsigned char*>(a.A) + static_cast<int64_t>(td.row_begin) * a.K * in_bytes, panel);
+      const uint32_t scratch = __builtin_amdgcn_readfirstlane(
+          static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_ptr_t)warm_scratch)) + wave * 256);
+      // the K-slices of a split tile share their tile's part
+      const int ns = td.slice >> 16, sl = td.slice & 0xffff;
+      warm_lines<kThreads>(rsP, panel, (td.n_tile % a.n_tiles_n) * ns + sl, a.n_tiles_n * ns, scratch, tid);
+    }
 
     f32x16 acc[MI][NI];
 #pragma unroll
@@ -535,7 +578,10 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
                                           __HIP_MEMORY_SCOPE_AGENT) == static_cast<uint32_t>(nslices - 1));
       __syncthreads();
       if (!s_state) {
-        if (a.trace && tid == 0) a.trace[4 * pos + 2] = wall_clock64();
+        if (a.trace && tid == 0) {
+          a.trace[kTraceWords * pos + 2] = wall_clock64();
+          a.trace[kTraceWords * pos + 5] = clock64();
+        }
         continue;
       }
       if (a.steal) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
@@ -573,7 +619,10 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
         }
       }
     }
-    if (a.trace && tid == 0) a.trace[4 * pos + 2] = wall_clock64();
+    if (a.trace && tid == 0) {
+      a.trace[kTraceWords * pos + 2] = wall_clock64();
+      a.trace[kTraceWords * pos + 5] = clock64();
+    }
   }
   if (tid == 0) atomicAdd(&a.diag->units_done, units);
 }

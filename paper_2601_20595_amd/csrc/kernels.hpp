@@ -64,15 +64,21 @@ struct GemmArgs {
   // it first sees a chunk ready. With line-aligned chunks no line of a chunk is read
   // before its flag, and lines cached by earlier work are dropped at kernel launch.
   int32_t acquire_fresh;
+  // Consumers: tiles along N (> 0: a workgroup that sees a chunk land first warms its
+  // share, 1 / n_tiles_n, of the tile's A rows; 0: off).
+  int32_t n_tiles_n;
   // 1: a workgroup whose die's sub-list is exhausted takes entries of other dies'
   // lists. 0: every entry runs on its own die, so the slices of a split tile share
   // that die's L2 and exchange partial sums through it without L2 maintenance.
   int32_t steal;
-  // Optional (nullptr = off): per execution position, 4 words written by the
-  // workgroup that ran it: wall-clock ticks (100 MHz) when it took the position,
-  // when its waits were over, when it finished, and (die << 32 | workgroup id).
+  // Optional (nullptr = off): per execution position, kTraceWords words written by
+  // the workgroup that ran it: wall-clock ticks (100 MHz) when it took the position,
+  // when its waits were over, when it finished, (die << 32 | workgroup id), and the
+  // shader-clock counter when its waits were over and when it finished.
   uint64_t* trace;
 };
+
+constexpr int kTraceWords = 6;
 
 enum class InType : int32_t { BF16 = 0, F32 = 1 };
 
