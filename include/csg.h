@@ -24,7 +24,8 @@
  *     weights are E x N x K. dtype CSG_BF16 elements are raw bfloat16 bit
  *     patterns (uint16), CSG_F32 are IEEE binary32.
  *   - Objects (schedules, plans) are not thread-safe; distinct objects are
- *     independent.
+ *     independent. Successive calls on one plan must pass the same compute stream:
+ *     the plan's per-call state is reset in that stream's order.
  */
 #ifndef CSG_H_
 #define CSG_H_

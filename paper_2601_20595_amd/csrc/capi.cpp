@@ -124,7 +124,10 @@ struct csg_plan {
   uint32_t* d_counters = nullptr;
   uint32_t* d_ticket = nullptr;
   csg::DeviceDiag* d_diag = nullptr;
-  uint32_t* h_out_flags = nullptr;     // coherent host memory (reduce-scatter completion flags)
+  uint32_t* h_out_flags = nullptr;     // coherent host memory, per chunk: the producer's emitted
+                                       // flags; consumers: the call whose kernel has finished reading
+                                       // the chunk's rows
+  uint32_t last_kernel_epoch = 0;      // call number of the latest kernel launched (0: none)
   uint32_t* h_out_flags_dev = nullptr; // its device address
   uint32_t* d_scratch = nullptr;       // target of the engines' warm-up copies
   csg::SdmaEngines sdma;
@@ -273,8 +276,13 @@ csg_status setup_device(csg_plan* p) {
   p->lines_aligned = true;
   for (const csg::ChunkDesc& c : p->sched.chunks)
     if ((c.row_begin * p->K * in_bytes(p)) % 128 != 0) p->lines_aligned = false;
-  std::vector<int32_t> need(p->n_chunks());
-  for (int32_t c = 0; c < p->n_chunks(); ++c) need[c] = m.chunk_ptr[c + 1] - m.chunk_ptr[c];
+  // per chunk: tiles that write it (producer), or work units that read it (consumers:
+  // the units of split tiles each read the chunk's rows for their K range)
+  std::vector<int32_t> need(p->n_chunks(), 0);
+  if (p->consumer())
+    for (int32_t c : lids) ++need[c];
+  else
+    for (int32_t c = 0; c < p->n_chunks(); ++c) need[c] = m.chunk_ptr[c + 1] - m.chunk_ptr[c];
   csg_status st;
   if ((st = upload(&p->d_tiles, tiles)) != CSG_OK) return st;
   if ((st = upload(&p->d_list_ptr, lptr)) != CSG_OK) return st;
@@ -416,7 +424,7 @@ csg_status begin_call(csg_plan* p, csg_mode mode, hipStream_t compute, CallState
     for (hsa_signal_t sgn : p->sig_ready[set]) hsa_signal_store_relaxed(sgn, v);
     std::atomic_thread_fence(std::memory_order_seq_cst);  // armed before the kernel launch below
   }
-  CSG_HIP(csg::launch_prologue(p->consumer() ? nullptr : p->d_counters, p->n_chunks(), p->epoch, p->d_ticket,
+  CSG_HIP(csg::launch_prologue(p->d_counters, p->n_chunks(), p->epoch, p->d_ticket,
                                p->d_diag, p->d_slot_count, p->ws_slices > 0 ? p->map.n_tiles() : 0, compute));
   CSG_HIP(hipEventRecord(p->ev_prologue, compute));
   p->kernel_pending[p->epoch & 1] = false;
@@ -493,24 +501,54 @@ csg_status launch_gemm(csg_plan* p, const void* A, const void* B, void* C, csg_m
   ++p->n_launches;
   CSG_HIP(hipEventRecord(p->ev_kernel_done[p->epoch & 1], compute));
   p->kernel_pending[p->epoch & 1] = true;
+  p->last_kernel_epoch = p->epoch;
   return CSG_OK;
 }
 
 // Consumer copies: staging -> landing per remote chunk, on engine (i mod engines)
 // for the i-th remote chunk in arrival order; each completes the chunk's (armed)
 // ready signal.
-csg_status issue_consumer_copies(csg_plan* p, void* landing, const void* staging) {
+csg_status issue_consumer_copies(csg_plan* p, void* landing, const void* staging, uint32_t prev_reader) {
   const int64_t row_bytes = p->K * in_bytes(p);
   const bool delayed = !p->delays_us.empty();
   const Clock::time_point t0 = Clock::now();
   double release_us = 0.0;
   const std::vector<hsa_signal_t>& sigs = call_signals(p);
+  const int prev_parity = static_cast<int>(prev_reader & 1);
+  bool prev_done = prev_reader == 0;
+  const auto budget = std::chrono::milliseconds(p->cfg.timeout_ms) * 4;
   for (size_t i = 0; i < p->remote_order.size(); ++i) {
     const int32_t cid = p->remote_order[i];
     const csg::ChunkDesc& c = p->sched.chunks[cid];
     if (delayed) {
       release_us += p->delays_us[i];
       spin_until(t0 + std::chrono::nanoseconds(static_cast<int64_t>(release_us * 1000.0)));
+    }
+    // write after read: the previous kernel must be done reading the chunk's rows; it
+    // reports that per chunk (consumed flags), and its completion event settles it
+    // for every chunk (also when it gave up early)
+    if (!prev_done) {
+      const volatile uint32_t* f = p->h_out_flags + cid;
+      const Clock::time_point tw = Clock::now();
+      uint32_t spins = 0;
+      while (*f < prev_reader) {
+        if ((++spins & 255u) == 0) {
+          const hipError_t q = hipEventQuery(p->ev_kernel_done[prev_parity]);
+          if (q == hipSuccess) {
+            prev_done = true;
+            break;
+          }
+          if (q != hipErrorNotReady) {
+            (void)finish_copies(p, i);
+            return hip_fail(q, "the previous call's kernel");
+          }
+        }
+        if (Clock::now() - tw > budget) {
+          (void)finish_copies(p, i);
+          p->host_diag = csg_diag{1, cid, -1, *f, p->epoch, 0};
+          return fail(CSG_ERR_TIMEOUT, "the previous kernel did not finish reading chunk %d in time", cid);
+        }
+      }
     }
     const int64_t off = c.row_begin * row_bytes;
     const int64_t bytes = (c.row_end - c.row_begin) * row_bytes;
@@ -538,15 +576,18 @@ csg_status consumer_call(csg_plan* p, void* landing, const void* staging, const 
   DeviceGuard g(p->device);
   if (g.err != hipSuccess) return hip_fail(g.err, "hipSetDevice");
   CallState cs;
+  // the kernel that last read the landing rows (before this call's own)
+  const uint32_t prev_reader = p->last_kernel_epoch;
   csg_status st = begin_call(p, mode, compute, &cs);
   if (st != CSG_OK) return st;
   // the kernel is queued first: it starts as soon as the previous kernel ends and
   // waits for its chunks, while the host releases the copies
   if (mode != CSG_MODE_COPY_ONLY && (st = launch_gemm(p, landing, b, c, mode, compute)) != CSG_OK) return st;
   if (mode == CSG_MODE_COMPUTE_ONLY || p->remote_order.empty()) return CSG_OK;
-  // the landing rows are rewritten: the previous kernel must be done reading them
-  if ((st = ready_copies(p, copy, cs, true)) != CSG_OK) return st;
-  return issue_consumer_copies(p, landing, staging);
+  // the landing rows are rewritten: issue_consumer_copies waits, chunk by chunk, until
+  // the kernel before this call's is done reading them
+  if ((st = ready_copies(p, copy, cs, false)) != CSG_OK) return st;
+  return issue_consumer_copies(p, landing, staging, prev_reader);
 }
 
 }  // namespace

@@ -507,6 +507,18 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
 #pragma unroll
       for (int j = 0; j < NI; ++j) acc[i][j] = f32x16{};
     Loop::run(lds, g, acc, wave, lane);
+    if (!kProducer && tid == 0) {
+      // every load of this unit has landed (the main loop ends on a wait and a
+      // barrier): count the unit against the remote chunks it read, and report a
+      // chunk whose last reader this was, so the next call may overwrite its rows
+      for (int p = a.list_ptr[pos]; p < a.list_ptr[pos + 1]; ++p) {
+        const int c = a.list_ids[p];
+        const uint32_t done =
+            __hip_atomic_fetch_add(a.counters + c, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) + 1u;
+        if (done == static_cast<uint32_t>(a.need[c]))
+          __hip_atomic_store(a.out_flags + c, a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+      }
+    }
 
     // Output run r = (i * NI + j) * 4 + q of this thread: accumulator elements
     // 4q..4q+3 of block (i, j), i.e. output row (i * 32 + lane % 32) and columns

@@ -45,9 +45,10 @@ struct GemmArgs {
   const int32_t* raster;     // [n_tiles] raster id per execution position (diagnostics)
   const int64_t* const* ready;  // consumer: per chunk, the value a copy engine brings to 0 once
                                 // the chunk has landed (local chunks point at a 0)
-  uint32_t* counters;        // producer: finished tiles per chunk
-  const int32_t* need;       // producer: tiles per chunk
-  uint32_t* out_flags;       // producer: per-chunk completion flags (host-visible memory)
+  uint32_t* counters;        // per chunk: producer: tiles written; consumers: units done reading it
+  const int32_t* need;       // per chunk: the count at which the chunk is complete
+  uint32_t* out_flags;       // per chunk, host-visible memory, set to epoch when complete:
+                             // producer: output rows written; consumers: rows read
   uint32_t* ticket;          // [kXcdLists] tickets, one per tile sub-list
   const int32_t* list_begin; // [kXcdLists + 1]: sub-list x is positions [list_begin[x], list_begin[x+1])
   DeviceDiag* diag;
@@ -102,9 +103,8 @@ int32_t kernel_max_chunks();
 hipError_t kernel_grid(const KernelKey& key, int device, int32_t* grid);
 hipError_t launch_chunk_gemm(const KernelKey& key, const GemmArgs& args, int32_t grid, hipStream_t stream);
 
-// Per-call set-up on the compute stream: clears the producer's per-chunk counters
-// (counters may be nullptr), the tickets, the split-K slot counts and the
-// diagnostics.
+// Per-call set-up on the compute stream: clears the per-chunk counters, the
+// tickets, the split-K slot counts and the diagnostics.
 hipError_t launch_prologue(uint32_t* counters, int32_t n_chunks, uint32_t epoch, uint32_t* ticket, DeviceDiag* diag,
                            uint32_t* slot_count, int32_t n_slots, hipStream_t stream);
 

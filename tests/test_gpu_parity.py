@@ -160,6 +160,45 @@ def test_plan_reuse_with_new_inputs(split):
         assert_close(out_to_f64(c, "bf16"), R, 2e-2, "rep %d" % rep)
 
 
+@pytest.mark.parametrize("split", [1, 2])
+def test_back_to_back_calls_into_one_landing_buffer(split):
+    """Two calls issued back to back with no synchronisation, the second copying
+    different remote rows into the same landing buffer: its copies of a chunk may
+    start only once the first call's kernel has read that chunk, so each output
+    matches its own inputs."""
+    W, r, S, Q, N, K = 4, 1, 256, 2, 512, 512
+    _say("back to back split=%d" % split)
+    s = csg.Schedule.uniform(W, r, S, Q, "ring")
+    chunks, order = oracle.uniform_schedule(W, r, S, Q, "ring")
+    plan = csg.Plan("ag", W * S, N, K, "bf16", "bf16", s, cfg={"timeout_ms": 1000, "split_k": split})
+    w, d1, _, _, _ = _small_ag(W, r, S, Q, "ring", N, K, "bf16", "bf16", rep=0)
+    _, d2, _, _, _ = _small_ag(W, r, S, Q, "ring", N, K, "bf16", "bf16", rep=1)
+    A1 = d1.A.device_array.copy()
+    A2 = d2.A.device_array.copy()
+    for ch in chunks:
+        if ch.is_local:                                   # the local shard is shared
+            A2[ch.row_begin:ch.row_end] = A1[ch.row_begin:ch.row_end]
+    st = streams()
+    landing = to_dev(A1).clone()
+    for ch in chunks:
+        if not ch.is_local:
+            landing[ch.row_begin:ch.row_end].zero_()
+    stage1, stage2, b = to_dev(A1), to_dev(A2), to_dev(d1.B.device_array)
+    c1, c2 = empty_out(W * S, N, "bf16"), empty_out(W * S, N, "bf16")
+    nan_fill_(c1)
+    nan_fill_(c2)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        plan.ag_gemm(landing, stage1, b, c1, "overlap", st.compute, st.copy)
+        plan.ag_gemm(landing, stage2, b, c2, "overlap", st.compute, st.copy)
+    plan.check()
+    torch.cuda.synchronize()
+    R1 = oracle.ag_gemm(A1, d1.B.device_array, chunks, order)
+    R2 = oracle.ag_gemm(A2, d1.B.device_array, chunks, order)
+    assert_close(out_to_f64(c1, "bf16"), R1, 2e-2, "first call")
+    assert_close(out_to_f64(c2, "bf16"), R2, 2e-2, "second call")
+
+
 def test_repeated_calls_reuse_the_plan():
     W, r, S, Q, N, K = 4, 2, 256, 2, 512, 256
     _say("repeated calls")
