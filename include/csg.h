@@ -260,9 +260,12 @@ csg_status csg_ag_gemm(csg_plan* p, void* a_landing, const void* a_staging, cons
 /* GEMM + ReduceScatter on one rank: the kernel computes C tiles in emission
  * order; the last tile of an output chunk releases the chunk's flag, and the
  * calling thread then copies the chunk by SDMA from c to c_outgoing (non-local
- * chunks only). The call returns when every copy has completed, i.e. shortly
- * after the kernel has emitted its last non-local chunk. In copy-only mode c must
- * already hold the output (the plan's previous kernel is waited for). */
+ * chunks only). The call returns once the kernel has emitted its last non-local
+ * chunk and every copy has been issued; the copies complete on their own. The next
+ * call's kernel waits for the copy out of a chunk before rewriting its rows of c, and
+ * csg_plan_check waits for all of them: call it (or csg_plan_destroy) before reading
+ * c_outgoing. In copy-only mode c must already hold the output (the plan's previous
+ * kernel is waited for). */
 csg_status csg_gemm_rs(csg_plan* p, const void* a, const void* b_nk, void* c, void* c_outgoing,
                        csg_mode mode, void* compute_stream, void* copy_stream);
 
@@ -273,7 +276,8 @@ csg_status csg_grouped_gemm(csg_plan* p, void* x_landing, const void* x_staging,
                             const void* b_enk, void* c, csg_mode mode, void* compute_stream,
                             void* copy_stream);
 
-/* Waits for the plan's last call to complete and reports its diagnostics.
+/* Waits for the plan's last call to complete (its kernel and every copy it issued)
+ * and reports its diagnostics.
  * CSG_ERR_TIMEOUT if a wait expired (details in *out); CSG_ERR_STATE if the kernel
  * finished without running every work unit (which only a grid that leaves a die
  * without workgroups can cause); CSG_OK otherwise. */

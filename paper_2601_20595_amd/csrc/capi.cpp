@@ -131,10 +131,12 @@ struct csg_plan {
   uint32_t* h_out_flags_dev = nullptr; // its device address
   uint32_t* d_scratch = nullptr;       // target of the engines' warm-up copies
   csg::SdmaEngines sdma;
-  std::vector<hsa_signal_t> sig_ready[2];  // consumers: per signal set, per remote chunk position
-  std::vector<hsa_signal_t> sig_data;  // producer: per remote chunk position, copy-out done
-  bool copies_in_flight = false;       // a call returned before its copies completed (error path)
-  int copies_set = 0;                  // signal set of those copies (consumers)
+  // Completion signals of the chunk copies, per set (calls alternate sets), per remote
+  // chunk position: consumers' copies in, the producer's copies out.
+  std::vector<hsa_signal_t> sig_ready[2];
+  bool copies_in_flight = false;       // a call returned before its copies completed (consumers:
+                                       // error paths only; producer: every call)
+  int copies_set = 0;                  // signal set of those copies
   hipEvent_t ev_copy_in = nullptr;     // the caller's copy stream reached the call
   hipEvent_t ev_prologue = nullptr;    // the prologue finished (waited for on an epoch wrap)
   hipEvent_t ev_kernel_done[2] = {nullptr, nullptr};  // by epoch parity
@@ -153,13 +155,9 @@ namespace {
 void free_plan_device(csg_plan* p) {
   if (p->device < 0) return;
   DeviceGuard g(p->device);
-  if (p->copies_in_flight) {
-    const std::vector<hsa_signal_t>& sigs = p->consumer() ? p->sig_ready[p->copies_set] : p->sig_data;
-    for (hsa_signal_t sgn : sigs)
-      if (sgn.handle) (void)csg::sdma_wait(sgn, 0, 10000);
-  }
-  for (hsa_signal_t sgn : p->sig_data)
-    if (sgn.handle) hsa_signal_destroy(sgn);
+  for (auto& set : p->sig_ready)
+    for (hsa_signal_t sgn : set)
+      if (sgn.handle) (void)csg::sdma_wait(sgn, 0, 10000);  // a copy may still be in flight
   for (auto& set : p->sig_ready)
     for (hsa_signal_t sgn : set)
       if (sgn.handle) hsa_signal_destroy(sgn);
@@ -317,25 +315,17 @@ csg_status setup_device(csg_plan* p) {
   std::string err = p->sdma.open(p->device, p->cfg.copy_engines, p->d_scratch, p->d_scratch + 8);
   if (!err.empty()) return fail(CSG_ERR_HIP, "copy engines: %s", err.c_str());
   const size_t n_remote = p->remote_order.size();
-  if (p->consumer()) {
-    for (int set = 0; set < 2; ++set) {
-      p->sig_ready[set].assign(n_remote, hsa_signal_t{0});
-      std::vector<const int64_t*> ptrs(p->n_chunks(), p->d_zero);
-      for (size_t i = 0; i < n_remote; ++i) {
-        hsa_status_t hs = p->sdma.make_signal(0, &p->sig_ready[set][i]);
-        const int64_t* vp = nullptr;
-        if (hs == HSA_STATUS_SUCCESS) hs = p->sdma.signal_value_ptr(p->sig_ready[set][i], &vp);
-        if (hs != HSA_STATUS_SUCCESS) return fail(CSG_ERR_NOMEM, "copy signal: %s", csg::hsa_error(hs).c_str());
-        ptrs[p->remote_order[i]] = vp;
-      }
-      if ((st = upload(&p->d_ready[set], ptrs)) != CSG_OK) return st;
-    }
-  } else {
-    p->sig_data.assign(n_remote, hsa_signal_t{0});
+  for (int set = 0; set < 2; ++set) {
+    p->sig_ready[set].assign(n_remote, hsa_signal_t{0});
+    std::vector<const int64_t*> ptrs(p->n_chunks(), p->d_zero);  // local chunks: never copied
     for (size_t i = 0; i < n_remote; ++i) {
-      const hsa_status_t hs = p->sdma.make_signal(0, &p->sig_data[i]);
+      hsa_status_t hs = p->sdma.make_signal(0, &p->sig_ready[set][i]);
+      const int64_t* vp = nullptr;
+      if (hs == HSA_STATUS_SUCCESS) hs = p->sdma.signal_value_ptr(p->sig_ready[set][i], &vp);
       if (hs != HSA_STATUS_SUCCESS) return fail(CSG_ERR_NOMEM, "copy signal: %s", csg::hsa_error(hs).c_str());
+      ptrs[p->remote_order[i]] = vp;
     }
+    if ((st = upload(&p->d_ready[set], ptrs)) != CSG_OK) return st;
   }
   CSG_HIP(hipEventCreateWithFlags(&p->ev_copy_in, hipEventDisableTiming));
   CSG_HIP(hipEventCreateWithFlags(&p->ev_prologue, hipEventDisableTiming));
@@ -377,19 +367,19 @@ struct CallState {
   bool prev_kernel = false;
 };
 
-// The signals copies of this call complete: one set per call parity (consumers), the
-// copy-out signals (producer).
-std::vector<hsa_signal_t>& call_signals(csg_plan* p) {
-  return p->consumer() ? p->sig_ready[p->epoch & 1] : p->sig_data;
-}
+// The signals this call's copies complete: one set per call parity.
+std::vector<hsa_signal_t>& call_signals(csg_plan* p) { return p->sig_ready[p->epoch & 1]; }
 
-// Waits for the copies a previous call left running (only after an error return).
-csg_status drain_copies(csg_plan* p) {
-  if (!p->copies_in_flight) return CSG_OK;
+// Waits for copies a previous call left running: a consumer's after an error return
+// (before its signals are armed again); with `all`, also the producer's copy-outs,
+// which complete after their call returns.
+csg_status drain_copies(csg_plan* p, bool all) {
+  if (!p->copies_in_flight || (!all && !p->consumer())) return CSG_OK;
   const int budget = p->cfg.timeout_ms * 4;
-  const std::vector<hsa_signal_t>& sigs = p->consumer() ? p->sig_ready[p->copies_set] : p->sig_data;
-  for (hsa_signal_t sgn : sigs)
-    if (csg::sdma_wait(sgn, 0, budget) > 0) return fail(CSG_ERR_TIMEOUT, "copies of the previous call did not complete");
+  for (int set = 0; set < 2; ++set)
+    for (hsa_signal_t sgn : p->sig_ready[set])
+      if (csg::sdma_wait(sgn, 0, budget) > 0)
+        return fail(CSG_ERR_TIMEOUT, "copies of an earlier call did not complete");
   p->copies_in_flight = false;
   return CSG_OK;
 }
@@ -399,7 +389,7 @@ csg_status drain_copies(csg_plan* p) {
 csg_status begin_call(csg_plan* p, csg_mode mode, hipStream_t compute, CallState* cs) {
   if (mode != CSG_MODE_OVERLAP && mode != CSG_MODE_COMPUTE_ONLY && mode != CSG_MODE_COPY_ONLY)
     return fail(CSG_ERR_INVALID, "unknown mode %d", static_cast<int>(mode));
-  csg_status st = drain_copies(p);
+  csg_status st = drain_copies(p, false);
   if (st != CSG_OK) return st;
   cs->prev_parity = p->epoch & 1;
   cs->prev_kernel = p->kernel_pending[cs->prev_parity];
@@ -474,7 +464,9 @@ csg_status launch_gemm(csg_plan* p, const void* A, const void* B, void* C, csg_m
   a.list_ptr = p->d_list_ptr;
   a.list_ids = p->d_list_ids;
   a.raster = p->d_raster;
-  a.ready = p->d_ready[p->epoch & 1];
+  // consumers wait for this call's copies in; the producer, before overwriting a
+  // chunk's rows of C, for the previous call's copy out of them
+  a.ready = p->d_ready[p->consumer() ? (p->epoch & 1) : ((p->epoch + 1) & 1)];
   a.counters = p->d_counters;
   a.need = p->d_need;
   a.out_flags = p->h_out_flags_dev;
@@ -884,13 +876,15 @@ csg_status csg_gemm_rs(csg_plan* p, const void* a, const void* b_nk, void* c, vo
   const int64_t row_bytes = p->N * out_bytes(p);
   const auto budget = std::chrono::milliseconds(p->cfg.timeout_ms) * 4;
   const Clock::time_point t0 = Clock::now();
+  const std::vector<hsa_signal_t>& sigs = call_signals(p);
+  p->copies_in_flight = true;
+  p->copies_set = p->epoch & 1;
   for (size_t i = 0; i < p->remote_order.size(); ++i) {
     const int32_t cid = p->remote_order[i];
     if (mode == CSG_MODE_OVERLAP) {
       const volatile uint32_t* f = p->h_out_flags + cid;
       while (*f < p->epoch) {
         if (Clock::now() - t0 > budget) {
-          (void)finish_copies(p, i);
           p->host_diag = csg_diag{1, cid, -1, *f, p->epoch, 0};
           return fail(CSG_ERR_TIMEOUT, "output chunk %d was not completed in time", cid);
         }
@@ -898,18 +892,26 @@ csg_status csg_gemm_rs(csg_plan* p, const void* a, const void* b_nk, void* c, vo
     }
     const csg::ChunkDesc& ch = p->sched.chunks[cid];
     const int64_t off = ch.row_begin * row_bytes;
-    hsa_signal_store_relaxed(p->sig_data[i], 1);
+    // this signal's copy two calls back has long completed (the previous kernel waited
+    // for it before rewriting the chunk); check before arming it again
+    const hsa_signal_t sig = sigs[i];
+    if (csg::sdma_wait(sig, 0, p->cfg.timeout_ms * 4) != 0) {
+      p->host_diag = csg_diag{1, cid, -1, 1, p->epoch, 0};
+      return fail(CSG_ERR_TIMEOUT, "an earlier copy out of chunk %d did not complete", cid);
+    }
+    hsa_signal_store_relaxed(sig, 1);
     const hsa_status_t hs =
         p->sdma.copy(static_cast<char*>(c_outgoing) + off, static_cast<const char*>(c) + off,
                      static_cast<size_t>((ch.row_end - ch.row_begin) * row_bytes), static_cast<int>(i % p->sdma.count()),
-                     nullptr, p->sig_data[i]);
+                     nullptr, sig);
     if (hs != HSA_STATUS_SUCCESS) {
-      hsa_signal_store_relaxed(p->sig_data[i], 0);
-      (void)finish_copies(p, i);
+      hsa_signal_store_relaxed(sig, 0);
       return fail(CSG_ERR_HIP, "SDMA copy: %s", csg::hsa_error(hs).c_str());
     }
   }
-  return finish_copies(p, p->remote_order.size());
+  // the copies complete on their own: the next call's kernel waits for each before
+  // rewriting the chunk, and csg_plan_check (or destroy) waits for all of them
+  return CSG_OK;
 }
 
 csg_status csg_plan_check(csg_plan* p, csg_diag* out) {
@@ -920,7 +922,7 @@ csg_status csg_plan_check(csg_plan* p, csg_diag* out) {
     if (g.err != hipSuccess) return hip_fail(g.err, "hipSetDevice");
     CSG_HIP(hipEventSynchronize(p->ev_prologue));
     if (p->kernel_pending[p->epoch & 1]) CSG_HIP(hipEventSynchronize(p->ev_kernel_done[p->epoch & 1]));
-    csg_status st = drain_copies(p);
+    csg_status st = drain_copies(p, true);
     if (st != CSG_OK) return st;
     csg::DeviceDiag dd{};
     CSG_HIP(hipMemcpyAsync(&dd, p->d_diag, sizeof dd, hipMemcpyDeviceToHost, p->aux));

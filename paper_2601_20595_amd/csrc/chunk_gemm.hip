@@ -65,9 +65,11 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, in
   return __builtin_amdgcn_make_buffer_rsrc(ub, 0, n, kBufferDword3);
 }
 
-// Waits (thread 0 only) until every listed chunk is ready. Returns 1 if a chunk was
-// seen ready for the first time in this workgroup, 0 if all were already known,
-// -1 if the wait gave up (timeout here, or another workgroup's abort).
+// Waits (thread 0 only) until every listed chunk is ready: consumers, until its copy
+// in has landed; the producer, until the previous call's copy out of its rows has
+// completed. Returns 1 if a chunk was seen ready for the first time in this
+// workgroup, 0 if all were already known, -1 if the wait gave up (timeout here, or
+// another workgroup's abort).
 __device__ int wait_chunks(const GemmArgs& a, int pos, uint32_t* ready_bits) {
   int fresh = 0;
   for (int p = a.list_ptr[pos]; p < a.list_ptr[pos + 1]; ++p) {
@@ -557,6 +559,16 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
       else
         __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, f), rsC, voff, soff, kCStorePolicy);
     };
+    // Producer: the previous call's copy out of a chunk reads the same rows of C this
+    // unit is about to write; wait until it has completed (its completion signal reads
+    // 0). It normally has, long ago. False if the wait gave up.
+    auto wait_previous_copy_out = [&]() -> bool {
+      if constexpr (!kProducer) return true;
+      __syncthreads();
+      if (tid == 0) s_state = wait_chunks(a, pos, ready_bits);
+      __syncthreads();
+      return s_state >= 0;
+    };
     auto acc_run = [&](int r) -> f32x4 {
       const int i = r / (NI * 4), j = (r / 4) % NI, q = r % 4;
       return f32x4{acc[i][j][4 * q + 0], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
@@ -598,12 +610,14 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
       }
       if (a.steal) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
       else asm volatile("buffer_inv sc0" ::: "memory");
+      if (!wait_previous_copy_out()) break;
       auto load_part = [&](int sl, int r) -> f32x4 {
         return __builtin_bit_cast(f32x4,
                                   __builtin_amdgcn_raw_buffer_load_b128(rsW, toff, sl * kSliceBytes + r * kThreads * 16, 0));
       };
       reduce_slices<kRuns>(nslices, load_part, store_run);
     } else {
+      if (!wait_previous_copy_out()) break;
 #pragma unroll
       for (int r = 0; r < kRuns; ++r) {
         store_run(r, acc_run(r));

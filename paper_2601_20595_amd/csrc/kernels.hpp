@@ -43,8 +43,9 @@ struct GemmArgs {
   const int32_t* list_ptr;   // [n_tiles + 1]: per execution position, its chunks
   const int32_t* list_ids;   // consumer: remote chunks to wait for; producer: chunks written
   const int32_t* raster;     // [n_tiles] raster id per execution position (diagnostics)
-  const int64_t* const* ready;  // consumer: per chunk, the value a copy engine brings to 0 once
-                                // the chunk has landed (local chunks point at a 0)
+  const int64_t* const* ready;  // per chunk, the value a copy engine brings to 0: consumers,
+                                // once the chunk has landed; producer, once the previous call's
+                                // copy out of the chunk has completed (local chunks: a 0)
   uint32_t* counters;        // per chunk: producer: tiles written; consumers: units done reading it
   const int32_t* need;       // per chunk: the count at which the chunk is complete
   uint32_t* out_flags;       // per chunk, host-visible memory, set to epoch when complete:
