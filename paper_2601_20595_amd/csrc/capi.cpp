@@ -384,9 +384,9 @@ csg_status drain_copies(csg_plan* p, bool all) {
   return CSG_OK;
 }
 
-// Front half of a call: the call's ready signals are armed and the prologue is
-// queued on the compute stream.
-csg_status begin_call(csg_plan* p, csg_mode mode, hipStream_t compute, CallState* cs) {
+// Front half of a call: the call number advances and the call's ready signals are
+// armed.
+csg_status begin_call(csg_plan* p, csg_mode mode, CallState* cs) {
   if (mode != CSG_MODE_OVERLAP && mode != CSG_MODE_COMPUTE_ONLY && mode != CSG_MODE_COPY_ONLY)
     return fail(CSG_ERR_INVALID, "unknown mode %d", static_cast<int>(mode));
   csg_status st = drain_copies(p, false);
@@ -414,18 +414,28 @@ csg_status begin_call(csg_plan* p, csg_mode mode, hipStream_t compute, CallState
     for (hsa_signal_t sgn : p->sig_ready[set]) hsa_signal_store_relaxed(sgn, v);
     std::atomic_thread_fence(std::memory_order_seq_cst);  // armed before the kernel launch below
   }
-  CSG_HIP(csg::launch_prologue(p->d_counters, p->n_chunks(), p->epoch, p->d_ticket,
-                               p->d_diag, p->d_slot_count, p->ws_slices > 0 ? p->map.n_tiles() : 0, compute));
-  CSG_HIP(hipEventRecord(p->ev_prologue, compute));
   p->kernel_pending[p->epoch & 1] = false;
+  return CSG_OK;
+}
+
+// The call's prologue on the compute stream (before its kernel, if any).
+csg_status launch_prologue_call(csg_plan* p, hipStream_t compute) {
+  CSG_HIP(csg::launch_prologue(p->d_counters, p->n_chunks(), p->epoch, p->d_ticket, p->d_diag, p->d_slot_count,
+                               p->ws_slices > 0 ? p->map.n_tiles() : 0, compute));
+  CSG_HIP(hipEventRecord(p->ev_prologue, compute));
   return CSG_OK;
 }
 
 // Ordering the copies need, enforced from the host (see the file comment).
 csg_status ready_copies(csg_plan* p, hipStream_t copy, const CallState& cs, bool war_on_previous_kernel) {
-  CSG_HIP(hipEventRecord(p->ev_copy_in, copy));
-  csg_status st = host_wait(p, p->ev_copy_in, "the copy stream's earlier work");
-  if (st != CSG_OK) return st;
+  csg_status st = CSG_OK;
+  const hipError_t q = hipStreamQuery(copy);  // idle: nothing to wait for
+  if (q == hipErrorNotReady) {
+    CSG_HIP(hipEventRecord(p->ev_copy_in, copy));
+    if ((st = host_wait(p, p->ev_copy_in, "the copy stream's earlier work")) != CSG_OK) return st;
+  } else if (q != hipSuccess) {
+    return hip_fail(q, "hipStreamQuery");
+  }
   if (war_on_previous_kernel && cs.prev_kernel) {
     st = host_wait(p, p->ev_kernel_done[cs.prev_parity], "the previous call's kernel");
     if (st != CSG_OK) return st;
@@ -499,63 +509,81 @@ csg_status launch_gemm(csg_plan* p, const void* A, const void* B, void* C, csg_m
 
 // Consumer copies: staging -> landing per remote chunk, on engine (i mod engines)
 // for the i-th remote chunk in arrival order; each completes the chunk's (armed)
-// ready signal.
-csg_status issue_consumer_copies(csg_plan* p, void* landing, const void* staging, uint32_t prev_reader) {
-  const int64_t row_bytes = p->K * in_bytes(p);
-  const bool delayed = !p->delays_us.empty();
-  const Clock::time_point t0 = Clock::now();
+// ready signal. Before overwriting a chunk's rows the issuer waits until the kernel
+// that read them last (call prev_reader) is done with them: that kernel reports it per
+// chunk (its consumed words), and its completion event settles it for every chunk
+// (also when it gave up early). Copy delays release chunk i at the sum of the first i
+// delays after the call started.
+struct CopyIssuer {
+  csg_plan* p;
+  void* landing;
+  const void* staging;
+  uint32_t prev_reader;
+  Clock::time_point t0;
+  size_t next = 0;
   double release_us = 0.0;
-  const std::vector<hsa_signal_t>& sigs = call_signals(p);
-  const int prev_parity = static_cast<int>(prev_reader & 1);
-  bool prev_done = prev_reader == 0;
-  const auto budget = std::chrono::milliseconds(p->cfg.timeout_ms) * 4;
-  for (size_t i = 0; i < p->remote_order.size(); ++i) {
-    const int32_t cid = p->remote_order[i];
-    const csg::ChunkDesc& c = p->sched.chunks[cid];
-    if (delayed) {
-      release_us += p->delays_us[i];
-      spin_until(t0 + std::chrono::nanoseconds(static_cast<int64_t>(release_us * 1000.0)));
-    }
-    // write after read: the previous kernel must be done reading the chunk's rows; it
-    // reports that per chunk (consumed flags), and its completion event settles it
-    // for every chunk (also when it gave up early)
-    if (!prev_done) {
-      const volatile uint32_t* f = p->h_out_flags + cid;
-      const Clock::time_point tw = Clock::now();
-      uint32_t spins = 0;
-      while (*f < prev_reader) {
-        if ((++spins & 255u) == 0) {
-          const hipError_t q = hipEventQuery(p->ev_kernel_done[prev_parity]);
-          if (q == hipSuccess) {
-            prev_done = true;
-            break;
+  bool prev_done;
+
+  CopyIssuer(csg_plan* plan, void* l, const void* s, uint32_t prev)
+      : p(plan), landing(l), staging(s), prev_reader(prev), t0(Clock::now()), prev_done(prev == 0) {}
+
+  // Issues copies in arrival order. Without `block` it stops at the first copy that
+  // would have to wait (for its release time or for the previous kernel).
+  csg_status run(bool block) {
+    const int64_t row_bytes = p->K * in_bytes(p);
+    const std::vector<hsa_signal_t>& sigs = call_signals(p);
+    const int prev_parity = static_cast<int>(prev_reader & 1);
+    const auto budget = std::chrono::milliseconds(p->cfg.timeout_ms) * 4;
+    for (; next < p->remote_order.size(); ++next) {
+      const size_t i = next;
+      const int32_t cid = p->remote_order[i];
+      const csg::ChunkDesc& c = p->sched.chunks[cid];
+      if (!p->delays_us.empty()) {
+        const Clock::time_point due =
+            t0 + std::chrono::nanoseconds(static_cast<int64_t>((release_us + p->delays_us[i]) * 1000.0));
+        if (!block && Clock::now() < due) return CSG_OK;
+        spin_until(due);
+      }
+      if (!prev_done) {
+        const volatile uint32_t* f = p->h_out_flags + cid;
+        const Clock::time_point tw = Clock::now();
+        uint32_t spins = 0;
+        while (*f < prev_reader) {
+          if (!block) return CSG_OK;
+          if ((++spins & 255u) == 0) {
+            const hipError_t q = hipEventQuery(p->ev_kernel_done[prev_parity]);
+            if (q == hipSuccess) {
+              prev_done = true;
+              break;
+            }
+            if (q != hipErrorNotReady) {
+              (void)finish_copies(p, i);
+              return hip_fail(q, "the previous call's kernel");
+            }
           }
-          if (q != hipErrorNotReady) {
+          if (Clock::now() - tw > budget) {
             (void)finish_copies(p, i);
-            return hip_fail(q, "the previous call's kernel");
+            p->host_diag = csg_diag{1, cid, -1, *f, p->epoch, 0};
+            return fail(CSG_ERR_TIMEOUT, "the previous kernel did not finish reading chunk %d in time", cid);
           }
-        }
-        if (Clock::now() - tw > budget) {
-          (void)finish_copies(p, i);
-          p->host_diag = csg_diag{1, cid, -1, *f, p->epoch, 0};
-          return fail(CSG_ERR_TIMEOUT, "the previous kernel did not finish reading chunk %d in time", cid);
         }
       }
+      if (!p->delays_us.empty()) release_us += p->delays_us[i];
+      const int64_t off = c.row_begin * row_bytes;
+      const int64_t bytes = (c.row_end - c.row_begin) * row_bytes;
+      const int eng = static_cast<int>(i % p->sdma.count());
+      const hsa_status_t hs = p->sdma.copy(static_cast<char*>(landing) + off, static_cast<const char*>(staging) + off,
+                                           static_cast<size_t>(bytes), eng, nullptr, sigs[i]);
+      if (hs != HSA_STATUS_SUCCESS) {
+        // the chunks not copied keep their signals armed: the kernel's bounded waits for
+        // them expire and it reports them through csg_plan_check
+        (void)finish_copies(p, i);
+        return fail(CSG_ERR_HIP, "SDMA copy of chunk %d: %s", cid, csg::hsa_error(hs).c_str());
+      }
     }
-    const int64_t off = c.row_begin * row_bytes;
-    const int64_t bytes = (c.row_end - c.row_begin) * row_bytes;
-    const int eng = static_cast<int>(i % p->sdma.count());
-    const hsa_status_t hs = p->sdma.copy(static_cast<char*>(landing) + off, static_cast<const char*>(staging) + off,
-                                         static_cast<size_t>(bytes), eng, nullptr, sigs[i]);
-    if (hs != HSA_STATUS_SUCCESS) {
-      // the chunks not copied keep their signals armed: the kernel's bounded waits for
-      // them expire and it reports them through csg_plan_check
-      (void)finish_copies(p, i);
-      return fail(CSG_ERR_HIP, "SDMA copy of chunk %d: %s", cid, csg::hsa_error(hs).c_str());
-    }
+    return CSG_OK;
   }
-  return finish_copies(p, p->remote_order.size());
-}
+};
 
 csg_status consumer_call(csg_plan* p, void* landing, const void* staging, const void* b, void* c, csg_mode mode,
                          void* compute_v, void* copy_v) {
@@ -570,16 +598,22 @@ csg_status consumer_call(csg_plan* p, void* landing, const void* staging, const 
   CallState cs;
   // the kernel that last read the landing rows (before this call's own)
   const uint32_t prev_reader = p->last_kernel_epoch;
-  csg_status st = begin_call(p, mode, compute, &cs);
+  csg_status st = begin_call(p, mode, &cs);
   if (st != CSG_OK) return st;
-  // the kernel is queued first: it starts as soon as the previous kernel ends and
-  // waits for its chunks, while the host releases the copies
+  const bool copies = mode != CSG_MODE_COMPUTE_ONLY && !p->remote_order.empty();
+  CopyIssuer issuer(p, landing, staging, prev_reader);
+  if (copies) {
+    // the copies that need not wait go first (they take the longest to land), then the
+    // kernel is queued: it starts as soon as the previous kernel ends and waits for its
+    // chunks, while the host releases the remaining copies
+    if ((st = ready_copies(p, copy, cs, false)) != CSG_OK) return st;
+    if ((st = issuer.run(false)) != CSG_OK) return st;
+  }
+  if ((st = launch_prologue_call(p, compute)) != CSG_OK) return st;
   if (mode != CSG_MODE_COPY_ONLY && (st = launch_gemm(p, landing, b, c, mode, compute)) != CSG_OK) return st;
-  if (mode == CSG_MODE_COMPUTE_ONLY || p->remote_order.empty()) return CSG_OK;
-  // the landing rows are rewritten: issue_consumer_copies waits, chunk by chunk, until
-  // the kernel before this call's is done reading them
-  if ((st = ready_copies(p, copy, cs, false)) != CSG_OK) return st;
-  return issue_consumer_copies(p, landing, staging, prev_reader);
+  if (!copies) return CSG_OK;
+  if ((st = issuer.run(true)) != CSG_OK) return st;
+  return finish_copies(p, p->remote_order.size());
 }
 
 }  // namespace
@@ -867,8 +901,9 @@ csg_status csg_gemm_rs(csg_plan* p, const void* a, const void* b_nk, void* c, vo
   DeviceGuard g(p->device);
   if (g.err != hipSuccess) return hip_fail(g.err, "hipSetDevice");
   CallState cs;
-  csg_status st = begin_call(p, mode, compute, &cs);
+  csg_status st = begin_call(p, mode, &cs);
   if (st != CSG_OK) return st;
+  if ((st = launch_prologue_call(p, compute)) != CSG_OK) return st;
   if (mode != CSG_MODE_COPY_ONLY && (st = launch_gemm(p, a, b_nk, c, mode, compute)) != CSG_OK) return st;
   if (mode == CSG_MODE_COMPUTE_ONLY || p->remote_order.empty()) return CSG_OK;
   // copy-only reads the C a previous kernel wrote: that kernel must have finished

@@ -400,6 +400,50 @@ __device__ __forceinline__ void reduce_fixed(Load load, Store store) {
   }
 }
 
+// Two-slice reduction: own (registers) + the other slice's stored partial, run by
+// run, with the loads of the next batch of runs in flight while a batch is added.
+template <int kRuns, class Load, class Own, class Store>
+__device__ __forceinline__ void add_stored_pair(Load load, Own own, Store store) {
+  constexpr int B = kRuns % 8 == 0 ? 8 : (kRuns % 4 == 0 ? 4 : 1);
+  f32x4 v[2][B];
+#pragma unroll
+  for (int b = 0; b < B; ++b) v[0][b] = load(b);
+#pragma unroll
+  for (int r0 = 0; r0 < kRuns; r0 += B) {
+    const int cur = (r0 / B) & 1;
+    if (r0 + B < kRuns) {
+#pragma unroll
+      for (int b = 0; b < B; ++b) v[cur ^ 1][b] = load(r0 + B + b);
+    }
+#pragma unroll
+    for (int b = 0; b < B; ++b) store(r0 + b, own(r0 + b) + v[cur][b]);
+  }
+}
+
+// Waits (thread 0 only) until `others` slices of a split tile have stored their
+// partial sums (high half of the tile's slot word). 1 when they have, -1 if the wait
+// gave up (timeout, or another workgroup's abort).
+__device__ int wait_slices_stored(const GemmArgs& a, const uint32_t* word, int others, int pos) {
+  const uint64_t t0 = wall_clock64();
+  uint32_t v = __hip_atomic_load(word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  while (static_cast<int>(v >> 16) < others) {
+    if (load_flag(&a.diag->abort)) return -1;
+    if (wall_clock64() - t0 > a.timeout_ticks) {
+      if (atomicCAS(&a.diag->timed_out, 0u, 1u) == 0u) {
+        a.diag->chunk = -1;
+        a.diag->tile = a.raster[pos];
+        a.diag->observed = v >> 16;
+        a.diag->epoch = a.epoch;
+      }
+      __hip_atomic_store(&a.diag->abort, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+      return -1;
+    }
+    __builtin_amdgcn_s_sleep(1);
+    v = __hip_atomic_load(word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  return 1;
+}
+
 template <int kRuns, class Load, class Store>
 __device__ void reduce_slices(int n, Load load, Store store) {
   switch (n) {
@@ -575,10 +619,54 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
     };
 
     const int nslices = td.slice >> 16;
-    if (nslices > 1) {
-      // Split along K: store this slice's partial sums; the slice that finishes its
-      // tile last adds all of them in slice order (so the result does not depend on
-      // which slice finished when) and writes the output from those sums.
+    if (nslices == 2) {
+      // Split in two along K. The slice that gets here second (low half of the tile's
+      // slot word) keeps its partial sums in registers, waits until the other slice has
+      // stored its own (high half) and writes the output from the sum of the two
+      // (fp32 addition commutes exactly, so the result does not depend on which slice
+      // came second); the first slice stores its partials and leaves.
+      constexpr int kSliceBytes = kRuns * kThreads * 16;  // one slice of one tile
+      const __amdgpu_buffer_rsrc_t rsW = make_rsrc(a.ws + static_cast<int64_t>(td.slot) * (kSliceBytes / 4),
+                                                   2 * static_cast<int64_t>(kSliceBytes));
+      const int toff = tid * 16;
+      const int me = td.slice & 0xffff;
+      uint32_t* word = a.slot_count + a.raster[pos];
+      if (tid == 0)
+        s_state = (__hip_atomic_fetch_add(word, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & 0xffffu) == 1u;
+      __syncthreads();
+      if (!s_state) {
+#pragma unroll
+        for (int r = 0; r < kRuns; ++r)
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc_run(r)), rsW, toff,
+                                                 me * kSliceBytes + r * kThreads * 16, 0);
+        // same-die slices meet in the die's L2 (see the general case below)
+        if (a.steal) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        else wait_dma_all();
+        __syncthreads();
+        if (tid == 0) __hip_atomic_fetch_add(word, 1u << 16, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (a.trace && tid == 0) {
+          a.trace[kTraceWords * pos + 2] = wall_clock64();
+          a.trace[kTraceWords * pos + 5] = clock64();
+        }
+        continue;
+      }
+      // the other slice has arrived, so it is only storing: a short, bounded wait
+      if (tid == 0) s_state = wait_slices_stored(a, word, 1, pos);
+      __syncthreads();
+      if (s_state < 0) break;
+      if (a.steal) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+      else asm volatile("buffer_inv sc0" ::: "memory");  // drop this CU's L1 copy, if any
+      if (!wait_previous_copy_out()) break;
+      const int other = (1 - me) * kSliceBytes;
+      add_stored_pair<kRuns>(
+          [&](int r) -> f32x4 {
+            return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rsW, toff, other + r * kThreads * 16, 0));
+          },
+          acc_run, store_run);
+    } else if (nslices > 2) {
+      // Split along K in more than two: store this slice's partial sums; the slice that
+      // finishes its tile last adds all of them in slice order (so the result does not
+      // depend on which slice finished when) and writes the output from those sums.
       constexpr int kSliceBytes = kRuns * kThreads * 16;  // one slice of one tile
       // slice layout: run r of thread t at byte (r * kThreads + t) * 16; addressed
       // through a buffer resource so the per-run offset is a scalar operand
