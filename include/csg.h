@@ -62,6 +62,21 @@ typedef enum {
     CSG_ORDER_RS_RING = 3       /* shards (r + 1 + t) mod W, t = 0..W-1 (own shard last) */
 } csg_order;
 
+/* What moves the chunks (Section 5.2, communication code generation: the same
+ * chunk schedule realised by different mechanisms). */
+typedef enum {
+    CSG_COPY_SDMA = 0,    /* copy engines, driven by the calling thread, with completion
+                             signals as the chunks' ready flags (realization (1)) */
+    CSG_COPY_KERNEL = 1   /* the GEMM kernel's own workgroups, by vector loads and stores:
+                             AG / grouped: workgroups 0 .. copy_workgroups - 1 (the first
+                             the device starts) move the remote chunks in arrival order,
+                             raise each chunk's ready flag, then take tiles (realization
+                             (4), specialised workgroups); GEMM-RS: a tile of a chunk that is sent also
+                             stores its output rows into the outgoing buffer from its
+                             epilogue (realization (5), co-located), which needs every
+                             chunk to start on a multiple of bm */
+} csg_copy_backend;
+
 typedef enum {
     CSG_MODE_OVERLAP = 0,       /* copies and kernel run concurrently */
     CSG_MODE_COMPUTE_ONLY = 1,  /* every flag pre-set, no copies; the kernel still polls */
@@ -104,7 +119,10 @@ typedef struct {
  *                   finished (read back with csg_plan_trace); 0 = off
  *   warm_rows       consumers: 0 or 1 = a workgroup that sees a chunk land first loads
  *                   its share of the tile's A rows into the caches before computing
- *                   (copy-engine writes leave the rows only in HBM); 2 = off */
+ *                   (copy-engine writes leave the rows only in HBM); 2 = off
+ *   copy_backend    a csg_copy_backend value; 0 = CSG_COPY_SDMA
+ *   copy_workgroups CSG_COPY_KERNEL: workgroups that move chunks (0 = 16); a copy-only
+ *                   call launches exactly this many */
 typedef struct {
     int32_t bm, bn, bk;
     int32_t intra_order;
@@ -117,6 +135,8 @@ typedef struct {
     int32_t tail_chunks;
     int32_t trace;
     int32_t warm_rows;
+    int32_t copy_backend;
+    int32_t copy_workgroups;
 } csg_plan_cfg;
 
 typedef struct csg_schedule csg_schedule;
@@ -240,7 +260,9 @@ csg_status csg_plan_get_map(const csg_plan* p, int32_t* tile_ptr, int32_t* tile_
  * chunks is not copied before sum_{j<=i} delay_us[j] after the call starts.
  * NULL clears them. With delays set, copies are issued from the calling thread
  * at their release times, so the call returns only after the last copy is
- * issued. */
+ * issued. With CSG_COPY_KERNEL the copy workgroups wait for the release times
+ * instead, counted from when the call's prologue runs on the device; setting
+ * delays then waits for the plan's kernels to finish. */
 csg_status csg_plan_set_copy_delays(csg_plan* p, const float* delay_us_host, int32_t n);
 
 /* AllGather + GEMM on one rank. a_landing is the full M x K A whose local rows are
@@ -253,7 +275,10 @@ csg_status csg_plan_set_copy_delays(csg_plan* p, const float* delay_us_host, int
  * kernel runs tiles in chunk order, each waiting for its chunks. Work queued on
  * `compute` afterwards is ordered after the kernel. Asynchronous failures (a flag
  * wait that timed out) surface through csg_plan_check. CSG_ERR_TIMEOUT if a host
- * wait expired. */
+ * wait expired.
+ * With CSG_COPY_KERNEL the call only queues the prologue and the kernel on
+ * `compute` (its copy workgroups move the chunks; copy-only: they alone run) and
+ * returns; `copy` is not used. */
 csg_status csg_ag_gemm(csg_plan* p, void* a_landing, const void* a_staging, const void* b_nk,
                        void* c, csg_mode mode, void* compute_stream, void* copy_stream);
 
@@ -265,7 +290,12 @@ csg_status csg_ag_gemm(csg_plan* p, void* a_landing, const void* a_staging, cons
  * call's kernel waits for the copy out of a chunk before rewriting its rows of c, and
  * csg_plan_check waits for all of them: call it (or csg_plan_destroy) before reading
  * c_outgoing. In copy-only mode c must already hold the output (the plan's previous
- * kernel is waited for). */
+ * kernel is waited for).
+ * With CSG_COPY_KERNEL the call only queues the prologue and the kernel on
+ * `compute` and returns; `copy` is not used. Overlap: the tiles of a non-local chunk
+ * store their output rows into both c and c_outgoing, and the chunk is sent when its
+ * last tile has stored; copy-only: copy workgroups move the non-local chunks' rows
+ * c -> c_outgoing, after the work queued earlier on `compute`. */
 csg_status csg_gemm_rs(csg_plan* p, const void* a, const void* b_nk, void* c, void* c_outgoing,
                        csg_mode mode, void* compute_stream, void* copy_stream);
 

@@ -31,12 +31,15 @@ CSG_AG_GEMM, CSG_GEMM_RS, CSG_GROUPED_GEMM = 0, 1, 2
 CSG_ORDER_RING, CSG_ORDER_SWIZZLE1D, CSG_ORDER_PERMUTATION, CSG_ORDER_RS_RING = 0, 1, 2, 3
 # csg_mode
 CSG_MODE_OVERLAP, CSG_MODE_COMPUTE_ONLY, CSG_MODE_COPY_ONLY = 0, 1, 2
+# csg_copy_backend
+CSG_COPY_SDMA, CSG_COPY_KERNEL = 0, 1
 
 ORDERS = {"ring": CSG_ORDER_RING, "swizzle1d": CSG_ORDER_SWIZZLE1D, "permutation": CSG_ORDER_PERMUTATION,
           "rs_ring": CSG_ORDER_RS_RING}
 MODES = {"overlap": CSG_MODE_OVERLAP, "compute_only": CSG_MODE_COMPUTE_ONLY, "copy_only": CSG_MODE_COPY_ONLY}
 DTYPES = {"bf16": CSG_BF16, "f32": CSG_F32}
 OPS = {"ag": CSG_AG_GEMM, "rs": CSG_GEMM_RS, "grouped": CSG_GROUPED_GEMM}
+COPY_BACKENDS = {"sdma": CSG_COPY_SDMA, "kernel": CSG_COPY_KERNEL}
 
 # every symbol include/csg.h declares
 ABI_FUNCTIONS = (
@@ -69,7 +72,8 @@ class csg_plan_cfg(ctypes.Structure):
                 ("intra_order", ctypes.c_int32), ("tile_dispatch", ctypes.c_int32),
                 ("num_workgroups", ctypes.c_int32), ("copy_engines", ctypes.c_int32), ("timeout_ms", ctypes.c_int32),
                 ("split_k", ctypes.c_int32), ("tail_split", ctypes.c_int32), ("tail_chunks", ctypes.c_int32),
-                ("trace", ctypes.c_int32), ("warm_rows", ctypes.c_int32)]
+                ("trace", ctypes.c_int32), ("warm_rows", ctypes.c_int32), ("copy_backend", ctypes.c_int32),
+                ("copy_workgroups", ctypes.c_int32)]
 
 
 class csg_plan_info(ctypes.Structure):
@@ -247,7 +251,10 @@ def csg_plan_create(op, M: int, N: int, K: int, in_dtype, out_dtype, sched: int,
     op = OPS[op] if isinstance(op, str) else int(op)
     ind = DTYPES[in_dtype] if isinstance(in_dtype, str) else int(in_dtype)
     outd = DTYPES[out_dtype] if isinstance(out_dtype, str) else int(out_dtype)
-    c = csg_plan_cfg(**(cfg or {}))
+    cfg = dict(cfg or {})
+    if isinstance(cfg.get("copy_backend"), str):
+        cfg["copy_backend"] = COPY_BACKENDS[cfg["copy_backend"]]
+    c = csg_plan_cfg(**cfg)
     if group_rows is not None:
         g = np.ascontiguousarray(np.asarray(group_rows, dtype=np.int64))
         gp, ng = g.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), g.size

@@ -81,6 +81,8 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 // Epochs run 1 .. kEpochWrap - 1; on reaching it the emitted-flag words are cleared.
 constexpr uint32_t kEpochWrap = 1u << 30;
 constexpr int kTimingRing = 256;  // kernel launches whose durations a plan keeps
+constexpr int64_t kCopySlab = 256 << 10;  // bytes per copy item of the copy workgroups
+constexpr int32_t kDefaultCopyWorkgroups = 16;
 
 }  // namespace
 
@@ -145,9 +147,25 @@ struct csg_plan {
   uint64_t n_launches = 0;
   hipStream_t aux = nullptr;           // plan-internal transfers (diagnostics)
   csg_diag host_diag{};                // host-side wait failures of the last call
+  uint32_t expected_units = 0;         // work units the last kernel launch had to run
+
+  // Chunks moved by the kernel itself (cfg.copy_backend == CSG_COPY_KERNEL)
+  csg::CopyItem* d_copy_items = nullptr;  // consumers: staging -> landing; producer: C -> outgoing
+  int32_t n_copy_items = 0;
+  int32_t* d_copy_chunk = nullptr;     // per remote position: chunk id
+  int32_t* d_copy_parts = nullptr;     // per remote position: copy items
+  uint32_t* d_copy_done = nullptr;     // per remote position: items finished
+  int64_t* d_kready = nullptr;         // per chunk: ready word the copy workgroups clear
+  const int64_t** d_ready_k = nullptr; // per chunk: its ready word (local chunks: d_zero)
+  int32_t* d_chunk_sent = nullptr;     // per chunk: 1 if sent (producer)
+  csg::CopyState* d_copy_state = nullptr;
+  uint64_t* d_release_ticks = nullptr; // per remote position: cumulative release time, 100 MHz ticks
+  bool release_set = false;
 
   int32_t n_chunks() const { return static_cast<int32_t>(sched.chunks.size()); }
+  int32_t copy_workgroups() const { return cfg.copy_workgroups; }
   bool consumer() const { return op != CSG_GEMM_RS; }
+  bool kernel_copies() const { return cfg.copy_backend == CSG_COPY_KERNEL; }
 };
 
 namespace {
@@ -171,7 +189,11 @@ void free_plan_device(csg_plan* p) {
                     static_cast<void*>(p->d_ready[0]), static_cast<void*>(p->d_ready[1]),
                     static_cast<void*>(p->d_zero),
                     static_cast<void*>(p->d_counters), static_cast<void*>(p->d_ticket), static_cast<void*>(p->d_diag),
-                    static_cast<void*>(p->d_scratch)})
+                    static_cast<void*>(p->d_scratch), static_cast<void*>(p->d_copy_items),
+                    static_cast<void*>(p->d_copy_chunk), static_cast<void*>(p->d_copy_parts),
+                    static_cast<void*>(p->d_copy_done), static_cast<void*>(p->d_kready),
+                    static_cast<void*>(p->d_ready_k), static_cast<void*>(p->d_chunk_sent),
+                    static_cast<void*>(p->d_copy_state), static_cast<void*>(p->d_release_ticks)})
     if (ptr) (void)hipFree(ptr);
   if (p->h_out_flags) (void)hipHostFree(p->h_out_flags);
   for (hipEvent_t e : {p->ev_copy_in, p->ev_prologue, p->ev_kernel_done[0], p->ev_kernel_done[1]})
@@ -311,6 +333,41 @@ csg_status setup_device(csg_plan* p) {
   std::memset(p->h_out_flags, 0, nflag * 4);
   CSG_HIP(hipHostGetDevicePointer(reinterpret_cast<void**>(&p->h_out_flags_dev), p->h_out_flags, 0));
   CSG_HIP(hipMalloc(&p->d_scratch, 64));
+  if (p->kernel_copies()) {
+    // copy items: every remote chunk in arrival (emission) order, cut into slabs of
+    // kCopySlab bytes; consumers move A rows staging -> landing, the producer (in
+    // copy-only calls; its overlap calls send from the epilogue) C rows C -> outgoing
+    const int64_t row_bytes = p->consumer() ? p->K * in_bytes(p) : p->N * out_bytes(p);
+    std::vector<csg::CopyItem> items;
+    std::vector<int32_t> parts, sent(p->n_chunks(), 0);
+    std::vector<const int64_t*> words(p->n_chunks(), p->d_zero);
+    // polled by workgroups on every die and written by others: fine-grained
+    // (coherent) device memory
+    CSG_HIP(hipExtMallocWithFlags(reinterpret_cast<void**>(&p->d_kready), nflag * 8, hipDeviceMallocFinegrained));
+    CSG_HIP(hipMemset(p->d_kready, 0, nflag * 8));
+    for (size_t i = 0; i < p->remote_order.size(); ++i) {
+      const int32_t cid = p->remote_order[i];
+      const csg::ChunkDesc& ch = p->sched.chunks[cid];
+      const int64_t off = ch.row_begin * row_bytes, bytes = (ch.row_end - ch.row_begin) * row_bytes;
+      int32_t n = 0;
+      for (int64_t b = 0; b < bytes; b += kCopySlab, ++n)
+        items.push_back({off + b, static_cast<int32_t>(std::min<int64_t>(kCopySlab, bytes - b)), static_cast<int32_t>(i)});
+      parts.push_back(n);
+      sent[cid] = 1;
+      words[cid] = p->d_kready + cid;
+    }
+    p->n_copy_items = static_cast<int32_t>(items.size());
+    if ((st = upload(&p->d_copy_items, items)) != CSG_OK) return st;
+    if ((st = upload(&p->d_copy_chunk, p->remote_order)) != CSG_OK) return st;
+    if ((st = upload(&p->d_copy_parts, parts)) != CSG_OK) return st;
+    if ((st = upload(&p->d_chunk_sent, sent)) != CSG_OK) return st;
+    if ((st = upload(&p->d_ready_k, words)) != CSG_OK) return st;
+    const size_t n_remote = std::max<size_t>(p->remote_order.size(), 1);
+    CSG_HIP(hipMalloc(&p->d_copy_done, n_remote * 4));
+    CSG_HIP(hipMalloc(&p->d_release_ticks, n_remote * 8));
+    CSG_HIP(hipMalloc(&p->d_copy_state, sizeof(csg::CopyState)));
+    CSG_HIP(hipMemset(p->d_copy_state, 0, sizeof(csg::CopyState)));
+  }
   CSG_HIP(hipDeviceSynchronize());
   std::string err = p->sdma.open(p->device, p->cfg.copy_engines, p->d_scratch, p->d_scratch + 8);
   if (!err.empty()) return fail(CSG_ERR_HIP, "copy engines: %s", err.c_str());
@@ -404,7 +461,7 @@ csg_status begin_call(csg_plan* p, csg_mode mode, CallState* cs) {
   }
   ++p->epoch;
   p->host_diag = csg_diag{0, -1, -1, 0, p->epoch, 0};
-  if (p->consumer() && !p->remote_order.empty()) {
+  if (p->consumer() && !p->remote_order.empty() && !p->kernel_copies()) {
     // this call's signal set was last polled by the kernel two calls back, which must
     // be done before the set is armed again (it normally ended long ago)
     const int set = p->epoch & 1;
@@ -419,9 +476,25 @@ csg_status begin_call(csg_plan* p, csg_mode mode, CallState* cs) {
 }
 
 // The call's prologue on the compute stream (before its kernel, if any).
-csg_status launch_prologue_call(csg_plan* p, hipStream_t compute) {
-  CSG_HIP(csg::launch_prologue(p->d_counters, p->n_chunks(), p->epoch, p->d_ticket, p->d_diag, p->d_slot_count,
-                               p->ws_slices > 0 ? p->map.n_tiles() : 0, compute));
+csg_status launch_prologue_call(csg_plan* p, csg_mode mode, hipStream_t compute) {
+  csg::PrologueArgs pa{};
+  pa.counters = p->d_counters;
+  pa.n_chunks = p->n_chunks();
+  pa.epoch = p->epoch;
+  pa.ticket = p->d_ticket;
+  pa.diag = p->d_diag;
+  pa.slot_count = p->d_slot_count;
+  pa.n_slots = p->ws_slices > 0 ? p->map.n_tiles() : 0;
+  if (p->kernel_copies()) {
+    // consumers' remote chunks are not there until the copy workgroups move them;
+    // the producer waits for nothing before rewriting C (no copy out reads it later)
+    pa.ready_words = p->d_kready;
+    pa.ready_value = (p->consumer() && mode != CSG_MODE_COMPUTE_ONLY) ? 1 : 0;
+    pa.copy_done = p->d_copy_done;
+    pa.n_remote = static_cast<int32_t>(p->remote_order.size());
+    pa.copy_state = p->d_copy_state;
+  }
+  CSG_HIP(csg::launch_prologue(pa, compute));
   CSG_HIP(hipEventRecord(p->ev_prologue, compute));
   return CSG_OK;
 }
@@ -461,7 +534,16 @@ csg_status finish_copies(csg_plan* p, size_t issued) {
   return CSG_OK;
 }
 
-csg_status launch_gemm(csg_plan* p, const void* A, const void* B, void* C, csg_mode mode, hipStream_t compute) {
+// Chunk moves a kernel launch does itself (copy backend CSG_COPY_KERNEL).
+struct KernelCopies {
+  bool copy = false;              // copy workgroups move the copy items src -> dst
+  const void* src = nullptr;
+  void* dst = nullptr;
+  void* c2 = nullptr;             // producer: the epilogue also stores sent chunks here
+};
+
+csg_status launch_gemm(csg_plan* p, const void* A, const void* B, void* C, csg_mode mode, hipStream_t compute,
+                       const KernelCopies* kc = nullptr) {
   csg::GemmArgs a{};
   a.A = A;
   a.B = B;
@@ -496,9 +578,37 @@ csg_status launch_gemm(csg_plan* p, const void* A, const void* B, void* C, csg_m
   // would only cost time
   a.n_tiles_n = (p->consumer() && mode == CSG_MODE_OVERLAP && p->cfg.warm_rows != 2) ? p->map.n_tiles_n : 0;
   a.acquire_fresh = (p->consumer() && (!p->lines_aligned || reinterpret_cast<uintptr_t>(A) % 128 != 0)) ? 1 : 0;
+  int32_t grid = p->grid;
+  if (kc) {
+    // kernel-moved chunks have ready words of their own, which the prologue set
+    a.ready = p->d_ready_k;
+    if (mode == CSG_MODE_COPY_ONLY) {
+      a.n_tiles = 0;  // the copy workgroups alone
+      a.n_tiles_n = 0;
+      grid = p->copy_workgroups();
+    }
+    if (kc->copy && p->n_copy_items > 0) {
+      a.copy_items = p->d_copy_items;
+      a.n_copy_items = p->n_copy_items;
+      a.copy_wgs = p->copy_workgroups();
+      a.copy_src = static_cast<const unsigned char*>(kc->src);
+      a.copy_dst = static_cast<unsigned char*>(kc->dst);
+      a.copy_chunk = p->d_copy_chunk;
+      a.copy_parts = p->d_copy_parts;
+      a.copy_done = p->d_copy_done;
+      a.copy_ready = p->d_kready;
+      a.copy_state = p->d_copy_state;
+      a.release_ticks = p->release_set ? p->d_release_ticks : nullptr;
+    }
+    if (kc->c2) {
+      a.C2 = kc->c2;
+      a.chunk_sent = p->d_chunk_sent;
+    }
+  }
+  p->expected_units = static_cast<uint32_t>(a.n_tiles);
   const int slot = static_cast<int>(p->n_launches % kTimingRing);
   CSG_HIP(hipEventRecord(p->ev_k0[slot], compute));
-  CSG_HIP(csg::launch_chunk_gemm(p->key, a, p->grid, compute));
+  CSG_HIP(csg::launch_chunk_gemm(p->key, a, grid, compute));
   CSG_HIP(hipEventRecord(p->ev_k1[slot], compute));
   ++p->n_launches;
   CSG_HIP(hipEventRecord(p->ev_kernel_done[p->epoch & 1], compute));
@@ -585,6 +695,31 @@ struct CopyIssuer {
   }
 };
 
+// A call whose chunks the kernel moves itself: the prologue and one kernel launch on
+// the compute stream, nothing on the copy stream, no host waits. Consumers: the copy
+// workgroups move staging -> landing (copy-only: they alone run). Producer: overlap
+// calls send from the epilogue (c2 = outgoing); copy-only calls move C -> outgoing.
+csg_status kernel_copy_call(csg_plan* p, const void* a, const void* staging, const void* b, void* c, void* outgoing,
+                            csg_mode mode, hipStream_t compute) {
+  CallState cs;
+  csg_status st = begin_call(p, mode, &cs);
+  if (st != CSG_OK) return st;
+  if ((st = launch_prologue_call(p, mode, compute)) != CSG_OK) return st;
+  KernelCopies kc;
+  if (p->consumer()) {
+    kc.copy = mode != CSG_MODE_COMPUTE_ONLY;
+    kc.src = staging;
+    kc.dst = const_cast<void*>(a);
+  } else if (mode == CSG_MODE_COPY_ONLY) {
+    kc.copy = true;
+    kc.src = c;
+    kc.dst = outgoing;
+  } else if (mode == CSG_MODE_OVERLAP) {
+    kc.c2 = outgoing;
+  }
+  return launch_gemm(p, a, b, c, mode, compute, &kc);
+}
+
 csg_status consumer_call(csg_plan* p, void* landing, const void* staging, const void* b, void* c, csg_mode mode,
                          void* compute_v, void* copy_v) {
   if (p->device < 0) return fail(CSG_ERR_STATE, "host-only plan (created with device < 0) cannot run");
@@ -595,6 +730,7 @@ csg_status consumer_call(csg_plan* p, void* landing, const void* staging, const 
   hipStream_t compute = static_cast<hipStream_t>(compute_v), copy = static_cast<hipStream_t>(copy_v);
   DeviceGuard g(p->device);
   if (g.err != hipSuccess) return hip_fail(g.err, "hipSetDevice");
+  if (p->kernel_copies()) return kernel_copy_call(p, landing, staging, b, c, nullptr, mode, compute);
   CallState cs;
   // the kernel that last read the landing rows (before this call's own)
   const uint32_t prev_reader = p->last_kernel_epoch;
@@ -609,7 +745,7 @@ csg_status consumer_call(csg_plan* p, void* landing, const void* staging, const 
     if ((st = ready_copies(p, copy, cs, false)) != CSG_OK) return st;
     if ((st = issuer.run(false)) != CSG_OK) return st;
   }
-  if ((st = launch_prologue_call(p, compute)) != CSG_OK) return st;
+  if ((st = launch_prologue_call(p, mode, compute)) != CSG_OK) return st;
   if (mode != CSG_MODE_COPY_ONLY && (st = launch_gemm(p, landing, b, c, mode, compute)) != CSG_OK) return st;
   if (!copies) return CSG_OK;
   if ((st = issuer.run(true)) != CSG_OK) return st;
@@ -746,9 +882,11 @@ csg_status csg_plan_create(csg_op op, int64_t M, int64_t N, int64_t K, csg_dtype
   if (c.bk == 0) c.bk = bf16 ? 64 : 16;
   if (c.timeout_ms == 0) c.timeout_ms = 2000;
   if (c.split_k == 0) c.split_k = 1;
+  if (c.copy_workgroups == 0) c.copy_workgroups = kDefaultCopyWorkgroups;
   if (c.bm < 1 || c.bn < 1 || c.bk < 1 || c.copy_engines < 0 || c.copy_engines > 32 || c.timeout_ms < 1 ||
       c.split_k < 1 || c.split_k > 64 || c.tail_split < 0 || c.tail_split > 64 || c.tail_chunks < 0 ||
-      c.trace < 0 || c.trace > 1 || c.warm_rows < 0 || c.warm_rows > 2 ||
+      c.trace < 0 || c.trace > 1 || c.warm_rows < 0 || c.warm_rows > 2 || c.copy_backend < 0 ||
+      c.copy_backend > CSG_COPY_KERNEL || c.copy_workgroups < 0 || c.copy_workgroups > 4096 ||
       c.num_workgroups < 0 || c.tile_dispatch < 0 || c.tile_dispatch > 2 || c.intra_order != 0)
     return fail(CSG_ERR_INVALID, "bad plan configuration");
   // split tiles run every slice on their own die (no stealing): every die needs
@@ -776,6 +914,14 @@ csg_status csg_plan_create(csg_op op, int64_t M, int64_t N, int64_t K, csg_dtype
   }
   for (int32_t c_id : p->sched.order)
     if (!p->sched.chunks[c_id].is_local) p->remote_order.push_back(c_id);
+  if (op == CSG_GEMM_RS && c.copy_backend == CSG_COPY_KERNEL)
+    for (const csg::ChunkDesc& ch : p->sched.chunks)
+      if (ch.row_begin % c.bm != 0) {
+        delete p;
+        return fail(CSG_ERR_UNSUPPORTED,
+                    "sending from the epilogue needs every chunk to start on a multiple of bm = %d (row %lld)", c.bm,
+                    static_cast<long long>(ch.row_begin));
+      }
 
   if (device >= 0) {
     p->key = csg::KernelKey{bf16 ? csg::InType::BF16 : csg::InType::F32, out_dtype == CSG_BF16, op == CSG_GEMM_RS,
@@ -864,6 +1010,7 @@ csg_status csg_plan_set_copy_delays(csg_plan* p, const float* delay_us_host, int
   if (!p) return fail(CSG_ERR_INVALID, "plan is NULL");
   if (!delay_us_host) {
     p->delays_us.clear();
+    p->release_set = false;
     return CSG_OK;
   }
   if (n != static_cast<int32_t>(p->remote_order.size()))
@@ -871,6 +1018,22 @@ csg_status csg_plan_set_copy_delays(csg_plan* p, const float* delay_us_host, int
   for (int32_t i = 0; i < n; ++i)
     if (!(delay_us_host[i] >= 0.0f) || delay_us_host[i] > 1e6f) return fail(CSG_ERR_INVALID, "bad delay %d", i);
   p->delays_us.assign(delay_us_host, delay_us_host + n);
+  if (p->device >= 0 && p->kernel_copies() && n > 0) {
+    // copy workgroups read the release times from device memory: wait until no kernel
+    // of this plan still does
+    DeviceGuard g(p->device);
+    if (g.err != hipSuccess) return hip_fail(g.err, "hipSetDevice");
+    for (int par = 0; par < 2; ++par)
+      if (p->kernel_pending[par]) CSG_HIP(hipEventSynchronize(p->ev_kernel_done[par]));
+    std::vector<uint64_t> ticks(n);
+    double t = 0.0;
+    for (int32_t i = 0; i < n; ++i) {
+      t += delay_us_host[i];
+      ticks[i] = static_cast<uint64_t>(t * 100.0);  // 100 MHz wall clock
+    }
+    CSG_HIP(hipMemcpy(p->d_release_ticks, ticks.data(), ticks.size() * 8, hipMemcpyHostToDevice));
+    p->release_set = true;
+  }
   return CSG_OK;
 }
 
@@ -900,10 +1063,11 @@ csg_status csg_gemm_rs(csg_plan* p, const void* a, const void* b_nk, void* c, vo
   hipStream_t compute = static_cast<hipStream_t>(compute_stream), copy = static_cast<hipStream_t>(copy_stream);
   DeviceGuard g(p->device);
   if (g.err != hipSuccess) return hip_fail(g.err, "hipSetDevice");
+  if (p->kernel_copies()) return kernel_copy_call(p, a, nullptr, b_nk, c, c_outgoing, mode, compute);
   CallState cs;
   csg_status st = begin_call(p, mode, &cs);
   if (st != CSG_OK) return st;
-  if ((st = launch_prologue_call(p, compute)) != CSG_OK) return st;
+  if ((st = launch_prologue_call(p, mode, compute)) != CSG_OK) return st;
   if (mode != CSG_MODE_COPY_ONLY && (st = launch_gemm(p, a, b_nk, c, mode, compute)) != CSG_OK) return st;
   if (mode == CSG_MODE_COMPUTE_ONLY || p->remote_order.empty()) return CSG_OK;
   // copy-only reads the C a previous kernel wrote: that kernel must have finished
@@ -963,10 +1127,10 @@ csg_status csg_plan_check(csg_plan* p, csg_diag* out) {
     CSG_HIP(hipMemcpyAsync(&dd, p->d_diag, sizeof dd, hipMemcpyDeviceToHost, p->aux));
     CSG_HIP(hipStreamSynchronize(p->aux));
     if (dd.timed_out && !d.timed_out) d = csg_diag{1, dd.chunk, dd.tile, dd.observed, dd.epoch, 0};
-    if (!d.timed_out && p->kernel_pending[p->epoch & 1] && dd.units_done != static_cast<uint32_t>(p->n_units)) {
+    if (!d.timed_out && p->kernel_pending[p->epoch & 1] && dd.units_done != p->expected_units) {
       if (out) *out = d;
-      return fail(CSG_ERR_STATE, "the kernel ran %u of %d work units (a die without workgroups?)", dd.units_done,
-                  p->n_units);
+      return fail(CSG_ERR_STATE, "the kernel ran %u of %u work units (a die without workgroups?)", dd.units_done,
+                  p->expected_units);
     }
   }
   if (out) *out = d;

@@ -464,6 +464,119 @@ __device__ void reduce_slices(int n, Load load, Store store) {
 }
 
 // ---------------------------------------------------------------------------------
+// Copy workgroups (Section 5.2, realization (4): load/store on specialized
+// workgroups, with global-memory signals)
+// ---------------------------------------------------------------------------------
+
+// Copy workgroup i (of n) moves items i, i + n, i + 2n, ... (slabs of the chunks in
+// arrival order), so the copy workgroups move each chunk together and the chunks
+// land in order, with no shared ticket to contend for. A slab moves as 16-byte
+// vectors, written through at device scope (sc1: a completed store is visible to
+// every die; the readers are this device's tiles). Non-temporal loads and
+// system-scope stores measured 30-45 % slower with 16 to 64 copy workgroups. The
+// workgroup waits until its stores have completed before it counts the item; the
+// one that counts a chunk's last item sets the chunk's ready word to 0. A tile on
+// any die that then sees the word at 0 reads the rows from memory: no L2 holds a
+// line of them from before (chunks are not read before they are ready, lines left by
+// earlier work are dropped at kernel launch, and line-unaligned chunks drop the
+// caches on first sight, as with the copy engines). Copy workgroups never wait for
+// tiles, so the chunks always land.
+template <int kThreads>
+__device__ void copy_chunks(const GemmArgs& a, int tid, int copier, int n_copiers) {
+  constexpr int U = 8;
+  constexpr int kStep = kThreads * 16 * U;
+  const uint64_t t0 = a.copy_state->t0;
+  int prev = -1;  // the item this workgroup moved last (counted by thread 0 at the next turn)
+  // The one thread-0 step of a turn sits right after a barrier and the loop leaves on
+  // a uniform value, so every lane of a wave reaches each barrier together.
+  for (int item = copier;; item += n_copiers) {
+    wait_dma_all();  // this thread's stores of the previous item have completed
+    __syncthreads();
+    if (tid == 0 && prev >= 0) {
+      const CopyItem done_it = a.copy_items[prev];
+      const uint32_t done =
+          __hip_atomic_fetch_add(a.copy_done + done_it.rpos, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) + 1u;
+      if (done == static_cast<uint32_t>(a.copy_parts[done_it.rpos]))
+        __hip_atomic_store(a.copy_ready + a.copy_chunk[done_it.rpos], int64_t{0}, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_SYSTEM);
+    }
+    if (item >= a.n_copy_items) break;
+    prev = item;
+    const CopyItem it = a.copy_items[item];
+    if (a.release_ticks) {
+      // the chunk's release time (a simulated peer that is late); bounded by the timeout
+      if (tid == 0) {
+        const uint64_t due = t0 + a.release_ticks[it.rpos];
+        const uint64_t t1 = wall_clock64();
+        while (wall_clock64() < due && wall_clock64() - t1 < a.timeout_ticks) __builtin_amdgcn_s_sleep(2);
+      }
+      __syncthreads();
+    }
+    const int bytes = __builtin_amdgcn_readfirstlane(it.bytes);
+    const int vec_bytes = bytes & ~15;
+    const __amdgpu_buffer_rsrc_t rsS = make_rsrc(a.copy_src + it.off, vec_bytes);
+    const __amdgpu_buffer_rsrc_t rsD = make_rsrc(a.copy_dst + it.off, vec_bytes);
+    // Two register stages: the loads of step k + 1 are in flight while step k is
+    // stored. Every 16-byte access is wholly inside the resource or wholly past its
+    // end (vec_bytes is a multiple of 16); those past it read 0 and write nothing.
+    // The whole offset is the vector operand, which the range check covers.
+    auto load_step = [&](u32x4(&v)[U], int base) {
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        v[u] = __builtin_amdgcn_raw_buffer_load_b128(rsS, base + (u * kThreads + tid) * 16, 0, 0);
+    };
+    auto store_step = [&](const u32x4(&v)[U], int base) {
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        __builtin_amdgcn_raw_buffer_store_b128(v[u], rsD, base + (u * kThreads + tid) * 16, 0, kPolicySc1);
+    };
+    // The next step's loads are issued unconditionally (past the end they read
+    // nothing), so the compiler's wait before each store covers only that store's data.
+    u32x4 v0[U], v1[U];
+    load_step(v0, 0);
+    for (int base = 0; base < vec_bytes; base += 2 * kStep) {
+      load_step(v1, base + kStep);
+      store_step(v0, base);
+      load_step(v0, base + 2 * kStep);
+      store_step(v1, base + kStep);
+    }
+    // a tail of 4, 8 or 12 bytes (rows of C whose byte length is not a multiple of 16)
+    if (tid < (bytes - vec_bytes) / 4) {
+      const uint32_t* src = reinterpret_cast<const uint32_t*>(a.copy_src + it.off + vec_bytes) + tid;
+      uint32_t* dst = reinterpret_cast<uint32_t*>(a.copy_dst + it.off + vec_bytes) + tid;
+      __hip_atomic_store(dst, *src, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
+  }
+}
+
+// Copies an output tile (rows x row_bytes at pitch bytes, through the resource
+// over its rows of C) to dst, the same tile of another buffer with the same pitch:
+// 8-byte units (row segments and row starts are multiples of 8 bytes, as N is a
+// multiple of 4), reread from L2 where the tile's stores just landed, written
+// through to memory. kRowBytes is the widest segment (a full tile row).
+template <int kThreads, int kRowBytes>
+__device__ void send_tile(const __amdgpu_buffer_rsrc_t& rsC, unsigned char* dst, int rows, int row_bytes, int pitch,
+                          int tid) {
+  constexpr int kUnitsPerRow = kRowBytes / 8;
+  constexpr int U = 8;
+  const __amdgpu_buffer_rsrc_t rsD = make_rsrc(dst, static_cast<int64_t>(rows) * pitch);
+  const int total = rows * kUnitsPerRow;
+  for (int base = 0; base < total; base += kThreads * U) {
+    u32x2 v[U];
+    int off[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int unit = base + u * kThreads + tid;
+      const int row = unit / kUnitsPerRow, col = (unit % kUnitsPerRow) * 8;
+      off[u] = (row < rows && col < row_bytes) ? row * pitch + col : kDropOffset;
+      v[u] = __builtin_amdgcn_raw_buffer_load_b64(rsC, off[u], 0, kPolicySc0);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) __builtin_amdgcn_raw_buffer_store_b64(v[u], rsD, off[u], 0, kPolicySc0 | kPolicySc1);
+  }
+}
+
+// ---------------------------------------------------------------------------------
 // The persistent kernel
 // ---------------------------------------------------------------------------------
 template <class Loop, bool kOutBf16, bool kProducer>
@@ -487,6 +600,12 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
   asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID, 0, 4)" : "=s"(xcd));
   xcd %= kXcdLists;
   uint32_t units = 0;  // work units this workgroup executed (the host checks the total)
+
+  // Workgroups 0 .. copy_wgs - 1 move the chunks, then take tiles too. The dispatcher
+  // starts workgroups in index order, so they are running whenever a tile waits.
+  const int n_copiers = a.copy_wgs < static_cast<int>(gridDim.x) ? a.copy_wgs : static_cast<int>(gridDim.x);
+  if (a.n_copy_items > 0 && static_cast<int>(blockIdx.x) < n_copiers)
+    copy_chunks<kThreads>(a, tid, static_cast<int>(blockIdx.x), n_copiers);
 
   int iter = 0;
   for (;; ++iter) {
@@ -723,6 +842,17 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
       // invalidated.
       wait_dma_all();
       __syncthreads();
+      if (a.C2 != nullptr && a.chunk_sent[a.list_ids[a.list_ptr[pos]]] != 0) {
+        // Sending from the epilogue (Section 5.2, load/store on the computing
+        // workgroup): the tile's output rows, just stored, go to the outgoing buffer
+        // too (plans that send this way keep every tile inside one chunk), and count
+        // as sent once these stores have completed as well
+        send_tile<kThreads, BN * kOutBytes>(rsC, static_cast<unsigned char*>(a.C2) +
+                                                     (static_cast<int64_t>(td.row_begin) * a.N + col0) * kOutBytes,
+                                            g.arows, g.brows * kOutBytes, N32 * kOutBytes, tid);
+        wait_dma_all();
+        __syncthreads();
+      }
       if (tid == 0) {
         for (int p = a.list_ptr[pos]; p < a.list_ptr[pos + 1]; ++p) {
           const int c = a.list_ids[p];
@@ -741,22 +871,25 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
   if (tid == 0) atomicAdd(&a.diag->units_done, units);
 }
 
-__global__ __launch_bounds__(kPrologueThreads) void chunk_prologue(uint32_t* counters, int32_t n_chunks,
-                                                                    uint32_t epoch, uint32_t* ticket, DeviceDiag* diag,
-                                                                    uint32_t* slot_count, int32_t n_slots) {
+__global__ __launch_bounds__(kPrologueThreads) void chunk_prologue(PrologueArgs p) {
   const int tid = threadIdx.x;
-  for (int i = tid; i < n_slots; i += blockDim.x) slot_count[i] = 0u;
-  if (counters)
-    for (int c = tid; c < n_chunks; c += blockDim.x) counters[c] = 0u;
-  if (tid < kXcdLists) ticket[tid] = 0u;
+  for (int i = tid; i < p.n_slots; i += blockDim.x) p.slot_count[i] = 0u;
+  if (p.counters)
+    for (int c = tid; c < p.n_chunks; c += blockDim.x) p.counters[c] = 0u;
+  if (p.ready_words)
+    for (int c = tid; c < p.n_chunks; c += blockDim.x) p.ready_words[c] = p.ready_value;
+  if (p.copy_done)
+    for (int i = tid; i < p.n_remote; i += blockDim.x) p.copy_done[i] = 0u;
+  if (tid < kXcdLists) p.ticket[tid] = 0u;
   if (tid == 0) {
-    diag->timed_out = 0u;
-    diag->chunk = -1;
-    diag->tile = -1;
-    diag->observed = 0u;
-    diag->epoch = epoch;
-    diag->abort = 0u;
-    diag->units_done = 0u;
+    p.diag->timed_out = 0u;
+    p.diag->chunk = -1;
+    p.diag->tile = -1;
+    p.diag->observed = 0u;
+    p.diag->epoch = p.epoch;
+    p.diag->abort = 0u;
+    p.diag->units_done = 0u;
+    if (p.copy_state) p.copy_state->t0 = wall_clock64();  // release times count from here
   }
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "");
 }
@@ -830,10 +963,8 @@ hipError_t launch_chunk_gemm(const KernelKey& key, const GemmArgs& args, int32_t
   return v->launch(args, grid, stream);
 }
 
-hipError_t launch_prologue(uint32_t* counters, int32_t n_chunks, uint32_t epoch, uint32_t* ticket, DeviceDiag* diag,
-                           uint32_t* slot_count, int32_t n_slots, hipStream_t stream) {
-  hipLaunchKernelGGL(chunk_prologue, dim3(1), dim3(kPrologueThreads), 0, stream, counters, n_chunks, epoch, ticket, diag,
-                     slot_count, n_slots);
+hipError_t launch_prologue(const PrologueArgs& args, hipStream_t stream) {
+  hipLaunchKernelGGL(chunk_prologue, dim3(1), dim3(kPrologueThreads), 0, stream, args);
   return hipGetLastError();
 }
 

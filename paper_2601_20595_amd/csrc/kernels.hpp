@@ -33,6 +33,19 @@ struct TileDesc {
   int32_t slice;      // split tiles: slice index | (number of slices << 16)
 };
 
+// One slab of a chunk moved by the kernel's copy workgroups: bytes [off, off + bytes)
+// of the copy source, written to the same offsets of the destination.
+struct CopyItem {
+  int64_t off;
+  int32_t bytes;  // a multiple of 4
+  int32_t rpos;   // position of the chunk among the remote chunks (arrival / emission order)
+};
+
+// Per-call state of the copy workgroups, set by the prologue.
+struct CopyState {
+  uint64_t t0;  // wall clock (100 MHz) when the call's prologue ran; release times count from it
+};
+
 struct GemmArgs {
   const void* A;             // rows of A (AG: landing buffer; grouped: routed X), K contiguous
   const void* B;             // N x K, or E x N x K
@@ -78,6 +91,41 @@ struct GemmArgs {
   // when its waits were over, when it finished, (die << 32 | workgroup id), and the
   // shader-clock counter when its waits were over and when it finished.
   uint64_t* trace;
+  // Chunk moves done by the kernel itself (Section 5.2, load/store realizations)
+  // instead of the copy engines; all zero / null when the engines move the chunks.
+  // Copy workgroups: workgroups 0 .. copy_wgs - 1 move the copy items (in arrival
+  // order, item i by workgroup i mod copy_wgs), then join the tile list.
+  const CopyItem* copy_items;
+  int32_t n_copy_items;      // 0: no copy workgroups in this launch
+  int32_t copy_wgs;
+  const unsigned char* copy_src;
+  unsigned char* copy_dst;
+  const int32_t* copy_chunk;     // per remote position: chunk id
+  const int32_t* copy_parts;     // per remote position: its copy items
+  uint32_t* copy_done;           // per remote position: items finished (cleared by the prologue)
+  int64_t* copy_ready;           // per chunk: ready word, set to 0 once the chunk's last item is done
+  CopyState* copy_state;
+  const uint64_t* release_ticks; // per remote position: earliest start after t0, 100 MHz ticks (null: none)
+  // Producer: output rows of a chunk that is sent are also stored here (same layout
+  // as C) by the tile epilogue; null when the copy engines send them.
+  void* C2;
+  const int32_t* chunk_sent;     // per chunk: 1 if it is sent (producer with C2)
+};
+
+// Everything the per-call prologue resets.
+struct PrologueArgs {
+  uint32_t* counters;
+  int32_t n_chunks;
+  uint32_t epoch;
+  uint32_t* ticket;
+  DeviceDiag* diag;
+  uint32_t* slot_count;   // split-K slot counts (null: none)
+  int32_t n_slots;
+  int64_t* ready_words;   // kernel-moved chunks: per chunk ready word, set to ready_value (null: none)
+  int64_t ready_value;    // 1 = not landed yet, 0 = ready
+  uint32_t* copy_done;    // per remote position, cleared
+  int32_t n_remote;
+  CopyState* copy_state;  // its t0 set to the prologue's wall clock
 };
 
 constexpr int kTraceWords = 6;
@@ -105,8 +153,8 @@ hipError_t kernel_grid(const KernelKey& key, int device, int32_t* grid);
 hipError_t launch_chunk_gemm(const KernelKey& key, const GemmArgs& args, int32_t grid, hipStream_t stream);
 
 // Per-call set-up on the compute stream: clears the per-chunk counters, the
-// tickets, the split-K slot counts and the diagnostics.
-hipError_t launch_prologue(uint32_t* counters, int32_t n_chunks, uint32_t epoch, uint32_t* ticket, DeviceDiag* diag,
-                           uint32_t* slot_count, int32_t n_slots, hipStream_t stream);
+// tickets, the split-K slot counts, the diagnostics and the copy workgroups' state,
+// and sets the ready words of kernel-moved chunks.
+hipError_t launch_prologue(const PrologueArgs& args, hipStream_t stream);
 
 }  // namespace csg

@@ -156,6 +156,22 @@ def test_validation_errors():
                    device=-1) == csg.CSG_OK
 
 
+def test_kernel_copy_backend_validation():
+    s = csg.Schedule.uniform(2, 0, 64, 2, "ring")
+    for bad in ({"copy_backend": 2}, {"copy_backend": -1}, {"copy_workgroups": -1}, {"copy_workgroups": 5000}):
+        assert _status(csg.Plan, "ag", 128, 64, 64, "bf16", "bf16", s, cfg=bad, device=-1) == csg.CSG_ERR_INVALID
+    kc = {"copy_backend": "kernel"}
+    assert _status(csg.Plan, "ag", 128, 64, 64, "bf16", "bf16", s, cfg=kc, device=-1) == csg.CSG_OK
+    # GEMM-RS sends from the tile epilogue: a tile must not mix rows of two chunks, so
+    # every chunk starts on a multiple of bm (256 for bf16 by default, 64 for fp32)
+    rs = csg.Schedule.uniform(4, 1, 512, 2, "rs_ring")                 # 256-row chunks
+    assert _status(csg.Plan, "rs", 2048, 64, 64, "bf16", "bf16", rs, cfg=kc, device=-1) == csg.CSG_OK
+    rs = csg.Schedule.uniform(4, 1, 256, 2, "rs_ring")                 # 128-row chunks
+    assert _status(csg.Plan, "rs", 1024, 64, 64, "bf16", "bf16", rs, cfg=kc, device=-1) == csg.CSG_ERR_UNSUPPORTED
+    assert _status(csg.Plan, "rs", 1024, 64, 64, "f32", "f32", rs, cfg=kc, device=-1) == csg.CSG_OK
+    assert _status(csg.Plan, "rs", 1024, 64, 64, "bf16", "bf16", rs, device=-1) == csg.CSG_OK   # copy engines
+
+
 def test_host_only_plan_cannot_run_and_delays_are_checked():
     s = csg.Schedule.uniform(4, 0, 64, 2, "ring")
     p = csg.Plan("ag", 256, 64, 64, "bf16", "bf16", s, device=-1)
