@@ -43,6 +43,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target length of the CPU baseline sample")
     ap.add_argument("--lanes", type=int, default=0, help="SDMA copy lanes (0 = library default)")
+    ap.add_argument("--no-kernel-copies", action="store_true",
+                    help="skip the comparison with chunks moved by the kernel's own workgroups")
     return ap.parse_args()
 
 
@@ -107,31 +109,33 @@ def main():
     del cal_src, cal_dst
     torch.cuda.synchronize()
 
-    def call(mode):
+    def call(mode, p=None):
+        p = p or plan
         if w.op == "rs":
-            plan.gemm_rs(a_full, b, c, outgoing, mode, compute, copy)
+            p.gemm_rs(a_full, b, c, outgoing, mode, compute, copy)
         elif w.op == "grouped":
-            plan.grouped_gemm(landing, a_full, b, c, mode, compute, copy)
+            p.grouped_gemm(landing, a_full, b, c, mode, compute, copy)
         else:
-            plan.ag_gemm(landing, a_full, b, c, mode, compute, copy)
+            p.ag_gemm(landing, a_full, b, c, mode, compute, copy)
 
-    def timed_loop(mode, steps, warmup):
+    def timed_loop(mode, steps, warmup, p=None):
         """Back-to-back calls, as a training or serving loop makes them: no event or
         stream dependency between steps beyond what the library itself orders, so the
         copies of one step may start while the previous step's kernel still runs.
         Returns wall seconds for `steps` calls and the kernel durations (ms) the
         library timed on the compute stream."""
+        p = p or plan
         for _ in range(warmup):
-            call(mode)
-        plan.check()
+            call(mode, p)
+        p.check()
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for _ in range(steps):
-            call(mode)
-        plan.check()              # every copy the steps issued has completed
+            call(mode, p)
+        p.check()                 # every copy the steps issued has completed
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
-        return wall, plan.kernel_times(steps)
+        return wall, p.kernel_times(steps)
 
     def bracketed(mode, reps, warmup):
         """Isolated calls (the GPU idle before each): per call, the wall time from the
@@ -211,9 +215,39 @@ def main():
                                   "frac": round(w.flops / (k_comp * 1e-3) / 1e12 / peak, 4),
                                   "kernel_ms_mean": round(k_comp, 4)},
     }
+    if not args.no_kernel_copies:
+        rec["kernel_copy_backend"] = kernel_copy_sweep(w, sched, group_rows, d, timed_loop, moved_bytes, args)
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(w, d, chunks, args.cpu_seconds)
     print(json.dumps(rec), flush=True)
+
+
+def kernel_copy_sweep(w, sched, group_rows, d, timed_loop, moved_bytes, args, sweep=(32, 64, 128)):
+    """The same workload with the chunks moved by the GEMM kernel's own workgroups
+    (CSG_COPY_KERNEL: copy workgroups for AG / grouped, sends from the tile epilogue
+    for GEMM-RS), per number of copy workgroups: steady-state ms per step in each
+    mode, as for the copy-engine path above. Outside the timed region; a comparison
+    of two realizations of the same chunk schedule, not the headline."""
+    import paper_2601_20595_amd as csg
+    out = {"note": "chunks moved by the kernel's workgroups instead of SDMA; steady-state ms per step",
+           "copy_workgroups": {}}
+    for cw in sweep:
+        p = csg.Plan(w.op, w.M, w.N, w.K, w.dtype, w.out_dtype, sched, group_rows=group_rows,
+                     cfg={"copy_backend": "kernel", "copy_workgroups": cw})
+        if d.delays_us is not None:
+            p.set_copy_delays(d.delays_us)
+        ms = {}
+        for mode in ("overlap", "compute_only", "copy_only"):
+            wall, _ = timed_loop(mode, args.steps, args.warmup, p)
+            ms[mode] = wall * 1e3 / args.steps
+        p.close()
+        out["copy_workgroups"][str(cw)] = {
+            "ms_per_step": round(ms["overlap"], 4), "ms_per_step_compute_only": round(ms["compute_only"], 4),
+            "ms_per_step_copy_only": round(ms["copy_only"], 4),
+            "overlap_eff": round(max(ms["compute_only"], ms["copy_only"]) / ms["overlap"], 4),
+            "tflops": round(w.flops / (ms["overlap"] * 1e-3) / 1e12, 2),
+            "copy_only_GBps": round(moved_bytes / (ms["copy_only"] * 1e-3) / 1e9, 2)}
+    return out
 
 
 KERNEL_SOURCES = ("paper_2601_20595_amd/csrc/chunk_gemm.hip", "paper_2601_20595_amd/csrc/kernels.hpp")

@@ -607,9 +607,7 @@ csg_status launch_gemm(csg_plan* p, const void* A, const void* B, void* C, csg_m
   }
   p->expected_units = static_cast<uint32_t>(a.n_tiles);
   const int slot = static_cast<int>(p->n_launches % kTimingRing);
-  CSG_HIP(hipEventRecord(p->ev_k0[slot], compute));
-  CSG_HIP(csg::launch_chunk_gemm(p->key, a, grid, compute));
-  CSG_HIP(hipEventRecord(p->ev_k1[slot], compute));
+  CSG_HIP(csg::launch_chunk_gemm(p->key, a, grid, compute, p->ev_k0[slot], p->ev_k1[slot]));
   ++p->n_launches;
   CSG_HIP(hipEventRecord(p->ev_kernel_done[p->epoch & 1], compute));
   p->kernel_pending[p->epoch & 1] = true;

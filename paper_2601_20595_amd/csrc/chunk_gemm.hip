@@ -24,6 +24,7 @@
 // The MFMA takes the B fragment as its first operand, so each lane ends up with
 // four runs of four consecutive output columns of one output row, which the
 // epilogue writes as 8-byte (bf16) or 16-byte (fp32) stores.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include "kernels.hpp"
@@ -900,9 +901,13 @@ __global__ __launch_bounds__(kPrologueThreads) void chunk_prologue(PrologueArgs 
 using LoopBf16_256 = Bf16Loop<256, 256>;
 using LoopF32_64 = F32Loop<64, 64>;
 
+// The timing events (either may be null) take the dispatch's own start and end
+// timestamps, not those of separate markers queued around it.
 template <class Loop, bool kOutBf16, bool kProducer>
-static hipError_t launch_one(const GemmArgs& args, int32_t grid, hipStream_t stream) {
-  hipLaunchKernelGGL((chunk_gemm<Loop, kOutBf16, kProducer>), dim3(grid), dim3(Loop::THREADS), 0, stream, args);
+static hipError_t launch_one(const GemmArgs& args, int32_t grid, hipStream_t stream, hipEvent_t start,
+                             hipEvent_t stop) {
+  hipExtLaunchKernelGGL((chunk_gemm<Loop, kOutBf16, kProducer>), dim3(grid), dim3(Loop::THREADS), 0, stream, start,
+                        stop, 0, args);
   return hipGetLastError();
 }
 
@@ -918,7 +923,7 @@ struct Variant {
   bool producer;
   int bm, bn, bk;
   int threads;
-  hipError_t (*launch)(const GemmArgs&, int32_t, hipStream_t);
+  hipError_t (*launch)(const GemmArgs&, int32_t, hipStream_t, hipEvent_t, hipEvent_t);
   const void* (*func)();
 };
 
@@ -957,10 +962,11 @@ hipError_t kernel_grid(const KernelKey& key, int device, int32_t* grid) {
   return hipSuccess;
 }
 
-hipError_t launch_chunk_gemm(const KernelKey& key, const GemmArgs& args, int32_t grid, hipStream_t stream) {
+hipError_t launch_chunk_gemm(const KernelKey& key, const GemmArgs& args, int32_t grid, hipStream_t stream,
+                             hipEvent_t start, hipEvent_t stop) {
   const Variant* v = find_variant(key);
   if (!v) return hipErrorInvalidValue;
-  return v->launch(args, grid, stream);
+  return v->launch(args, grid, stream, start, stop);
 }
 
 hipError_t launch_prologue(const PrologueArgs& args, hipStream_t stream) {

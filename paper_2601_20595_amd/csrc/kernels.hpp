@@ -150,7 +150,9 @@ bool kernel_supported(const KernelKey& key);
 int32_t kernel_max_chunks();
 // Persistent grid size: co-resident workgroups on the device.
 hipError_t kernel_grid(const KernelKey& key, int device, int32_t* grid);
-hipError_t launch_chunk_gemm(const KernelKey& key, const GemmArgs& args, int32_t grid, hipStream_t stream);
+// start/stop (may be null) receive the kernel's own start and end timestamps
+hipError_t launch_chunk_gemm(const KernelKey& key, const GemmArgs& args, int32_t grid, hipStream_t stream,
+                             hipEvent_t start, hipEvent_t stop);
 
 // Per-call set-up on the compute stream: clears the per-chunk counters, the
 // tickets, the split-K slot counts, the diagnostics and the copy workgroups' state,
