@@ -1,0 +1,100 @@
+"""The autotuner's host logic: the search space and the choice of the best
+candidate, with stand-in plans (no GPU)."""
+import time
+
+import pytest
+
+import paper_2601_20595_amd as csg
+from paper_2601_20595_amd import tune
+
+
+def test_search_space_shape():
+    ag = tune.search_space("ag")
+    # backends: sdma + 3 copy-workgroup counts; dispatch 2; (split 1 x tail 2) + (split 2 x no tail)
+    assert len(ag) == 4 * 2 * 3
+    assert ag[0].cfg_dict() == {} and ag[0].chunks_per_shard is None      # the library's default plan first
+    assert len(set(ag)) == len(ag)
+    for c in ag:
+        d = c.cfg_dict()
+        assert not (d.get("split_k", 1) > 1 and d.get("tail_split", 0) > 1)
+        assert ("copy_workgroups" in d) == (d.get("copy_backend", 0) == 1)
+    rs = tune.search_space("rs", chunk_splits=(1, 2))
+    kernel = [c for c in rs if c.cfg_dict().get("copy_backend") == 1]
+    assert kernel and all("copy_workgroups" not in c.cfg_dict() for c in kernel)   # sends from the epilogue
+    assert {c.chunks_per_shard for c in rs} == {1, 2}
+    assert len(tune.search_space("grouped", kernel_copies=False)) == 2 * 3
+    with pytest.raises(ValueError):
+        tune.search_space("gemm")
+
+
+class _FakePlan:
+    def __init__(self, ms, fail=False):
+        self.ms, self.fail, self.closed, self.calls = ms, fail, False, 0
+
+    def check(self):
+        if self.fail:
+            raise csg.CsgError(csg.CSG_ERR_TIMEOUT, "csg_plan_check", "stand-in failure")
+
+    def close(self):
+        self.closed = True
+
+
+def test_autotune_picks_fastest_and_records_rejections():
+    cands = tune.search_space("ag", dispatch=(1,), split_k=(1,), tail=((0, 0),), copy_workgroups=(32, 64))
+    assert len(cands) == 3
+    speed = {0: 3.0, 1: 1.0, 2: None}        # candidate index -> ms per call (None: rejected)
+    made = []
+
+    def make(c):
+        i = cands.index(c)
+        if speed[i] is None:
+            raise csg.CsgError(csg.CSG_ERR_UNSUPPORTED, "csg_plan_create", "stand-in rejection")
+        p = _FakePlan(speed[i])
+        made.append(p)
+        return p
+
+    def call(p, mode):
+        assert mode == "overlap"
+        p.calls += 1
+        time.sleep(p.ms * 1e-3)
+
+    res, best_plan = tune.autotune(make, call, cands, steps=3, warmup=1, keep_best=True)
+    assert res.best == cands[1]
+    assert best_plan is made[1] and not best_plan.closed
+    assert made[0].closed                     # measured and released
+    assert made[0].calls == 4 and made[1].calls == 4
+    st = {t.candidate: t.status for t in res.trials}
+    assert st[cands[0]] == "ok" and st[cands[2]].startswith("rejected")
+    assert res.best_ms == pytest.approx(1.0, abs=5.0)
+    assert [r["status"] for r in res.table()] == ["ok", "ok", st[cands[2]]]
+
+
+def test_autotune_failures_and_empty():
+    cands = tune.search_space("ag", dispatch=(1,), split_k=(1,), tail=((0, 0),), copy_workgroups=(32,))
+    plans = [_FakePlan(0.1, fail=True), _FakePlan(0.2)]
+    res, keep = tune.autotune(lambda c: plans[cands.index(c)], lambda p, m: None, cands, steps=1, warmup=0)
+    assert keep is None and res.best == cands[1]
+    assert res.trials[0].status.startswith("failed") and plans[0].closed and plans[1].closed
+    with pytest.raises(ValueError):
+        tune.autotune(lambda c: None, lambda p, m: None, [])
+    with pytest.raises(RuntimeError):
+        tune.autotune(lambda c: _FakePlan(0, fail=True), lambda p, m: None, cands[:1], steps=1, warmup=0)
+
+
+def test_uniform_plan_factory_builds_host_plans_and_rejects_unaligned_epilogue_sends():
+    make = tune.uniform_plan_factory("rs", 1024, 64, 64, "bf16", "bf16", world=4, rank=1, shard_rows=256,
+                                     order="rs_ring", default_q=1, device=-1)
+    kernel = tune.Candidate(2, (("copy_backend", 1),))        # 128-row chunks, 256-row tiles
+    with pytest.raises(csg.CsgError) as e:
+        make(kernel)
+    assert e.value.status == csg.CSG_ERR_UNSUPPORTED
+    p = make(tune.Candidate(None, (("copy_backend", 1),)))   # default Q = 1: 256-row chunks
+    assert p.info.n_chunks == 4
+    p.close()
+    perm_make = tune.uniform_plan_factory("ag", 1024, 64, 64, "bf16", "bf16", world=4, rank=0, shard_rows=256,
+                                          order="permutation", default_q=2,
+                                          perm_for=lambda q: list(reversed(range(3 * q))),
+                                          delays_for=lambda q: [1.0] * (3 * q), device=-1)
+    p = perm_make(tune.Candidate(4, ()))
+    assert p.info.n_chunks == 16
+    p.close()
