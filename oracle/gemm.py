@@ -119,6 +119,50 @@ def gemm_rs(A: np.ndarray, B_nk: np.ndarray, chunks: Sequence[Chunk], order: Seq
     return C, out, log
 
 
+def gemm_ar(A: np.ndarray, B_nk: np.ndarray, chunks: Sequence[Chunk], order: Sequence[int],
+            partials: np.ndarray, reduced_in: np.ndarray, row_subset: Optional[Sequence[int]] = None):
+    """GEMM + AllReduce on one rank (Evaluation: the GEMM-AR operator; Section 5.1,
+    Fig. of communication schedules, the partition-based AllReduce pattern), taken as
+    a reduce-scatter followed by an all-gather over the rank's row shards.
+
+    Every rank r holds a K-slice A_r, B_r of a row-parallel product; the all-reduced
+    result is sum_r A_r . B_r^T. On this rank:
+      - its partial P = A . B_nk^T is produced chunk by chunk in emission order;
+      - a non-local chunk is sent to its owner (reduce-scatter half):
+        outgoing[rows] = P[rows];
+      - an own (local) chunk is reduced with the other ranks' partials of the same
+        rows, partials[j] for the j-th other rank in ascending rank order, stored as
+        [world-1, S, N] over the own shard S (rows own0 .. own0+S-1):
+        C[rows] = P[rows] + sum_j partials[j][rows - own0]; it is then sent to every
+        other rank (all-gather half): outgoing[rows] = C[rows];
+      - a non-local chunk's final rows come from its owner: C[rows] = reduced_in[rows].
+    Returns (C, outgoing, emission_log)."""
+    M = A.shape[0]
+    N = B_nk.shape[0]
+    C = np.full((M, N), np.nan, dtype=np.float64)
+    out = np.full((M, N), np.nan, dtype=np.float64)
+    own = [ch for ch in chunks if ch.is_local]
+    own0 = min(ch.row_begin for ch in own)
+    want = None if row_subset is None else set(int(r) for r in row_subset)
+    log = []
+    for c in order:
+        ch = chunks[int(c)]
+        rows = [r for r in range(ch.row_begin, ch.row_end) if want is None or r in want]
+        if rows:
+            P = gemm_rows(A, B_nk, rows)
+            if ch.is_local:
+                red = P.copy()
+                for j in range(partials.shape[0]):
+                    red += partials[j][np.asarray(rows) - own0].astype(np.float64)
+                C[rows] = red
+                out[rows] = red
+            else:
+                out[rows] = P
+                C[rows] = reduced_in[rows].astype(np.float64)
+        log.append(int(c))
+    return C, out, log
+
+
 def grouped_gemm(X: np.ndarray, B_enk: np.ndarray, chunks: Sequence[Chunk], order: Sequence[int],
                  row_subset: Optional[Sequence[int]] = None) -> np.ndarray:
     """All-to-all + grouped GEMM on one rank: as the (source, expert) segment

@@ -11,7 +11,8 @@ Generators are ``numpy.random.default_rng([cfg_id, stream, rep])`` with the
 streams
 
     0 = A / X values, 1 = B values, 2 = arrival permutation,
-    3 = copy delays,  4 = token routing.
+    3 = copy delays,  4 = token routing,
+    5 = the peers' partial sums (GEMM-AR), 6 = the other shards' reduced rows (GEMM-AR).
 
 Workload shapes are tensor-parallel FFN slices of Llama-3-8B-like
 (hidden 4096, FFN 14336/8 = 1792) and Llama-3-70B-like (hidden 8192,
@@ -27,6 +28,7 @@ from typing import Optional
 import numpy as np
 
 STREAM_A, STREAM_B, STREAM_PERM, STREAM_DELAY, STREAM_ROUTE = 0, 1, 2, 3, 4
+STREAM_PARTIALS, STREAM_REDUCED = 5, 6
 
 
 def rng(cfg_id: int, stream: int, rep: int = 0) -> np.random.Generator:
@@ -111,7 +113,8 @@ def draw_topk_routing(cfg_id: int, rep: int, n_tokens: int, n_experts: int, topk
 # ----------------------------------------------------------------------------
 @dataclass
 class Workload:
-    """One workload of the benchmark/test suite. ``op`` is "ag", "rs" or "grouped"."""
+    """One workload of the benchmark/test suite. ``op`` is "ag", "rs", "ar" (GEMM +
+    all-reduce) or "grouped"."""
     cfg_id: int
     name: str
     op: str
@@ -154,6 +157,11 @@ WORKLOADS = {
     5: Workload(5, "a2a_grouped_e8_bf16_32768x4096x1792", "grouped", M=32768, N=1792, K=4096,
                 dtype="bf16", out_dtype="bf16", dist="normal", world=8, n_tokens=16384,
                 n_experts=8, topk=2, zipf_s=1.2),
+    # GEMM + all-reduce: the row-parallel down-projection of the 8B-like layer, K = 14336 / 8
+    # per rank, all-reduced over 8 ranks (reduce-scatter then all-gather of 4 chunks per shard)
+    6: Workload(6, "ar_w8_bf16_8192x1792x4096", "ar", M=8192, N=4096, K=1792, dtype="bf16",
+                out_dtype="bf16", dist="normal", world=8, shard_rows=1024, chunks_per_shard=4,
+                order="rs_ring"),
 }
 
 
@@ -167,6 +175,9 @@ class Drawn:
     routing: Optional[np.ndarray] = None     # grouped: [n_tokens, topk] expert ids
     counts: Optional[np.ndarray] = None      # grouped: [world, n_experts] rows per (source, expert)
     tokens: Optional[Matrix] = None          # grouped: un-routed token matrix
+    partials: Optional[Matrix] = None        # ar: [world-1, S, N] the peers' partial sums of this
+                                             # rank's shard, peers in ascending rank order
+    reduced: Optional[Matrix] = None         # ar: [M, N] reduced rows the other shards' owners send
 
 
 def grouped_layout(routing: np.ndarray, world: int, n_experts: int):
@@ -193,12 +204,19 @@ def draw(w: Workload, rep: int = 0, dist: Optional[str] = None, M: Optional[int]
     N = N or w.N
     K = K or w.K
     cid = w.cfg_id
-    if w.op in ("ag", "rs"):
+    if w.op in ("ag", "rs", "ar"):
         A = draw_matrix(cid, STREAM_A, rep, (M, K), dist, w.dtype)
         B = draw_matrix(cid, STREAM_B, rep, (N, K), dist, w.dtype)
         d = Drawn(A=A, B=B)
         S, Q = w.shard_rows, w.chunks_per_shard
         n_remote = (w.world - 1) * Q
+        if w.op == "ar":
+            # values spread like a partial product of A and B (and a sum of world of them)
+            part_scale = 0.02 * 0.02 * float(np.sqrt(K))
+            d.partials = draw_matrix(cid, STREAM_PARTIALS, rep, (w.world - 1, S, N), dist, w.out_dtype,
+                                     scale=part_scale)
+            d.reduced = draw_matrix(cid, STREAM_REDUCED, rep, (M, N), dist, w.out_dtype,
+                                    scale=part_scale * float(np.sqrt(w.world)))
         if w.op == "ag" and w.order == "permutation":
             d.perm = draw_permutation(cid, rep, n_remote)
         if w.delays:

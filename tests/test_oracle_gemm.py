@@ -154,3 +154,73 @@ def test_max_rel_error_metric():
     G = R.copy()
     G[1, 1] = 4.4
     assert oracle.max_rel_error(G, R) == pytest.approx(0.1)
+
+
+# ---------------------------------------------------------------------------------
+# GEMM + AllReduce (one rank's share)
+# ---------------------------------------------------------------------------------
+def _ar_case(W, r, S, Q, N, K, dist, dtype="f32", cfg=91):
+    """Per-rank K-slices A_s (M x K) and B_s (N x K) of a row-parallel product; rank r's
+    view: its own slices, the other ranks' partials of its shard (ascending rank order)
+    and the other shards' all-reduced rows."""
+    M = W * S
+    As = [_draw((M, K), dist, dtype, 0, rep=s, cfg=cfg).values for s in range(W)]      # float32 values
+    Bs = [_draw((N, K), dist, dtype, 1, rep=s, cfg=cfg).values for s in range(W)]
+    parts = [a.astype(np.float64) @ b.astype(np.float64).T for a, b in zip(As, Bs)]  # numpy fp64 matmul
+    full = sum(parts)
+    own = slice(r * S, (r + 1) * S)
+    partials = np.stack([parts[s][own] for s in range(W) if s != r])
+    chunks, order = oracle.uniform_schedule(W, r, S, Q, "rs_ring")
+    return As[r], Bs[r], partials, full, parts[r], chunks, order
+
+
+@pytest.mark.parametrize("W,r,S,Q", [(2, 0, 8, 1), (4, 1, 12, 3), (4, 3, 16, 2), (8, 5, 4, 2)])
+def test_ar_equals_the_unsplit_gemm_over_all_ranks_k(W, r, S, Q):
+    """An all-reduce of the ranks' K-slice products is the product over the whole K
+    (the row-parallel layer's identity): the oracle's reduced own rows, made from its
+    own partial plus the others' partials, equal numpy's product of the concatenated
+    slices; integer inputs make every sum exact."""
+    N, K = 10, 6
+    for dist in ("int", "normal"):
+        A, B, partials, full, mine, chunks, order = _ar_case(W, r, S, Q, N, K, dist)
+        C, out, log = oracle.gemm_ar(A, B, chunks, order, partials, full)
+        own = slice(r * S, (r + 1) * S)
+        if dist == "int":
+            assert np.array_equal(C[own], full[own])
+        else:
+            np.testing.assert_allclose(C[own], full[own], rtol=0, atol=1e-15 * W * K)
+        assert not np.isnan(C).any() and not np.isnan(out).any()
+        assert log == list(order)
+        for ch in chunks:
+            rows = slice(ch.row_begin, ch.row_end)
+            if ch.is_local:
+                assert np.array_equal(out[rows], C[rows])           # the reduced chunk is sent
+            else:
+                assert np.array_equal(C[rows], full[rows])          # arrived from its owner
+                np.testing.assert_allclose(out[rows], mine[rows], rtol=0, atol=1e-15 * K)   # own partial sent
+
+
+def test_ar_drops_no_peer():
+    """Leaving out any one peer's partial changes the reduced rows."""
+    W, r, S, Q, N, K = 4, 2, 8, 2, 6, 5
+    A, B, partials, full, mine, chunks, order = _ar_case(W, r, S, Q, N, K, "int")
+    C, _, _ = oracle.gemm_ar(A, B, chunks, order, partials, full)
+    own = slice(r * S, (r + 1) * S)
+    for j in range(W - 1):
+        p = partials.copy()
+        p[j] = 0
+        Cj, _, _ = oracle.gemm_ar(A, B, chunks, order, p, full)
+        assert not np.array_equal(Cj[own], C[own])
+
+
+def test_ar_order_invariance_and_row_subset():
+    W, r, S, Q, N, K = 4, 1, 16, 4, 12, 9
+    A, B, partials, full, mine, chunks, order = _ar_case(W, r, S, Q, N, K, "normal")
+    C, out, _ = oracle.gemm_ar(A, B, chunks, order, partials, full)
+    for rep in range(3):
+        perm = list(np.random.default_rng(rep).permutation(len(order)))
+        C2, out2, log2 = oracle.gemm_ar(A, B, chunks, perm, partials, full)
+        assert np.array_equal(C2, C) and np.array_equal(out2, out) and log2 == perm
+    rows = [0, 17, 20, 31, 63]
+    Cs, outs, _ = oracle.gemm_ar(A, B, chunks, order, partials, full, row_subset=rows)
+    assert np.array_equal(Cs[rows], C[rows]) and np.array_equal(outs[rows], out[rows])
