@@ -52,7 +52,8 @@ typedef enum { CSG_BF16 = 0, CSG_F32 = 1 } csg_dtype;
 typedef enum {
     CSG_AG_GEMM = 0,        /* AllGather(A) + GEMM: tiles consume arriving A row chunks */
     CSG_GEMM_RS = 1,        /* GEMM + ReduceScatter: tiles produce C row chunks that are sent */
-    CSG_GROUPED_GEMM = 2    /* all-to-all(X) + grouped GEMM: per-(source, expert) row segments */
+    CSG_GROUPED_GEMM = 2,   /* all-to-all(X) + grouped GEMM: per-(source, expert) row segments */
+    CSG_GEMM_AR = 3         /* GEMM + AllReduce (reduce-scatter then all-gather of C row chunks) */
 } csg_op;
 
 typedef enum {
@@ -298,6 +299,35 @@ csg_status csg_ag_gemm(csg_plan* p, void* a_landing, const void* a_staging, cons
  * c -> c_outgoing, after the work queued earlier on `compute`. */
 csg_status csg_gemm_rs(csg_plan* p, const void* a, const void* b_nk, void* c, void* c_outgoing,
                        csg_mode mode, void* compute_stream, void* copy_stream);
+
+/* GEMM + AllReduce on one rank (Evaluation, the GEMM-AR operator; Section 5.1, the
+ * partition-based AllReduce schedule), as a reduce-scatter then an all-gather of C row
+ * chunks. Every rank holds a K-slice of a row-parallel product; the result is the sum
+ * of all ranks' partial products a . b_nk^T. The plan's schedule is that of
+ * GEMM-RS (emission order, own shard last; every chunk the same height; the local
+ * chunks, contiguous, are the own shard of S rows, starting and ending on tile rows;
+ * M = world * S). The kernel computes this rank's partial in emission order:
+ *   - a non-local chunk's partial rows go to c; once emitted, the calling thread sends
+ *     them by SDMA (c -> c_outgoing) and then copies that chunk's all-reduced rows,
+ *     which its owner sends (reduced_staging, M x N, same row offsets), into the same
+ *     rows of c, on the same engine after the send;
+ *   - a tile of the own shard first waits for the other ranks' partial sums of its rows
+ *     (partials_staging -> partials_landing by SDMA, [world-1][S][N] in C's element
+ *     type, ranks in ascending order without this one, copied at the start of the
+ *     call), adds them to its fp32 accumulators in that order, and stores the reduced
+ *     rows; each reduced own chunk is then sent (c -> c_outgoing).
+ * When every copy is done, c holds the all-reduced M x N result and c_outgoing what
+ * this rank sent. The call returns once every copy has been issued; the copies
+ * complete on their own (the next call's kernel waits per chunk for the last copy of
+ * its rows; csg_plan_check waits for all). Compute-only: partials_landing must already
+ * hold the partials, nothing is copied (c's non-local rows keep the partial products).
+ * Copy-only: the copies alone, on what c holds (the previous kernel is waited for).
+ * CSG_ERR_UNSUPPORTED at plan creation for schedules not of that form, split tiles or
+ * the kernel copy backend. */
+csg_status csg_gemm_ar(csg_plan* p, const void* a, const void* b_nk, void* c, void* c_outgoing,
+                       const void* partials_staging, void* partials_landing,
+                       const void* reduced_staging, csg_mode mode, void* compute_stream,
+                       void* copy_stream);
 
 /* All-to-all + grouped GEMM on one rank: x_landing / x_staging as in csg_ag_gemm
  * (expert-major rows), b_enk the E x N x K expert weights; tile rows never cross

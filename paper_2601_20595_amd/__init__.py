@@ -26,7 +26,7 @@ CSG_OK, CSG_ERR_INVALID, CSG_ERR_UNSUPPORTED, CSG_ERR_HIP, CSG_ERR_NOMEM, CSG_ER
 # csg_dtype
 CSG_BF16, CSG_F32 = 0, 1
 # csg_op
-CSG_AG_GEMM, CSG_GEMM_RS, CSG_GROUPED_GEMM = 0, 1, 2
+CSG_AG_GEMM, CSG_GEMM_RS, CSG_GROUPED_GEMM, CSG_GEMM_AR = 0, 1, 2, 3
 # csg_order
 CSG_ORDER_RING, CSG_ORDER_SWIZZLE1D, CSG_ORDER_PERMUTATION, CSG_ORDER_RS_RING = 0, 1, 2, 3
 # csg_mode
@@ -38,7 +38,7 @@ ORDERS = {"ring": CSG_ORDER_RING, "swizzle1d": CSG_ORDER_SWIZZLE1D, "permutation
           "rs_ring": CSG_ORDER_RS_RING}
 MODES = {"overlap": CSG_MODE_OVERLAP, "compute_only": CSG_MODE_COMPUTE_ONLY, "copy_only": CSG_MODE_COPY_ONLY}
 DTYPES = {"bf16": CSG_BF16, "f32": CSG_F32}
-OPS = {"ag": CSG_AG_GEMM, "rs": CSG_GEMM_RS, "grouped": CSG_GROUPED_GEMM}
+OPS = {"ag": CSG_AG_GEMM, "rs": CSG_GEMM_RS, "grouped": CSG_GROUPED_GEMM, "ar": CSG_GEMM_AR}
 COPY_BACKENDS = {"sdma": CSG_COPY_SDMA, "kernel": CSG_COPY_KERNEL}
 
 # every symbol include/csg.h declares
@@ -47,7 +47,7 @@ ABI_FUNCTIONS = (
     "csg_schedule_create", "csg_schedule_uniform", "csg_schedule_grouped", "csg_schedule_info",
     "csg_schedule_get", "csg_schedule_destroy",
     "csg_plan_create", "csg_plan_info_get", "csg_plan_get_map", "csg_plan_set_copy_delays",
-    "csg_ag_gemm", "csg_gemm_rs", "csg_grouped_gemm", "csg_plan_check", "csg_plan_kernel_times",
+    "csg_ag_gemm", "csg_gemm_rs", "csg_gemm_ar", "csg_grouped_gemm", "csg_plan_check", "csg_plan_kernel_times",
     "csg_plan_trace", "csg_plan_destroy",
 )
 
@@ -124,6 +124,7 @@ def _lib():
         "csg_plan_set_copy_delays": ([vp, P(ctypes.c_float), i32], st),
         "csg_ag_gemm": ([vp, vp, vp, vp, vp, st, vp, vp], st),
         "csg_gemm_rs": ([vp, vp, vp, vp, vp, st, vp, vp], st),
+        "csg_gemm_ar": ([vp, vp, vp, vp, vp, vp, vp, vp, st, vp, vp], st),
         "csg_grouped_gemm": ([vp, vp, vp, vp, vp, st, vp, vp], st),
         "csg_plan_check": ([vp, P(csg_diag)], st),
         "csg_plan_kernel_times": ([vp, P(ctypes.c_float), i32, P(i32)], st),
@@ -310,6 +311,13 @@ def csg_gemm_rs(plan: int, a, b_nk, c, c_outgoing, mode="overlap", compute_strea
                               _stream(compute_stream), _stream(copy_stream)), "csg_gemm_rs")
 
 
+def csg_gemm_ar(plan: int, a, b_nk, c, c_outgoing, partials_staging, partials_landing, reduced_staging,
+                mode="overlap", compute_stream=None, copy_stream=None) -> None:
+    _check(_lib().csg_gemm_ar(plan, _ptr(a), _ptr(b_nk), _ptr(c), _ptr(c_outgoing), _ptr(partials_staging),
+                              _ptr(partials_landing), _ptr(reduced_staging), _mode(mode), _stream(compute_stream),
+                              _stream(copy_stream)), "csg_gemm_ar")
+
+
 def csg_grouped_gemm(plan: int, x_landing, x_staging, b_enk, c, mode="overlap", compute_stream=None,
                      copy_stream=None) -> None:
     _check(_lib().csg_grouped_gemm(plan, _ptr(x_landing), _ptr(x_staging), _ptr(b_enk), _ptr(c), _mode(mode),
@@ -413,6 +421,11 @@ class Plan:
 
     def gemm_rs(self, a, b_nk, c, c_outgoing, mode="overlap", compute_stream=None, copy_stream=None):
         csg_gemm_rs(self.handle, a, b_nk, c, c_outgoing, mode, compute_stream, copy_stream)
+
+    def gemm_ar(self, a, b_nk, c, c_outgoing, partials_staging, partials_landing, reduced_staging, mode="overlap",
+                compute_stream=None, copy_stream=None):
+        csg_gemm_ar(self.handle, a, b_nk, c, c_outgoing, partials_staging, partials_landing, reduced_staging, mode,
+                    compute_stream, copy_stream)
 
     def grouped_gemm(self, x_landing, x_staging, b_enk, c, mode="overlap", compute_stream=None, copy_stream=None):
         csg_grouped_gemm(self.handle, x_landing, x_staging, b_enk, c, mode, compute_stream, copy_stream)

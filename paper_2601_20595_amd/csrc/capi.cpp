@@ -136,6 +136,16 @@ struct csg_plan {
   // Completion signals of the chunk copies, per set (calls alternate sets), per remote
   // chunk position: consumers' copies in, the producer's copies out.
   std::vector<hsa_signal_t> sig_ready[2];
+  // GEMM + all-reduce, per set: sig_ready holds every chunk's last copy (emission
+  // order); sig_send the reduce-scatter send of a non-local chunk, which the copy-in of
+  // its reduced rows waits for; sig_part the landing of each other rank's partial sums
+  // of an own chunk ([peer * own chunks + q]), polled by the own-shard tiles
+  std::vector<hsa_signal_t> sig_send[2];
+  std::vector<hsa_signal_t> sig_part[2];
+  const int64_t** d_part_ready[2] = {nullptr, nullptr};
+  int64_t ar_own_row0 = 0, ar_own_rows = 0;  // the own shard
+  int32_t ar_chunk_rows = 0, ar_peers = 0, ar_own_shard = 0;
+  const void* ar_partials = nullptr;  // this call's partials landing buffer
   bool copies_in_flight = false;       // a call returned before its copies completed (consumers:
                                        // error paths only; producer: every call)
   int copies_set = 0;                  // signal set of those copies
@@ -164,7 +174,11 @@ struct csg_plan {
 
   int32_t n_chunks() const { return static_cast<int32_t>(sched.chunks.size()); }
   int32_t copy_workgroups() const { return cfg.copy_workgroups; }
-  bool consumer() const { return op != CSG_GEMM_RS; }
+  bool consumer() const { return op == CSG_AG_GEMM || op == CSG_GROUPED_GEMM; }
+  bool allreduce() const { return op == CSG_GEMM_AR; }
+  // chunks that get copies, in the order the copies are issued: consumers and GEMM-RS,
+  // the remote chunks; GEMM-AR, every chunk (own chunks are sent once reduced)
+  const std::vector<int32_t>& copied_chunks() const { return allreduce() ? sched.order : remote_order; }
   bool kernel_copies() const { return cfg.copy_backend == CSG_COPY_KERNEL; }
 };
 
@@ -173,12 +187,14 @@ namespace {
 void free_plan_device(csg_plan* p) {
   if (p->device < 0) return;
   DeviceGuard g(p->device);
-  for (auto& set : p->sig_ready)
-    for (hsa_signal_t sgn : set)
-      if (sgn.handle) (void)csg::sdma_wait(sgn, 0, 10000);  // a copy may still be in flight
-  for (auto& set : p->sig_ready)
-    for (hsa_signal_t sgn : set)
-      if (sgn.handle) hsa_signal_destroy(sgn);
+  for (auto* sets : {p->sig_ready, p->sig_send, p->sig_part})
+    for (int k = 0; k < 2; ++k)
+      for (hsa_signal_t sgn : sets[k])
+        if (sgn.handle) (void)csg::sdma_wait(sgn, 0, 10000);  // a copy may still be in flight
+  for (auto* sets : {p->sig_ready, p->sig_send, p->sig_part})
+    for (int k = 0; k < 2; ++k)
+      for (hsa_signal_t sgn : sets[k])
+        if (sgn.handle) hsa_signal_destroy(sgn);
   p->sdma.close();
   for (hipEvent_t e : p->ev_kernel_done)
     if (e) (void)hipEventSynchronize(e);
@@ -187,6 +203,7 @@ void free_plan_device(csg_plan* p) {
                     static_cast<void*>(p->d_list_begin), static_cast<void*>(p->d_ws),
                     static_cast<void*>(p->d_slot_count), static_cast<void*>(p->d_trace),
                     static_cast<void*>(p->d_ready[0]), static_cast<void*>(p->d_ready[1]),
+                    static_cast<void*>(p->d_part_ready[0]), static_cast<void*>(p->d_part_ready[1]),
                     static_cast<void*>(p->d_zero),
                     static_cast<void*>(p->d_counters), static_cast<void*>(p->d_ticket), static_cast<void*>(p->d_diag),
                     static_cast<void*>(p->d_scratch), static_cast<void*>(p->d_copy_items),
@@ -371,18 +388,31 @@ csg_status setup_device(csg_plan* p) {
   CSG_HIP(hipDeviceSynchronize());
   std::string err = p->sdma.open(p->device, p->cfg.copy_engines, p->d_scratch, p->d_scratch + 8);
   if (!err.empty()) return fail(CSG_ERR_HIP, "copy engines: %s", err.c_str());
-  const size_t n_remote = p->remote_order.size();
-  for (int set = 0; set < 2; ++set) {
-    p->sig_ready[set].assign(n_remote, hsa_signal_t{0});
-    std::vector<const int64_t*> ptrs(p->n_chunks(), p->d_zero);  // local chunks: never copied
-    for (size_t i = 0; i < n_remote; ++i) {
-      hsa_status_t hs = p->sdma.make_signal(0, &p->sig_ready[set][i]);
+  const std::vector<int32_t>& copied = p->copied_chunks();
+  const size_t n_copied = copied.size();
+  auto make_set = [&](std::vector<hsa_signal_t>& sigs, size_t n, std::vector<const int64_t*>* ptrs,
+                      const std::vector<int32_t>* slot) -> csg_status {
+    sigs.assign(n, hsa_signal_t{0});
+    for (size_t i = 0; i < n; ++i) {
+      hsa_status_t hs = p->sdma.make_signal(0, &sigs[i]);
       const int64_t* vp = nullptr;
-      if (hs == HSA_STATUS_SUCCESS) hs = p->sdma.signal_value_ptr(p->sig_ready[set][i], &vp);
+      if (hs == HSA_STATUS_SUCCESS) hs = p->sdma.signal_value_ptr(sigs[i], &vp);
       if (hs != HSA_STATUS_SUCCESS) return fail(CSG_ERR_NOMEM, "copy signal: %s", csg::hsa_error(hs).c_str());
-      ptrs[p->remote_order[i]] = vp;
+      if (ptrs) (*ptrs)[slot ? (*slot)[i] : static_cast<int32_t>(i)] = vp;
     }
+    return CSG_OK;
+  };
+  for (int set = 0; set < 2; ++set) {
+    std::vector<const int64_t*> ptrs(p->n_chunks(), p->d_zero);  // chunks never copied: ready
+    if ((st = make_set(p->sig_ready[set], n_copied, &ptrs, &copied)) != CSG_OK) return st;
     if ((st = upload(&p->d_ready[set], ptrs)) != CSG_OK) return st;
+    if (p->allreduce()) {
+      if ((st = make_set(p->sig_send[set], n_copied, nullptr, nullptr)) != CSG_OK) return st;
+      const size_t n_part = static_cast<size_t>(p->ar_peers) * (p->ar_own_rows / p->ar_chunk_rows);
+      std::vector<const int64_t*> pp(std::max<size_t>(n_part, 1), p->d_zero);
+      if ((st = make_set(p->sig_part[set], n_part, &pp, nullptr)) != CSG_OK) return st;
+      if ((st = upload(&p->d_part_ready[set], pp)) != CSG_OK) return st;
+    }
   }
   CSG_HIP(hipEventCreateWithFlags(&p->ev_copy_in, hipEventDisableTiming));
   CSG_HIP(hipEventCreateWithFlags(&p->ev_prologue, hipEventDisableTiming));
@@ -433,10 +463,11 @@ std::vector<hsa_signal_t>& call_signals(csg_plan* p) { return p->sig_ready[p->ep
 csg_status drain_copies(csg_plan* p, bool all) {
   if (!p->copies_in_flight || (!all && !p->consumer())) return CSG_OK;
   const int budget = p->cfg.timeout_ms * 4;
-  for (int set = 0; set < 2; ++set)
-    for (hsa_signal_t sgn : p->sig_ready[set])
-      if (csg::sdma_wait(sgn, 0, budget) > 0)
-        return fail(CSG_ERR_TIMEOUT, "copies of an earlier call did not complete");
+  for (auto* sets : {p->sig_ready, p->sig_send, p->sig_part})
+    for (int set = 0; set < 2; ++set)
+      for (hsa_signal_t sgn : sets[set])
+        if (csg::sdma_wait(sgn, 0, budget) > 0)
+          return fail(CSG_ERR_TIMEOUT, "copies of an earlier call did not complete");
   p->copies_in_flight = false;
   return CSG_OK;
 }
@@ -461,14 +492,25 @@ csg_status begin_call(csg_plan* p, csg_mode mode, CallState* cs) {
   }
   ++p->epoch;
   p->host_diag = csg_diag{0, -1, -1, 0, p->epoch, 0};
-  if (p->consumer() && !p->remote_order.empty() && !p->kernel_copies()) {
+  // the signals this call's kernel polls: consumers', the copies in of their chunks;
+  // GEMM + all-reduce, the landing of the other ranks' partial sums
+  const int set = p->epoch & 1;
+  std::vector<hsa_signal_t>* polled = nullptr;
+  if (p->consumer() && !p->remote_order.empty() && !p->kernel_copies()) polled = &p->sig_ready[set];
+  if (p->allreduce() && !p->sig_part[set].empty()) polled = &p->sig_part[set];
+  if (polled) {
     // this call's signal set was last polled by the kernel two calls back, which must
     // be done before the set is armed again (it normally ended long ago)
-    const int set = p->epoch & 1;
     if (p->kernel_pending[set] && (st = host_wait(p, p->ev_kernel_done[set], "the kernel two calls back")) != CSG_OK)
       return st;
+    // the partials' copies complete after their call returns (a copy-only call has no
+    // kernel that waited for them): each must be done before its signal is armed again
+    if (p->allreduce())
+      for (hsa_signal_t sgn : *polled)
+        if (csg::sdma_wait(sgn, 0, p->cfg.timeout_ms * 4) != 0)
+          return fail(CSG_ERR_TIMEOUT, "an earlier copy of a partial sum did not complete");
     const hsa_signal_value_t v = mode == CSG_MODE_COMPUTE_ONLY ? 0 : 1;  // compute-only: every chunk ready
-    for (hsa_signal_t sgn : p->sig_ready[set]) hsa_signal_store_relaxed(sgn, v);
+    for (hsa_signal_t sgn : *polled) hsa_signal_store_relaxed(sgn, v);
     std::atomic_thread_fence(std::memory_order_seq_cst);  // armed before the kernel launch below
   }
   p->kernel_pending[p->epoch & 1] = false;
@@ -604,6 +646,15 @@ csg_status launch_gemm(csg_plan* p, const void* A, const void* B, void* C, csg_m
       a.C2 = kc->c2;
       a.chunk_sent = p->d_chunk_sent;
     }
+  }
+  if (p->allreduce()) {
+    a.partials = static_cast<const unsigned char*>(p->ar_partials);
+    a.partial_ready = p->d_part_ready[p->epoch & 1];
+    a.own_row0 = p->ar_own_row0;
+    a.own_rows = p->ar_own_rows;
+    a.n_peers = p->ar_peers;
+    a.own_chunk_rows = p->ar_chunk_rows;
+    a.own_shard = p->ar_own_shard;
   }
   p->expected_units = static_cast<uint32_t>(a.n_tiles);
   const int slot = static_cast<int>(p->n_launches % kTimingRing);
@@ -861,7 +912,7 @@ csg_status csg_plan_create(csg_op op, int64_t M, int64_t N, int64_t K, csg_dtype
   if (!out) return fail(CSG_ERR_INVALID, "out is NULL");
   *out = nullptr;
   if (!s) return fail(CSG_ERR_INVALID, "schedule is NULL");
-  if (op < CSG_AG_GEMM || op > CSG_GROUPED_GEMM) return fail(CSG_ERR_INVALID, "unknown op");
+  if (op < CSG_AG_GEMM || op > CSG_GEMM_AR) return fail(CSG_ERR_INVALID, "unknown op");
   if ((in_dtype != CSG_BF16 && in_dtype != CSG_F32) || (out_dtype != CSG_BF16 && out_dtype != CSG_F32))
     return fail(CSG_ERR_INVALID, "unknown dtype");
   if (M < 1 || N < 1 || K < 1 || M > 0x7fffffff || N > 0x7fffffff || K > (1 << 22))
@@ -905,13 +956,46 @@ csg_status csg_plan_create(csg_op op, int64_t M, int64_t N, int64_t K, csg_dtype
   p->sched = s->s;
   p->group_rows = groups;
   p->cfg = c;
-  std::string err = csg::build_tile_map(p->sched, M, N, c.bm, c.bn, op == CSG_GEMM_RS, groups, &p->map);
+  std::string err = csg::build_tile_map(p->sched, M, N, c.bm, c.bn, !p->consumer(), groups, &p->map);
   if (!err.empty()) {
     delete p;
     return fail(CSG_ERR_INVALID, "%s", err.c_str());
   }
   for (int32_t c_id : p->sched.order)
     if (!p->sched.chunks[c_id].is_local) p->remote_order.push_back(c_id);
+  if (op == CSG_GEMM_AR) {
+    // the own shard: the local chunks, contiguous; every chunk the same height; tiles
+    // never straddle the own shard's edges; no split tiles; copies by the engines
+    const std::vector<csg::ChunkDesc>& ch = p->sched.chunks;
+    const int64_t h = ch[0].row_end - ch[0].row_begin;
+    int64_t own0 = -1, own1 = -1;
+    std::string why;
+    for (const csg::ChunkDesc& x : ch) {
+      if (x.row_end - x.row_begin != h) why = "every chunk must have the same number of rows";
+      if (x.is_local) {
+        if (own0 < 0) own0 = x.row_begin;
+        else if (x.row_begin != own1) why = "the local chunks must be contiguous (the own shard)";
+        own1 = x.row_end;
+      }
+    }
+    if (why.empty() && own0 < 0) why = "a GEMM + all-reduce plan needs local chunks (the own shard)";
+    const int64_t S = own1 - own0;
+    if (why.empty() && M % S != 0) why = "M must be a multiple of the own shard's rows";
+    if (why.empty() && (own0 % c.bm != 0 || (own1 % c.bm != 0 && own1 != M)))
+      why = "the own shard must start and end on a tile-row boundary (bm)";
+    if (why.empty() && (c.split_k > 1 || (c.tail_split > 1 && c.tail_chunks > 0)))
+      why = "GEMM + all-reduce splits no tile";
+    if (why.empty() && c.copy_backend != CSG_COPY_SDMA) why = "GEMM + all-reduce copies with the SDMA engines";
+    if (!why.empty()) {
+      delete p;
+      return fail(CSG_ERR_UNSUPPORTED, "%s", why.c_str());
+    }
+    p->ar_own_row0 = own0;
+    p->ar_own_rows = S;
+    p->ar_chunk_rows = static_cast<int32_t>(h);
+    p->ar_peers = static_cast<int32_t>(M / S - 1);
+    p->ar_own_shard = static_cast<int32_t>(own0 / S);
+  }
   if (op == CSG_GEMM_RS && c.copy_backend == CSG_COPY_KERNEL)
     for (const csg::ChunkDesc& ch : p->sched.chunks)
       if (ch.row_begin % c.bm != 0) {
@@ -922,8 +1006,8 @@ csg_status csg_plan_create(csg_op op, int64_t M, int64_t N, int64_t K, csg_dtype
       }
 
   if (device >= 0) {
-    p->key = csg::KernelKey{bf16 ? csg::InType::BF16 : csg::InType::F32, out_dtype == CSG_BF16, op == CSG_GEMM_RS,
-                            c.bm, c.bn, c.bk};
+    p->key = csg::KernelKey{bf16 ? csg::InType::BF16 : csg::InType::F32, out_dtype == CSG_BF16, !p->consumer(),
+                            c.bm, c.bn, c.bk, p->allreduce()};
     if (!csg::kernel_supported(p->key)) {
       delete p;
       return fail(CSG_ERR_UNSUPPORTED, "no kernel for dtype %d->%d tile %dx%dx%d", in_dtype, out_dtype, c.bm, c.bn,
@@ -1108,6 +1192,104 @@ csg_status csg_gemm_rs(csg_plan* p, const void* a, const void* b_nk, void* c, vo
   }
   // the copies complete on their own: the next call's kernel waits for each before
   // rewriting the chunk, and csg_plan_check (or destroy) waits for all of them
+  return CSG_OK;
+}
+
+csg_status csg_gemm_ar(csg_plan* p, const void* a, const void* b_nk, void* c, void* c_outgoing,
+                       const void* partials_staging, void* partials_landing, const void* reduced_staging,
+                       csg_mode mode, void* compute_stream, void* copy_stream) {
+  if (!p) return fail(CSG_ERR_INVALID, "plan is NULL");
+  if (p->op != CSG_GEMM_AR) return fail(CSG_ERR_INVALID, "plan is not a GEMM + all-reduce plan");
+  if (p->device < 0) return fail(CSG_ERR_STATE, "host-only plan (created with device < 0) cannot run");
+  const bool copies = mode != CSG_MODE_COMPUTE_ONLY;
+  if (!a || !b_nk || !c || !partials_landing ||
+      (copies && (!c_outgoing || !partials_staging || (!reduced_staging && !p->remote_order.empty()))))
+    return fail(CSG_ERR_INVALID, "NULL buffer");
+  if (!aligned16(a) || !aligned16(b_nk) || !aligned16(c) || !aligned16(c_outgoing) || !aligned16(partials_staging) ||
+      !aligned16(partials_landing) || !aligned16(reduced_staging))
+    return fail(CSG_ERR_INVALID, "buffers must be 16-byte aligned");
+  hipStream_t compute = static_cast<hipStream_t>(compute_stream), copy = static_cast<hipStream_t>(copy_stream);
+  DeviceGuard g(p->device);
+  if (g.err != hipSuccess) return hip_fail(g.err, "hipSetDevice");
+  CallState cs;
+  csg_status st = begin_call(p, mode, &cs);
+  if (st != CSG_OK) return st;
+  p->ar_partials = partials_landing;
+  if ((st = launch_prologue_call(p, mode, compute)) != CSG_OK) return st;
+  if (mode != CSG_MODE_COPY_ONLY && (st = launch_gemm(p, a, b_nk, c, mode, compute)) != CSG_OK) return st;
+  if (!copies) return CSG_OK;
+  // the partials land where the previous call's kernel read them, and copy-only sends
+  // what a finished kernel wrote: wait for the previous kernel
+  if ((st = ready_copies(p, copy, cs, true)) != CSG_OK) return st;
+  const int set = p->epoch & 1;
+  const int64_t row_bytes = p->N * out_bytes(p);
+  const int64_t chunk_bytes = p->ar_chunk_rows * row_bytes;
+  const int nq = static_cast<int>(p->ar_own_rows / p->ar_chunk_rows);
+  int eng = 0;
+  // 1. the other ranks' partial sums of the own shard land, own chunk by own chunk
+  const std::vector<hsa_signal_t>& part = p->sig_part[set];
+  for (int q = 0; q < nq; ++q)
+    for (int j = 0; j < p->ar_peers; ++j) {
+      const int64_t off = (static_cast<int64_t>(j) * p->ar_own_rows + static_cast<int64_t>(q) * p->ar_chunk_rows) *
+                          row_bytes;
+      const hsa_status_t hs =
+          p->sdma.copy(static_cast<char*>(partials_landing) + off, static_cast<const char*>(partials_staging) + off,
+                       static_cast<size_t>(chunk_bytes), eng++, nullptr, part[static_cast<size_t>(j * nq + q)]);
+      // a partial not copied keeps its signal armed: the tiles' bounded waits for it
+      // expire and csg_plan_check reports it
+      if (hs != HSA_STATUS_SUCCESS) return fail(CSG_ERR_HIP, "SDMA copy of a partial: %s", csg::hsa_error(hs).c_str());
+    }
+  // 2. in emission order: a non-local chunk is sent (reduce-scatter), then its reduced
+  //    rows arrive from their owner into the same rows of c (all-gather), on the same
+  //    engine, once the send has read them; an own chunk, reduced by its tiles, is sent
+  const std::vector<int32_t>& order = p->sched.order;
+  const std::vector<hsa_signal_t>& last = p->sig_ready[set];
+  const std::vector<hsa_signal_t>& send = p->sig_send[set];
+  const auto budget = std::chrono::milliseconds(p->cfg.timeout_ms) * 4;
+  const Clock::time_point t0 = Clock::now();
+  for (size_t i = 0; i < order.size(); ++i) {
+    const int32_t cid = order[i];
+    if (mode == CSG_MODE_OVERLAP) {
+      const volatile uint32_t* f = p->h_out_flags + cid;
+      while (*f < p->epoch) {
+        if (Clock::now() - t0 > budget) {
+          p->host_diag = csg_diag{1, cid, -1, *f, p->epoch, 0};
+          return fail(CSG_ERR_TIMEOUT, "output chunk %d was not completed in time", cid);
+        }
+      }
+    }
+    // this set's signals were last used two calls back (the previous kernel waited for
+    // them before rewriting the chunk's rows)
+    if (csg::sdma_wait(last[i], 0, p->cfg.timeout_ms * 4) != 0 || csg::sdma_wait(send[i], 0, p->cfg.timeout_ms * 4) != 0) {
+      p->host_diag = csg_diag{1, cid, -1, 1, p->epoch, 0};
+      return fail(CSG_ERR_TIMEOUT, "an earlier copy of chunk %d did not complete", cid);
+    }
+    const csg::ChunkDesc& ch = p->sched.chunks[cid];
+    const int64_t off = ch.row_begin * row_bytes;
+    const size_t bytes = static_cast<size_t>((ch.row_end - ch.row_begin) * row_bytes);
+    const int e = eng++;
+    hsa_signal_store_relaxed(last[i], 1);
+    hsa_status_t hs;
+    if (ch.is_local) {
+      hs = p->sdma.copy(static_cast<char*>(c_outgoing) + off, static_cast<const char*>(c) + off, bytes, e, nullptr,
+                        last[i]);
+    } else {
+      hsa_signal_store_relaxed(send[i], 1);
+      hs = p->sdma.copy(static_cast<char*>(c_outgoing) + off, static_cast<const char*>(c) + off, bytes, e, nullptr,
+                        send[i]);
+      if (hs == HSA_STATUS_SUCCESS)
+        hs = p->sdma.copy(static_cast<char*>(c) + off, static_cast<const char*>(reduced_staging) + off, bytes, e,
+                          &send[i], last[i]);
+      else
+        hsa_signal_store_relaxed(send[i], 0);
+    }
+    if (hs != HSA_STATUS_SUCCESS) {
+      hsa_signal_store_relaxed(last[i], 0);
+      return fail(CSG_ERR_HIP, "SDMA copy: %s", csg::hsa_error(hs).c_str());
+    }
+  }
+  // the copies complete on their own: the next call's kernel waits for each chunk's
+  // last copy before rewriting its rows, and csg_plan_check waits for all of them
   return CSG_OK;
 }
 

@@ -103,6 +103,37 @@ __device__ int wait_chunks(const GemmArgs& a, int pos, uint32_t* ready_bits) {
   return fresh;
 }
 
+// GEMM + all-reduce (thread 0 only): waits until the other ranks' partial sums of the
+// own-shard tile's rows have landed (each partial chunk's copy brings its value to
+// 0). 0 when they have, -1 if the wait gave up.
+__device__ int wait_partials(const GemmArgs& a, const TileDesc& td, int pos) {
+  const int nq = static_cast<int>(a.own_rows / a.own_chunk_rows);
+  const int q0 = static_cast<int>((td.row_begin - a.own_row0) / a.own_chunk_rows);
+  const int q1 = static_cast<int>((td.row_end - 1 - a.own_row0) / a.own_chunk_rows);
+  for (int j = 0; j < a.n_peers; ++j)
+    for (int q = q0; q <= q1; ++q) {
+      const int64_t* rp = a.partial_ready[j * nq + q];
+      const uint64_t t0 = wall_clock64();
+      int64_t v = load_ready(rp);
+      while (v != 0) {
+        if (load_flag(&a.diag->abort)) return -1;
+        if (wall_clock64() - t0 > a.timeout_ticks) {
+          if (atomicCAS(&a.diag->timed_out, 0u, 1u) == 0u) {
+            a.diag->chunk = a.own_shard * nq + q;
+            a.diag->tile = a.raster[pos];
+            a.diag->observed = static_cast<uint32_t>(v);
+            a.diag->epoch = a.epoch;
+          }
+          __hip_atomic_store(&a.diag->abort, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+          return -1;
+        }
+        __builtin_amdgcn_s_sleep(32);
+        v = load_ready(rp);
+      }
+    }
+  return 0;
+}
+
 // Next execution position for a workgroup on die `xcd` (thread 0 only): the next
 // entry of that die's sub-list, else (when stealing is on) of the following dies'
 // sub-lists; n_tiles when no list it may take from has entries left.
@@ -580,7 +611,7 @@ __device__ void send_tile(const __amdgpu_buffer_rsrc_t& rsC, unsigned char* dst,
 // ---------------------------------------------------------------------------------
 // The persistent kernel
 // ---------------------------------------------------------------------------------
-template <class Loop, bool kOutBf16, bool kProducer>
+template <class Loop, bool kOutBf16, bool kProducer, bool kReduce = false>
 __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
   constexpr int kThreads = Loop::THREADS;
   constexpr int BN = Loop::BN;
@@ -737,6 +768,48 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
       const int i = r / (NI * 4), j = (r / 4) % NI, q = r % 4;
       return f32x4{acc[i][j][4 * q + 0], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
     };
+
+    if constexpr (kReduce) {
+      // GEMM + all-reduce: a tile of the own shard adds the other ranks' partial sums of
+      // its rows (in ascending rank order, in fp32) before its output is stored, so the
+      // stored rows are the reduced ones (the reduce-scatter's reduction, fused into the
+      // epilogue). Plans with the reduction split no tile and keep tiles inside shards.
+      if (td.row_begin >= a.own_row0 && td.row_begin < a.own_row0 + a.own_rows) {
+        __syncthreads();
+        if (tid == 0) s_state = wait_partials(a, td, pos);
+        __syncthreads();
+        if (s_state < 0) break;
+        const int64_t prow = td.row_begin - a.own_row0;
+        for (int j = 0; j < a.n_peers; ++j) {
+          const __amdgpu_buffer_rsrc_t rsP =
+              make_rsrc(a.partials + ((static_cast<int64_t>(j) * a.own_rows + prow) * a.N + col0) * kOutBytes,
+                        static_cast<int64_t>(g.arows) * a.N * kOutBytes);
+#pragma unroll
+          for (int r = 0; r < kRuns; ++r) {
+            const int i = r / (NI * 4), jj = (r / 4) % NI, q = r % 4;
+            const bool ok = (vrow + 32 * i < g.arows) && (vcol + 32 * jj + 8 * q < g.brows);
+            const int voff = (ok ? voff_c : kDropOffset) + (32 * jj + 8 * q) * kOutBytes;
+            const int soff = __builtin_amdgcn_readfirstlane(32 * i * N32 * kOutBytes);
+            float f[4];
+            if constexpr (kOutBf16) {
+              const u32x2 raw = __builtin_amdgcn_raw_buffer_load_b64(rsP, voff, soff, 0);
+              f[0] = __builtin_bit_cast(float, raw.x << 16);
+              f[1] = __builtin_bit_cast(float, raw.x & 0xffff0000u);
+              f[2] = __builtin_bit_cast(float, raw.y << 16);
+              f[3] = __builtin_bit_cast(float, raw.y & 0xffff0000u);
+            } else {
+              const f32x4 v = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rsP, voff, soff, 0));
+              f[0] = v[0];
+              f[1] = v[1];
+              f[2] = v[2];
+              f[3] = v[3];
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc[i][jj][4 * q + e] += f[e];
+          }
+        }
+      }
+    }
 
     const int nslices = td.slice >> 16;
     if (nslices == 2) {
@@ -903,17 +976,17 @@ using LoopF32_64 = F32Loop<64, 64>;
 
 // The timing events (either may be null) take the dispatch's own start and end
 // timestamps, not those of separate markers queued around it.
-template <class Loop, bool kOutBf16, bool kProducer>
+template <class Loop, bool kOutBf16, bool kProducer, bool kReduce>
 static hipError_t launch_one(const GemmArgs& args, int32_t grid, hipStream_t stream, hipEvent_t start,
                              hipEvent_t stop) {
-  hipExtLaunchKernelGGL((chunk_gemm<Loop, kOutBf16, kProducer>), dim3(grid), dim3(Loop::THREADS), 0, stream, start,
-                        stop, 0, args);
+  hipExtLaunchKernelGGL((chunk_gemm<Loop, kOutBf16, kProducer, kReduce>), dim3(grid), dim3(Loop::THREADS), 0, stream,
+                        start, stop, 0, args);
   return hipGetLastError();
 }
 
-template <class Loop, bool kOutBf16, bool kProducer>
+template <class Loop, bool kOutBf16, bool kProducer, bool kReduce>
 static const void* kernel_ptr() {
-  return reinterpret_cast<const void*>(&chunk_gemm<Loop, kOutBf16, kProducer>);
+  return reinterpret_cast<const void*>(&chunk_gemm<Loop, kOutBf16, kProducer, kReduce>);
 }
 
 namespace {
@@ -921,25 +994,32 @@ struct Variant {
   InType in;
   bool out_bf16;
   bool producer;
+  bool reduce;
   int bm, bn, bk;
   int threads;
   hipError_t (*launch)(const GemmArgs&, int32_t, hipStream_t, hipEvent_t, hipEvent_t);
   const void* (*func)();
 };
 
-#define CSG_VARIANT(IN, LOOP, OB, PR) \
-  Variant { IN, OB, PR, LOOP::BM, LOOP::BN, LOOP::BK, LOOP::THREADS, &launch_one<LOOP, OB, PR>, &kernel_ptr<LOOP, OB, PR> }
+#define CSG_VARIANT(IN, LOOP, OB, PR, RD)                                                                    \
+  Variant {                                                                                                   \
+    IN, OB, PR, RD, LOOP::BM, LOOP::BN, LOOP::BK, LOOP::THREADS, &launch_one<LOOP, OB, PR, RD>,               \
+        &kernel_ptr<LOOP, OB, PR, RD>                                                                         \
+  }
 
 const Variant kVariants[] = {
-    CSG_VARIANT(InType::BF16, LoopBf16_256, true, false),  CSG_VARIANT(InType::BF16, LoopBf16_256, true, true),
-    CSG_VARIANT(InType::BF16, LoopBf16_256, false, false), CSG_VARIANT(InType::BF16, LoopBf16_256, false, true),
-    CSG_VARIANT(InType::F32, LoopF32_64, false, false),    CSG_VARIANT(InType::F32, LoopF32_64, false, true),
+    CSG_VARIANT(InType::BF16, LoopBf16_256, true, false, false),  CSG_VARIANT(InType::BF16, LoopBf16_256, true, true, false),
+    CSG_VARIANT(InType::BF16, LoopBf16_256, false, false, false), CSG_VARIANT(InType::BF16, LoopBf16_256, false, true, false),
+    CSG_VARIANT(InType::F32, LoopF32_64, false, false, false),    CSG_VARIANT(InType::F32, LoopF32_64, false, true, false),
+    // GEMM + all-reduce: producers with the fused reduction
+    CSG_VARIANT(InType::BF16, LoopBf16_256, true, true, true),    CSG_VARIANT(InType::BF16, LoopBf16_256, false, true, true),
+    CSG_VARIANT(InType::F32, LoopF32_64, false, true, true),
 };
 
 const Variant* find_variant(const KernelKey& k) {
   for (const Variant& v : kVariants)
-    if (v.in == k.in && v.out_bf16 == k.out_bf16 && v.producer == k.producer && v.bm == k.bm && v.bn == k.bn &&
-        v.bk == k.bk)
+    if (v.in == k.in && v.out_bf16 == k.out_bf16 && v.producer == k.producer && v.reduce == k.reduce &&
+        v.bm == k.bm && v.bn == k.bn && v.bk == k.bk)
       return &v;
   return nullptr;
 }

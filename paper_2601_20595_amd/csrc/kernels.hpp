@@ -110,6 +110,16 @@ struct GemmArgs {
   // as C) by the tile epilogue; null when the copy engines send them.
   void* C2;
   const int32_t* chunk_sent;     // per chunk: 1 if it is sent (producer with C2)
+  // GEMM + all-reduce (producer kernels built with the reduction): a tile of the own
+  // shard adds the other ranks' partial sums of its rows to its accumulators before
+  // storing, once they have landed.
+  const unsigned char* partials;        // [n_peers][own_rows][N], C's element type
+  const int64_t* const* partial_ready;  // [n_peers * (own_rows / own_chunk_rows)]: 0 once landed
+  int64_t own_row0;                     // first row of the own shard
+  int64_t own_rows;
+  int32_t n_peers;
+  int32_t own_chunk_rows;
+  int32_t own_shard;                    // shard index of the own shard (diagnostics)
 };
 
 // Everything the per-call prologue resets.
@@ -142,6 +152,7 @@ struct KernelKey {
   bool out_bf16;
   bool producer;
   int32_t bm, bn, bk;
+  bool reduce = false;  // producer with the all-reduce's fused reduction
 };
 
 // Kernel variants compiled into this library; false if `key` has none.

@@ -184,3 +184,30 @@ def test_host_only_plan_cannot_run_and_delays_are_checked():
     assert p.info.num_workgroups == 0
     assert _status(p.kernel_times, 4) == csg.CSG_ERR_STATE               # nothing ever ran
     assert _status(p.kernel_times, -1) == csg.CSG_ERR_INVALID
+
+
+def test_allreduce_plans_map_like_reduce_scatter_and_validate():
+    s = csg.Schedule.uniform(4, 1, 256, 2, "rs_ring")
+    ar = csg.Plan("ar", 1024, 320, 64, "bf16", "bf16", s, device=-1)
+    rs = csg.Plan("rs", 1024, 320, 64, "bf16", "bf16", s, device=-1)
+    m_ar, m_rs = ar.get_map(), rs.get_map()
+    for k in m_rs:
+        assert np.array_equal(np.asarray(m_ar[k]), np.asarray(m_rs[k])), k
+    assert _status(csg.Plan, "ar", 1024, 320, 64, "bf16", "bf16", s, cfg={"split_k": 2}, device=-1) \
+        == csg.CSG_ERR_UNSUPPORTED
+    assert _status(csg.Plan, "ar", 1024, 320, 64, "bf16", "bf16", s, cfg={"copy_backend": "kernel"}, device=-1) \
+        == csg.CSG_ERR_UNSUPPORTED
+    # own shard rows 100..199 do not start on a 256-row tile (fp32 tiles are 64 rows: also not)
+    s100 = csg.Schedule.uniform(4, 1, 100, 2, "rs_ring")
+    assert _status(csg.Plan, "ar", 400, 64, 64, "bf16", "bf16", s100, device=-1) == csg.CSG_ERR_UNSUPPORTED
+    assert _status(csg.Plan, "ar", 400, 64, 64, "f32", "f32", s100, device=-1) == csg.CSG_ERR_UNSUPPORTED
+    s128 = csg.Schedule.uniform(4, 1, 128, 2, "rs_ring")
+    assert _status(csg.Plan, "ar", 512, 64, 64, "f32", "f32", s128, device=-1) == csg.CSG_OK
+    # unequal chunks; local chunks that are not contiguous
+    uneq = csg.Schedule.create([(0, 64, 0, 0, 1), (64, 192, 1, 0, 0)], [1, 0])
+    assert _status(csg.Plan, "ar", 192, 64, 64, "f32", "f32", uneq, device=-1) == csg.CSG_ERR_UNSUPPORTED
+    split = csg.Schedule.create([(0, 64, 0, 0, 1), (64, 128, 1, 0, 0), (128, 192, 0, 0, 1), (192, 256, 1, 0, 0)],
+                                [1, 3, 0, 2])
+    assert _status(csg.Plan, "ar", 256, 64, 64, "f32", "f32", split, device=-1) == csg.CSG_ERR_UNSUPPORTED
+    assert _status(ar.gemm_ar, 16, 16, 16, 16, 16, 16, 16) == csg.CSG_ERR_STATE        # host-only plan
+    assert _status(rs.gemm_ar, 16, 16, 16, 16, 16, 16, 16) == csg.CSG_ERR_INVALID      # wrong op
