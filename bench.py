@@ -91,7 +91,18 @@ def main():
     c = torch.empty((w.M, w.N), dtype=out_t, device=dev)
     in_bytes = 2 if w.dtype == "bf16" else 4
     out_bytes = 2 if w.out_dtype == "bf16" else 4
-    if w.op == "rs":
+    p_stage = p_land = reduced = None
+    if w.op == "ar":
+        # reduce-scatter sends and all-gather arrivals of the non-local chunks, the other
+        # ranks' partials of the own shard, and the sends of the reduced own chunks
+        landing = None
+        outgoing = torch.zeros((w.M, w.N), dtype=out_t, device=dev)
+        p_stage = to_dev(d.partials.device_array)
+        p_land = p_stage.clone()
+        reduced = to_dev(d.reduced.device_array)
+        own_rows = w.M - remote_rows
+        moved_bytes = (2 * remote_rows + (w.world - 1) * own_rows + own_rows) * w.N * out_bytes
+    elif w.op == "rs":
         landing = None
         outgoing = torch.zeros((w.M, w.N), dtype=out_t, device=dev)
         moved_bytes = remote_rows * w.N * out_bytes
@@ -111,7 +122,9 @@ def main():
 
     def call(mode, p=None):
         p = p or plan
-        if w.op == "rs":
+        if w.op == "ar":
+            p.gemm_ar(a_full, b, c, outgoing, p_stage, p_land, reduced, mode, compute, copy)
+        elif w.op == "rs":
             p.gemm_rs(a_full, b, c, outgoing, mode, compute, copy)
         elif w.op == "grouped":
             p.grouped_gemm(landing, a_full, b, c, mode, compute, copy)
@@ -215,7 +228,7 @@ def main():
                                   "frac": round(w.flops / (k_comp * 1e-3) / 1e12 / peak, 4),
                                   "kernel_ms_mean": round(k_comp, 4)},
     }
-    if not args.no_kernel_copies:
+    if not args.no_kernel_copies and w.op != "ar":  # GEMM + all-reduce copies with the engines only
         rec["kernel_copy_backend"] = kernel_copy_sweep(w, sched, group_rows, d, timed_loop, moved_bytes, args)
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(w, d, chunks, args.cpu_seconds)
