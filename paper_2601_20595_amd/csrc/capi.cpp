@@ -114,7 +114,7 @@ struct csg_plan {
   int32_t* d_need = nullptr;
   int32_t* d_list_begin = nullptr;     // [kXcdLists + 1] per-die sub-list bounds (in units)
   float* d_ws = nullptr;               // split-K partial sums
-  uint32_t* d_slot_count = nullptr;    // split-K finished slices per tile
+  uint32_t* d_slot_count = nullptr;    // split-K finished slices per tile, [2][n_tiles]
   int32_t ws_slices = 0;               // partial-sum buffers of split tiles (0: nothing is split)
   uint64_t* d_trace = nullptr;         // per-unit trace words (cfg.trace)
   std::vector<csg::TileDesc> units;    // host copy of the execution list
@@ -123,9 +123,11 @@ struct csg_plan {
   int32_t n_units = 0;                 // entries of the execution list
   const int64_t** d_ready[2] = {nullptr, nullptr};  // per signal set: [n_chunks] ready-value pointers
   int64_t* d_zero = nullptr;           // the "ready" value local chunks point at
-  uint32_t* d_counters = nullptr;
-  uint32_t* d_ticket = nullptr;
-  csg::DeviceDiag* d_diag = nullptr;
+  // per-call state, two sets by call parity (see GemmArgs::next_ticket)
+  uint32_t* d_counters = nullptr;      // [2][n_chunks]
+  uint32_t* d_ticket = nullptr;        // [2][kXcdLists]
+  csg::DeviceDiag* d_diag = nullptr;   // [2]
+  uint32_t reset_for_epoch = 0;        // call whose state set a launched kernel clears (0: none)
   uint32_t* h_out_flags = nullptr;     // coherent host memory, per chunk: the producer's emitted
                                        // flags; consumers: the call whose kernel has finished reading
                                        // the chunk's rows
@@ -174,6 +176,11 @@ struct csg_plan {
 
   int32_t n_chunks() const { return static_cast<int32_t>(sched.chunks.size()); }
   int32_t copy_workgroups() const { return cfg.copy_workgroups; }
+  size_t n_flags() const { return static_cast<size_t>(std::max(n_chunks(), 1)); }
+  uint32_t* counters(int set) const { return d_counters + set * n_flags(); }
+  uint32_t* ticket(int set) const { return d_ticket + set * csg::kXcdLists; }
+  csg::DeviceDiag* diag(int set) const { return d_diag + set; }
+  uint32_t* slot_count(int set) const { return d_slot_count ? d_slot_count + set * map.n_tiles() : nullptr; }
   bool consumer() const { return op == CSG_AG_GEMM || op == CSG_GROUPED_GEMM; }
   bool allreduce() const { return op == CSG_GEMM_AR; }
   // chunks that get copies, in the order the copies are issued: consumers and GEMM-RS,
@@ -330,22 +337,23 @@ csg_status setup_device(csg_plan* p) {
   const size_t nflag = static_cast<size_t>(std::max(p->n_chunks(), 1));
   CSG_HIP(hipMalloc(&p->d_zero, 64));
   CSG_HIP(hipMemset(p->d_zero, 0, 64));
-  CSG_HIP(hipMalloc(&p->d_counters, nflag * 4));
-  CSG_HIP(hipMemset(p->d_counters, 0, nflag * 4));
-  CSG_HIP(hipMalloc(&p->d_ticket, csg::kXcdLists * 4));
+  CSG_HIP(hipMalloc(&p->d_counters, 2 * nflag * 4));
+  CSG_HIP(hipMemset(p->d_counters, 0, 2 * nflag * 4));
+  CSG_HIP(hipMalloc(&p->d_ticket, 2 * csg::kXcdLists * 4));
+  CSG_HIP(hipMemset(p->d_ticket, 0, 2 * csg::kXcdLists * 4));
   if (ws_slices > 0) {
     const size_t ws_bytes = static_cast<size_t>(ws_slices) * p->cfg.bm * p->cfg.bn * sizeof(float);
     CSG_HIP(hipMalloc(&p->d_ws, ws_bytes));
-    CSG_HIP(hipMalloc(&p->d_slot_count, static_cast<size_t>(n_tiles) * 4));
-    CSG_HIP(hipMemset(p->d_slot_count, 0, static_cast<size_t>(n_tiles) * 4));
+    CSG_HIP(hipMalloc(&p->d_slot_count, 2 * static_cast<size_t>(n_tiles) * 4));
+    CSG_HIP(hipMemset(p->d_slot_count, 0, 2 * static_cast<size_t>(n_tiles) * 4));
   }
   if (p->cfg.trace) {
     const size_t words = static_cast<size_t>(std::max(n_units, 1)) * csg::kTraceWords;
     CSG_HIP(hipMalloc(&p->d_trace, words * sizeof(uint64_t)));
     CSG_HIP(hipMemset(p->d_trace, 0, words * sizeof(uint64_t)));
   }
-  CSG_HIP(hipMalloc(&p->d_diag, sizeof(csg::DeviceDiag)));
-  CSG_HIP(hipMemset(p->d_diag, 0, sizeof(csg::DeviceDiag)));
+  CSG_HIP(hipMalloc(&p->d_diag, 2 * sizeof(csg::DeviceDiag)));
+  CSG_HIP(hipMemset(p->d_diag, 0, 2 * sizeof(csg::DeviceDiag)));
   CSG_HIP(hipHostMalloc(&p->h_out_flags, nflag * 4, hipHostMallocMapped | hipHostMallocCoherent));
   std::memset(p->h_out_flags, 0, nflag * 4);
   CSG_HIP(hipHostGetDevicePointer(reinterpret_cast<void**>(&p->h_out_flags_dev), p->h_out_flags, 0));
@@ -518,14 +526,19 @@ csg_status begin_call(csg_plan* p, csg_mode mode, CallState* cs) {
 }
 
 // The call's prologue on the compute stream (before its kernel, if any).
+// The previous call's kernel cleared this call's state set when it ran, unless the
+// previous call launched none (copy-only, an error) or the copies are the kernel's own
+// (their ready words depend on this call's mode): then the prologue kernel does.
 csg_status launch_prologue_call(csg_plan* p, csg_mode mode, hipStream_t compute) {
+  const int set = p->epoch & 1;
+  if (mode != CSG_MODE_COPY_ONLY && !p->kernel_copies() && p->reset_for_epoch == p->epoch) return CSG_OK;
   csg::PrologueArgs pa{};
-  pa.counters = p->d_counters;
+  pa.counters = p->counters(set);
   pa.n_chunks = p->n_chunks();
   pa.epoch = p->epoch;
-  pa.ticket = p->d_ticket;
-  pa.diag = p->d_diag;
-  pa.slot_count = p->d_slot_count;
+  pa.ticket = p->ticket(set);
+  pa.diag = p->diag(set);
+  pa.slot_count = p->slot_count(set);
   pa.n_slots = p->ws_slices > 0 ? p->map.n_tiles() : 0;
   if (p->kernel_copies()) {
     // consumers' remote chunks are not there until the copy workgroups move them;
@@ -601,17 +614,26 @@ csg_status launch_gemm(csg_plan* p, const void* A, const void* B, void* C, csg_m
   // consumers wait for this call's copies in; the producer, before overwriting a
   // chunk's rows of C, for the previous call's copy out of them
   a.ready = p->d_ready[p->consumer() ? (p->epoch & 1) : ((p->epoch + 1) & 1)];
-  a.counters = p->d_counters;
+  const int set = p->epoch & 1, next = set ^ 1;
+  a.counters = p->counters(set);
   a.need = p->d_need;
   a.out_flags = p->h_out_flags_dev;
-  a.ticket = p->d_ticket;
+  a.ticket = p->ticket(set);
   a.list_begin = p->d_list_begin;
-  a.diag = p->d_diag;
+  a.diag = p->diag(set);
   a.timeout_ticks = static_cast<uint64_t>(p->cfg.timeout_ms) * 100000ull;  // 100 MHz wall clock
   a.epoch = p->epoch;
   a.n_tiles = p->n_units;
   a.ws = p->d_ws;
-  a.slot_count = p->d_slot_count;
+  a.slot_count = p->slot_count(set);
+  if (!p->kernel_copies()) {
+    // clear the next call's set in this kernel (the next call then needs no prologue)
+    a.next_ticket = p->ticket(next);
+    a.next_counters = p->counters(next);
+    a.next_slot_count = p->slot_count(next);
+    a.next_diag = p->diag(next);
+    a.next_n_slots = p->ws_slices > 0 ? p->map.n_tiles() : 0;
+  }
   a.n_chunks = p->n_chunks();
   a.dynamic_ticket = p->cfg.tile_dispatch == 2 ? 0 : 1;
   a.steal = (p->ws_slices > 0 && a.dynamic_ticket) ? 0 : 1;
@@ -659,6 +681,7 @@ csg_status launch_gemm(csg_plan* p, const void* A, const void* B, void* C, csg_m
   p->expected_units = static_cast<uint32_t>(a.n_tiles);
   const int slot = static_cast<int>(p->n_launches % kTimingRing);
   CSG_HIP(csg::launch_chunk_gemm(p->key, a, grid, compute, p->ev_k0[slot], p->ev_k1[slot]));
+  p->reset_for_epoch = a.next_ticket ? p->epoch + 1 : 0;
   ++p->n_launches;
   CSG_HIP(hipEventRecord(p->ev_kernel_done[p->epoch & 1], compute));
   p->kernel_pending[p->epoch & 1] = true;
@@ -1304,7 +1327,7 @@ csg_status csg_plan_check(csg_plan* p, csg_diag* out) {
     csg_status st = drain_copies(p, true);
     if (st != CSG_OK) return st;
     csg::DeviceDiag dd{};
-    CSG_HIP(hipMemcpyAsync(&dd, p->d_diag, sizeof dd, hipMemcpyDeviceToHost, p->aux));
+    CSG_HIP(hipMemcpyAsync(&dd, p->diag(p->epoch & 1), sizeof dd, hipMemcpyDeviceToHost, p->aux));
     CSG_HIP(hipStreamSynchronize(p->aux));
     if (dd.timed_out && !d.timed_out) d = csg_diag{1, dd.chunk, dd.tile, dd.observed, dd.epoch, 0};
     if (!d.timed_out && p->kernel_pending[p->epoch & 1] && dd.units_done != p->expected_units) {

@@ -626,6 +626,21 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int wm = wave % Loop::WAVES_M, wn = wave / Loop::WAVES_M;
+  if (blockIdx.x == 0 && a.next_ticket) {
+    // clear the next call's state set (its own prologue, folded into this kernel)
+    for (int i = tid; i < a.next_n_slots; i += kThreads) a.next_slot_count[i] = 0u;
+    for (int c = tid; c < a.n_chunks; c += kThreads) a.next_counters[c] = 0u;
+    if (tid < kXcdLists) a.next_ticket[tid] = 0u;
+    if (tid == 0) {
+      a.next_diag->timed_out = 0u;
+      a.next_diag->chunk = -1;
+      a.next_diag->tile = -1;
+      a.next_diag->observed = 0u;
+      a.next_diag->epoch = a.epoch + 1;
+      a.next_diag->abort = 0u;
+      a.next_diag->units_done = 0u;
+    }
+  }
   for (int i = tid; i < kMaxChunks / 32; i += kThreads) ready_bits[i] = 0;
   const int in_bytes = (Loop::BK == 64) ? 2 : 4;
   uint32_t xcd;

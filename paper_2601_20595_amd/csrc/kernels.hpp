@@ -120,6 +120,15 @@ struct GemmArgs {
   int32_t n_peers;
   int32_t own_chunk_rows;
   int32_t own_shard;                    // shard index of the own shard (diagnostics)
+  // Per-call state comes in two sets, by call parity. The kernel of one call clears the
+  // set the next call uses (workgroup 0, at its start: the call before, which used that
+  // set, has finished), so a call whose predecessor ran such a kernel needs no prologue
+  // kernel. Null when the next call's prologue clears it instead.
+  uint32_t* next_ticket;
+  uint32_t* next_counters;
+  uint32_t* next_slot_count;
+  DeviceDiag* next_diag;
+  int32_t next_n_slots;
 };
 
 // Everything the per-call prologue resets.
