@@ -23,5 +23,6 @@ The paper prints no numeric worked example, so no stored value comes from it.
 from .schedule import (Chunk, ScheduleError, uniform_chunks, uniform_schedule, grouped_schedule,
                        order_ring, order_swizzle1d, order_rs_ring, order_permutation, validate)
 from .depmap import dep_map, tile_grid, DepMap
+from .attention import attention, attention_chunked, attention_fsum
 from .gemm import (ag_gemm, gemm_rs, gemm_ar, grouped_gemm, gemm_rows, gemm_elems, exact_dot_fsum,
                    max_rel_error, num_threads)

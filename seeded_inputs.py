@@ -12,7 +12,8 @@ streams
 
     0 = A / X values, 1 = B values, 2 = arrival permutation,
     3 = copy delays,  4 = token routing,
-    5 = the peers' partial sums (GEMM-AR), 6 = the other shards' reduced rows (GEMM-AR).
+    5 = the peers' partial sums (GEMM-AR), 6 = the other shards' reduced rows (GEMM-AR),
+    7 = attention values (Q, then K, then V, from one generator).
 
 Workload shapes are tensor-parallel FFN slices of Llama-3-8B-like
 (hidden 4096, FFN 14336/8 = 1792) and Llama-3-70B-like (hidden 8192,
@@ -28,7 +29,7 @@ from typing import Optional
 import numpy as np
 
 STREAM_A, STREAM_B, STREAM_PERM, STREAM_DELAY, STREAM_ROUTE = 0, 1, 2, 3, 4
-STREAM_PARTIALS, STREAM_REDUCED = 5, 6
+STREAM_PARTIALS, STREAM_REDUCED, STREAM_ATTN = 5, 6, 7
 
 
 def rng(cfg_id: int, stream: int, rep: int = 0) -> np.random.Generator:
@@ -114,7 +115,8 @@ def draw_topk_routing(cfg_id: int, rep: int, n_tokens: int, n_experts: int, topk
 @dataclass
 class Workload:
     """One workload of the benchmark/test suite. ``op`` is "ag", "rs", "ar" (GEMM +
-    all-reduce) or "grouped"."""
+    all-reduce), "grouped" or "attn" (ring attention: M = query rows of this rank,
+    shard_rows = key rows per rank, heads / kv_heads / head_dim in ``extras``)."""
     cfg_id: int
     name: str
     op: str
@@ -139,6 +141,10 @@ class Workload:
 
     @property
     def flops(self) -> float:
+        if self.op == "attn":
+            # two products (scores and weighted values) per query row, key row and head
+            e = self.extras
+            return 4.0 * self.M * self.world * self.shard_rows * e["head_dim"] * e["heads"]
         return 2.0 * self.M * self.N * self.K
 
 
@@ -162,6 +168,12 @@ WORKLOADS = {
     6: Workload(6, "ar_w8_bf16_8192x1792x4096", "ar", M=8192, N=4096, K=1792, dtype="bf16",
                 out_dtype="bf16", dist="normal", world=8, shard_rows=1024, chunks_per_shard=4,
                 order="rs_ring"),
+    # sequence-parallel ring attention, 8B-like heads (32 query heads, 8 key/value heads,
+    # head dim 128), a 32768-token sequence over 8 ranks: 4096 queries and 4096 keys per
+    # rank, key/value shards arriving in ring order, 2 chunks per shard
+    7: Workload(7, "ring_attn_w8_bf16_h32kv8_s32768_d128", "attn", M=4096, N=0, K=0, dtype="bf16",
+                out_dtype="bf16", dist="normal", world=8, shard_rows=4096, chunks_per_shard=2,
+                order="ring", extras={"heads": 32, "kv_heads": 8, "head_dim": 128}),
 }
 
 
@@ -178,6 +190,8 @@ class Drawn:
     partials: Optional[Matrix] = None        # ar: [world-1, S, N] the peers' partial sums of this
                                              # rank's shard, peers in ascending rank order
     reduced: Optional[Matrix] = None         # ar: [M, N] reduced rows the other shards' owners send
+    V: Optional[Matrix] = None               # attn: values [S, kv_heads, head_dim] (A = queries
+                                             # [Sq, heads, head_dim], B = keys [S, kv_heads, head_dim])
 
 
 def grouped_layout(routing: np.ndarray, world: int, n_experts: int):
@@ -222,6 +236,23 @@ def draw(w: Workload, rep: int = 0, dist: Optional[str] = None, M: Optional[int]
         if w.delays:
             d.delays_us = draw_delays_us(cid, rep, n_remote)
         return d
+    if w.op == "attn":
+        e = w.extras
+        S = w.world * w.shard_rows
+        g = rng(cid, STREAM_ATTN, rep)
+        mats = []
+        for shape in ((M, e["heads"], e["head_dim"]), (S, e["kv_heads"], e["head_dim"]),
+                      (S, e["kv_heads"], e["head_dim"])):
+            if dist == "int":
+                v = g.integers(-2, 3, size=shape).astype(np.float32)
+            else:
+                v = g.standard_normal(size=shape, dtype=np.float32)
+            if w.dtype == "bf16":
+                bits = f32_to_bf16_bits(v)
+                mats.append(Matrix(values=bf16_bits_to_f32(bits), dtype="bf16", bits=bits))
+            else:
+                mats.append(Matrix(values=np.ascontiguousarray(v), dtype="f32"))
+        return Drawn(A=mats[0], B=mats[1], V=mats[2])
     if w.op == "grouped":
         routing = draw_topk_routing(cid, rep, w.n_tokens, w.n_experts, w.topk, w.zipf_s)
         row_token, counts = grouped_layout(routing, w.world, w.n_experts)
