@@ -336,6 +336,36 @@ csg_status csg_grouped_gemm(csg_plan* p, void* x_landing, const void* x_staging,
                             const void* b_enk, void* c, csg_mode mode, void* compute_stream,
                             void* copy_stream);
 
+/* ---- ring attention (Evaluation, the Ring-Attn operator; Section 5.2) ------------- */
+
+/* Sequence-parallel attention on one rank: the rank's q_rows queries (n_heads heads
+ * of head_dim) attend to every rank's keys and values, whose rows arrive in chunks
+ * by the schedule kv_schedule (chunks over key rows, arrival order; local chunks
+ * are the rank's own keys). Key/value heads are shared by n_heads / n_kv_heads
+ * query heads each. The kernel supports head_dim 128 (else CSG_ERR_UNSUPPORTED) and
+ * chunks of a multiple of 64 key rows; cfg may set timeout_ms, copy_engines and
+ * num_workgroups (others must be 0). Free with csg_plan_destroy; csg_plan_check and
+ * csg_plan_kernel_times apply. */
+csg_status csg_attn_plan_create(int32_t n_heads, int32_t n_kv_heads, int32_t head_dim,
+                                int64_t q_rows, const csg_schedule* kv_schedule,
+                                const csg_plan_cfg* cfg, int device, csg_plan** out);
+
+/* One ring-attention call. Layouts (bf16, row-major, no padding): q and o are
+ * [q_rows][n_heads][head_dim]; k_landing / v_landing (and k_staging / v_staging, the
+ * simulated peers' shards at the same offsets) are [S][n_kv_heads][head_dim] with S
+ * the schedule's key rows, the local rows already in place in the landing buffers;
+ * lse is float [n_heads][q_rows], the natural-log log-sum-exp of each row's scaled
+ * scores. The result, for every query row and head, is softmax(q . k^T / sqrt(d)) . v
+ * over all S keys (no mask). As for csg_ag_gemm: the kernel is queued on `compute`,
+ * the calling thread copies each remote chunk's keys and values by SDMA (two copies,
+ * one completion signal as the chunk's ready flag) once the previous call's kernel
+ * has finished reading those rows, and returns when the copies have completed. Each
+ * work unit (one head, 128 query rows) consumes the chunks in arrival order, waiting
+ * for each once. Compute-only: the landing buffers must already hold every row. */
+csg_status csg_ring_attn(csg_plan* p, const void* q, void* k_landing, void* v_landing,
+                         const void* k_staging, const void* v_staging, void* o, void* lse,
+                         csg_mode mode, void* compute_stream, void* copy_stream);
+
 /* Waits for the plan's last call to complete (its kernel and every copy it issued)
  * and reports its diagnostics.
  * CSG_ERR_TIMEOUT if a wait expired (details in *out); CSG_ERR_STATE if the kernel

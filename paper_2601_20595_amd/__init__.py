@@ -48,7 +48,7 @@ ABI_FUNCTIONS = (
     "csg_schedule_get", "csg_schedule_destroy",
     "csg_plan_create", "csg_plan_info_get", "csg_plan_get_map", "csg_plan_set_copy_delays",
     "csg_ag_gemm", "csg_gemm_rs", "csg_gemm_ar", "csg_grouped_gemm", "csg_plan_check", "csg_plan_kernel_times",
-    "csg_plan_trace", "csg_plan_destroy",
+    "csg_plan_trace", "csg_plan_destroy", "csg_attn_plan_create", "csg_ring_attn",
 )
 
 
@@ -125,6 +125,8 @@ def _lib():
         "csg_ag_gemm": ([vp, vp, vp, vp, vp, st, vp, vp], st),
         "csg_gemm_rs": ([vp, vp, vp, vp, vp, st, vp, vp], st),
         "csg_gemm_ar": ([vp, vp, vp, vp, vp, vp, vp, vp, st, vp, vp], st),
+        "csg_attn_plan_create": ([i32, i32, i32, i64, vp, P(csg_plan_cfg), ctypes.c_int, P(vp)], st),
+        "csg_ring_attn": ([vp, vp, vp, vp, vp, vp, vp, vp, st, vp, vp], st),
         "csg_grouped_gemm": ([vp, vp, vp, vp, vp, st, vp, vp], st),
         "csg_plan_check": ([vp, P(csg_diag)], st),
         "csg_plan_kernel_times": ([vp, P(ctypes.c_float), i32, P(i32)], st),
@@ -311,6 +313,22 @@ def csg_gemm_rs(plan: int, a, b_nk, c, c_outgoing, mode="overlap", compute_strea
                               _stream(compute_stream), _stream(copy_stream)), "csg_gemm_rs")
 
 
+def csg_attn_plan_create(n_heads: int, n_kv_heads: int, head_dim: int, q_rows: int, sched: int,
+                         cfg: Optional[dict] = None, device: int = 0) -> int:
+    c = csg_plan_cfg(**(cfg or {}))
+    out = ctypes.c_void_p()
+    _check(_lib().csg_attn_plan_create(n_heads, n_kv_heads, head_dim, q_rows, sched, ctypes.byref(c), device,
+                                       ctypes.byref(out)), "csg_attn_plan_create")
+    return out.value
+
+
+def csg_ring_attn(plan: int, q, k_landing, v_landing, k_staging, v_staging, o, lse, mode="overlap",
+                  compute_stream=None, copy_stream=None) -> None:
+    _check(_lib().csg_ring_attn(plan, _ptr(q), _ptr(k_landing), _ptr(v_landing), _ptr(k_staging), _ptr(v_staging),
+                                _ptr(o), _ptr(lse), _mode(mode), _stream(compute_stream), _stream(copy_stream)),
+           "csg_ring_attn")
+
+
 def csg_gemm_ar(plan: int, a, b_nk, c, c_outgoing, partials_staging, partials_landing, reduced_staging,
                 mode="overlap", compute_stream=None, copy_stream=None) -> None:
     _check(_lib().csg_gemm_ar(plan, _ptr(a), _ptr(b_nk), _ptr(c), _ptr(c_outgoing), _ptr(partials_staging),
@@ -449,3 +467,16 @@ class Plan:
             self.close()
         except Exception:
             pass
+
+
+class AttnPlan(Plan):
+    """Owns a ring-attention csg_plan (csg_attn_plan_create)."""
+
+    def __init__(self, n_heads, n_kv_heads, head_dim, q_rows, schedule: Schedule, cfg=None, device: int = 0):
+        self.op = "attn"
+        self.handle = csg_attn_plan_create(n_heads, n_kv_heads, head_dim, q_rows, schedule.handle, cfg, device)
+
+    def ring_attn(self, q, k_landing, v_landing, k_staging, v_staging, o, lse, mode="overlap", compute_stream=None,
+                  copy_stream=None):
+        csg_ring_attn(self.handle, q, k_landing, v_landing, k_staging, v_staging, o, lse, mode, compute_stream,
+                      copy_stream)

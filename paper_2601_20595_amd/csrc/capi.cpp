@@ -24,6 +24,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <atomic>
 #include <chrono>
 #include <cstdarg>
@@ -35,6 +36,7 @@
 #include <vector>
 
 #include "../../include/csg.h"
+#include "attn.hpp"
 #include "kernels.hpp"
 #include "planner.hpp"
 #include "sdma.hpp"
@@ -92,6 +94,7 @@ struct csg_schedule {
 
 struct csg_plan {
   csg_op op = CSG_AG_GEMM;
+  bool attn = false;                   // a ring-attention plan (csg_attn_plan_create); op is unused
   int64_t M = 0, N = 0, K = 0;
   csg_dtype in_dtype = CSG_BF16, out_dtype = CSG_BF16;
   csg::Schedule sched;
@@ -147,6 +150,10 @@ struct csg_plan {
   const int64_t** d_part_ready[2] = {nullptr, nullptr};
   int64_t ar_own_row0 = 0, ar_own_rows = 0;  // the own shard
   int32_t ar_chunk_rows = 0, ar_peers = 0, ar_own_shard = 0;
+  // ring attention: heads, key/value heads, query rows; device arrays
+  int32_t at_heads = 0, at_kv_heads = 0, at_q_rows = 0;
+  int32_t* d_arrival = nullptr;        // [n_chunks] chunk id at each arrival position
+  int32_t* d_chunk_rows = nullptr;     // [2 * n_chunks] key row begin / end by chunk id
   const void* ar_partials = nullptr;  // this call's partials landing buffer
   bool copies_in_flight = false;       // a call returned before its copies completed (consumers:
                                        // error paths only; producer: every call)
@@ -181,7 +188,10 @@ struct csg_plan {
   uint32_t* ticket(int set) const { return d_ticket + set * csg::kXcdLists; }
   csg::DeviceDiag* diag(int set) const { return d_diag + set; }
   uint32_t* slot_count(int set) const { return d_slot_count ? d_slot_count + set * map.n_tiles() : nullptr; }
-  bool consumer() const { return op == CSG_AG_GEMM || op == CSG_GROUPED_GEMM; }
+  bool consumer() const { return op == CSG_AG_GEMM || op == CSG_GROUPED_GEMM || attention(); }
+  bool attention() const { return attn; }
+  // ring attention: copies per chunk (keys and values), both completing its signal
+  hsa_signal_value_t copies_per_chunk() const { return attention() ? 2 : 1; }
   bool allreduce() const { return op == CSG_GEMM_AR; }
   // chunks that get copies, in the order the copies are issued: consumers and GEMM-RS,
   // the remote chunks; GEMM-AR, every chunk (own chunks are sent once reduced)
@@ -217,7 +227,8 @@ void free_plan_device(csg_plan* p) {
                     static_cast<void*>(p->d_copy_chunk), static_cast<void*>(p->d_copy_parts),
                     static_cast<void*>(p->d_copy_done), static_cast<void*>(p->d_kready),
                     static_cast<void*>(p->d_ready_k), static_cast<void*>(p->d_chunk_sent),
-                    static_cast<void*>(p->d_copy_state), static_cast<void*>(p->d_release_ticks)})
+                    static_cast<void*>(p->d_copy_state), static_cast<void*>(p->d_release_ticks),
+                    static_cast<void*>(p->d_arrival), static_cast<void*>(p->d_chunk_rows)})
     if (ptr) (void)hipFree(ptr);
   if (p->h_out_flags) (void)hipHostFree(p->h_out_flags);
   for (hipEvent_t e : {p->ev_copy_in, p->ev_prologue, p->ev_kernel_done[0], p->ev_kernel_done[1]})
@@ -517,7 +528,8 @@ csg_status begin_call(csg_plan* p, csg_mode mode, CallState* cs) {
       for (hsa_signal_t sgn : *polled)
         if (csg::sdma_wait(sgn, 0, p->cfg.timeout_ms * 4) != 0)
           return fail(CSG_ERR_TIMEOUT, "an earlier copy of a partial sum did not complete");
-    const hsa_signal_value_t v = mode == CSG_MODE_COMPUTE_ONLY ? 0 : 1;  // compute-only: every chunk ready
+    // compute-only: every chunk ready; otherwise one decrement per copy of the chunk
+    const hsa_signal_value_t v = mode == CSG_MODE_COMPUTE_ONLY ? 0 : p->copies_per_chunk();
     for (hsa_signal_t sgn : *polled) hsa_signal_store_relaxed(sgn, v);
     std::atomic_thread_fence(std::memory_order_seq_cst);  // armed before the kernel launch below
   }
@@ -705,6 +717,8 @@ struct CopyIssuer {
   size_t next = 0;
   double release_us = 0.0;
   bool prev_done;
+  void* landing2 = nullptr;        // ring attention: values (landing / staging: keys)
+  const void* staging2 = nullptr;
 
   CopyIssuer(csg_plan* plan, void* l, const void* s, uint32_t prev)
       : p(plan), landing(l), staging(s), prev_reader(prev), t0(Clock::now()), prev_done(prev == 0) {}
@@ -712,7 +726,7 @@ struct CopyIssuer {
   // Issues copies in arrival order. Without `block` it stops at the first copy that
   // would have to wait (for its release time or for the previous kernel).
   csg_status run(bool block) {
-    const int64_t row_bytes = p->K * in_bytes(p);
+    const int64_t row_bytes = p->attention() ? int64_t{p->at_kv_heads} * csg::kAttnHeadDim * 2 : p->K * in_bytes(p);
     const std::vector<hsa_signal_t>& sigs = call_signals(p);
     const int prev_parity = static_cast<int>(prev_reader & 1);
     const auto budget = std::chrono::milliseconds(p->cfg.timeout_ms) * 4;
@@ -754,8 +768,13 @@ struct CopyIssuer {
       const int64_t off = c.row_begin * row_bytes;
       const int64_t bytes = (c.row_end - c.row_begin) * row_bytes;
       const int eng = static_cast<int>(i % p->sdma.count());
-      const hsa_status_t hs = p->sdma.copy(static_cast<char*>(landing) + off, static_cast<const char*>(staging) + off,
-                                           static_cast<size_t>(bytes), eng, nullptr, sigs[i]);
+      hsa_status_t hs = p->sdma.copy(static_cast<char*>(landing) + off, static_cast<const char*>(staging) + off,
+                                     static_cast<size_t>(bytes), eng, nullptr, sigs[i]);
+      // ring attention: the values follow on the next engine; the chunk's signal,
+      // armed to 2, reaches 0 when both copies have completed
+      if (hs == HSA_STATUS_SUCCESS && landing2)
+        hs = p->sdma.copy(static_cast<char*>(landing2) + off, static_cast<const char*>(staging2) + off,
+                          static_cast<size_t>(bytes), eng + 1, nullptr, sigs[i]);
       if (hs != HSA_STATUS_SUCCESS) {
         // the chunks not copied keep their signals armed: the kernel's bounded waits for
         // them expire and it reports them through csg_plan_check
@@ -766,6 +785,98 @@ struct CopyIssuer {
     return CSG_OK;
   }
 };
+
+// Ring attention: device state of a plan (work units, chunk tables, per-call state,
+// copy engines and the per-chunk signals of the key/value copies).
+csg_status setup_attn_device(csg_plan* p) {
+  DeviceGuard g(p->device);
+  if (g.err != hipSuccess) return hip_fail(g.err, "hipSetDevice");
+  p->n_units = ((p->at_q_rows + csg::kAttnBlockQ - 1) / csg::kAttnBlockQ) * p->at_heads;
+  std::vector<int32_t> rows(2 * static_cast<size_t>(p->n_chunks()));
+  for (int32_t c = 0; c < p->n_chunks(); ++c) {
+    rows[2 * c] = static_cast<int32_t>(p->sched.chunks[c].row_begin);
+    rows[2 * c + 1] = static_cast<int32_t>(p->sched.chunks[c].row_end);
+  }
+  csg_status st;
+  if ((st = upload(&p->d_arrival, p->sched.order)) != CSG_OK) return st;
+  if ((st = upload(&p->d_chunk_rows, rows)) != CSG_OK) return st;
+  const size_t nflag = p->n_flags();
+  CSG_HIP(hipMalloc(&p->d_zero, 64));
+  CSG_HIP(hipMemset(p->d_zero, 0, 64));
+  CSG_HIP(hipMalloc(&p->d_counters, 2 * nflag * 4));
+  CSG_HIP(hipMemset(p->d_counters, 0, 2 * nflag * 4));
+  CSG_HIP(hipMalloc(&p->d_ticket, 2 * csg::kXcdLists * 4));
+  CSG_HIP(hipMemset(p->d_ticket, 0, 2 * csg::kXcdLists * 4));
+  CSG_HIP(hipMalloc(&p->d_diag, 2 * sizeof(csg::DeviceDiag)));
+  CSG_HIP(hipMemset(p->d_diag, 0, 2 * sizeof(csg::DeviceDiag)));
+  CSG_HIP(hipHostMalloc(&p->h_out_flags, nflag * 4, hipHostMallocMapped | hipHostMallocCoherent));
+  std::memset(p->h_out_flags, 0, nflag * 4);
+  CSG_HIP(hipHostGetDevicePointer(reinterpret_cast<void**>(&p->h_out_flags_dev), p->h_out_flags, 0));
+  CSG_HIP(hipMalloc(&p->d_scratch, 64));
+  CSG_HIP(hipDeviceSynchronize());
+  std::string err = p->sdma.open(p->device, p->cfg.copy_engines, p->d_scratch, p->d_scratch + 8);
+  if (!err.empty()) return fail(CSG_ERR_HIP, "copy engines: %s", err.c_str());
+  for (int set = 0; set < 2; ++set) {
+    p->sig_ready[set].assign(p->remote_order.size(), hsa_signal_t{0});
+    std::vector<const int64_t*> ptrs(p->n_chunks(), p->d_zero);  // local chunks: never copied
+    for (size_t i = 0; i < p->remote_order.size(); ++i) {
+      hsa_status_t hs = p->sdma.make_signal(0, &p->sig_ready[set][i]);
+      const int64_t* vp = nullptr;
+      if (hs == HSA_STATUS_SUCCESS) hs = p->sdma.signal_value_ptr(p->sig_ready[set][i], &vp);
+      if (hs != HSA_STATUS_SUCCESS) return fail(CSG_ERR_NOMEM, "copy signal: %s", csg::hsa_error(hs).c_str());
+      ptrs[p->remote_order[i]] = vp;
+    }
+    if ((st = upload(&p->d_ready[set], ptrs)) != CSG_OK) return st;
+  }
+  CSG_HIP(hipEventCreateWithFlags(&p->ev_copy_in, hipEventDisableTiming));
+  CSG_HIP(hipEventCreateWithFlags(&p->ev_prologue, hipEventDisableTiming));
+  for (hipEvent_t& e : p->ev_kernel_done) CSG_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+  for (int i = 0; i < kTimingRing; ++i) {
+    CSG_HIP(hipEventCreate(&p->ev_k0[i]));
+    CSG_HIP(hipEventCreate(&p->ev_k1[i]));
+  }
+  CSG_HIP(hipStreamCreateWithFlags(&p->aux, hipStreamNonBlocking));
+  CSG_HIP(hipDeviceSynchronize());
+  return CSG_OK;
+}
+
+csg_status launch_attn(csg_plan* p, const void* q, const void* k, const void* v, void* o, void* lse,
+                       hipStream_t compute) {
+  const int set = p->epoch & 1, next = set ^ 1;
+  csg::AttnArgs a{};
+  a.Q = static_cast<const uint16_t*>(q);
+  a.K = static_cast<const uint16_t*>(k);
+  a.V = static_cast<const uint16_t*>(v);
+  a.O = static_cast<uint16_t*>(o);
+  a.LSE = static_cast<float*>(lse);
+  a.Sq = p->at_q_rows;
+  a.H = p->at_heads;
+  a.Hkv = p->at_kv_heads;
+  a.n_units = p->n_units;
+  a.n_chunks = p->n_chunks();
+  a.arrival = p->d_arrival;
+  a.chunk_rows = p->d_chunk_rows;
+  a.ready = p->d_ready[set];
+  a.counters = p->counters(set);
+  a.out_flags = p->h_out_flags_dev;
+  a.ticket = p->ticket(set);
+  a.diag = p->diag(set);
+  a.timeout_ticks = static_cast<uint64_t>(p->cfg.timeout_ms) * 100000ull;  // 100 MHz wall clock
+  a.epoch = p->epoch;
+  a.scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(static_cast<double>(csg::kAttnHeadDim)));
+  a.next_ticket = p->ticket(next);
+  a.next_counters = p->counters(next);
+  a.next_diag = p->diag(next);
+  const int slot = static_cast<int>(p->n_launches % kTimingRing);
+  CSG_HIP(csg::launch_ring_attn(a, p->grid, compute, p->ev_k0[slot], p->ev_k1[slot]));
+  p->reset_for_epoch = p->epoch + 1;
+  p->expected_units = static_cast<uint32_t>(p->n_units);
+  ++p->n_launches;
+  CSG_HIP(hipEventRecord(p->ev_kernel_done[p->epoch & 1], compute));
+  p->kernel_pending[p->epoch & 1] = true;
+  p->last_kernel_epoch = p->epoch;
+  return CSG_OK;
+}
 
 // A call whose chunks the kernel moves itself: the prologue and one kernel launch on
 // the compute stream, nothing on the copy stream, no host waits. Consumers: the copy
@@ -1145,21 +1256,22 @@ csg_status csg_plan_set_copy_delays(csg_plan* p, const float* delay_us_host, int
 csg_status csg_ag_gemm(csg_plan* p, void* a_landing, const void* a_staging, const void* b_nk, void* c, csg_mode mode,
                        void* compute_stream, void* copy_stream) {
   if (!p) return fail(CSG_ERR_INVALID, "plan is NULL");
-  if (p->op != CSG_AG_GEMM) return fail(CSG_ERR_INVALID, "plan is not an all-gather GEMM plan");
+  if (p->op != CSG_AG_GEMM || p->attention()) return fail(CSG_ERR_INVALID, "plan is not an all-gather GEMM plan");
   return consumer_call(p, a_landing, a_staging, b_nk, c, mode, compute_stream, copy_stream);
 }
 
 csg_status csg_grouped_gemm(csg_plan* p, void* x_landing, const void* x_staging, const void* b_enk, void* c,
                             csg_mode mode, void* compute_stream, void* copy_stream) {
   if (!p) return fail(CSG_ERR_INVALID, "plan is NULL");
-  if (p->op != CSG_GROUPED_GEMM) return fail(CSG_ERR_INVALID, "plan is not a grouped GEMM plan");
+  if (p->op != CSG_GROUPED_GEMM || p->attention()) return fail(CSG_ERR_INVALID, "plan is not a grouped GEMM plan");
   return consumer_call(p, x_landing, x_staging, b_enk, c, mode, compute_stream, copy_stream);
 }
 
 csg_status csg_gemm_rs(csg_plan* p, const void* a, const void* b_nk, void* c, void* c_outgoing, csg_mode mode,
                        void* compute_stream, void* copy_stream) {
   if (!p) return fail(CSG_ERR_INVALID, "plan is NULL");
-  if (p->op != CSG_GEMM_RS) return fail(CSG_ERR_INVALID, "plan is not a GEMM + reduce-scatter plan");
+  if (p->op != CSG_GEMM_RS || p->attention())
+    return fail(CSG_ERR_INVALID, "plan is not a GEMM + reduce-scatter plan");
   if (p->device < 0) return fail(CSG_ERR_STATE, "host-only plan (created with device < 0) cannot run");
   if (!a || !b_nk || !c || (mode != CSG_MODE_COMPUTE_ONLY && !c_outgoing && !p->remote_order.empty()))
     return fail(CSG_ERR_INVALID, "NULL buffer");
@@ -1218,11 +1330,112 @@ csg_status csg_gemm_rs(csg_plan* p, const void* a, const void* b_nk, void* c, vo
   return CSG_OK;
 }
 
+csg_status csg_attn_plan_create(int32_t n_heads, int32_t n_kv_heads, int32_t head_dim, int64_t q_rows,
+                                const csg_schedule* s, const csg_plan_cfg* cfg, int device, csg_plan** out) {
+  if (!out) return fail(CSG_ERR_INVALID, "out is NULL");
+  *out = nullptr;
+  if (!s) return fail(CSG_ERR_INVALID, "schedule is NULL");
+  if (n_heads < 1 || n_kv_heads < 1 || n_heads % n_kv_heads != 0 || head_dim < 1 || q_rows < 1 ||
+      q_rows > (int64_t{1} << 30))
+    return fail(CSG_ERR_INVALID, "bad attention shape");
+  if (head_dim != csg::kAttnHeadDim)
+    return fail(CSG_ERR_UNSUPPORTED, "the attention kernel is built for head dimension %d", csg::kAttnHeadDim);
+  csg_plan_cfg c = cfg ? *cfg : csg_plan_cfg{};
+  if (c.timeout_ms == 0) c.timeout_ms = 2000;
+  if (c.copy_engines < 0 || c.copy_engines > 32 || c.timeout_ms < 1 || c.num_workgroups < 0)
+    return fail(CSG_ERR_INVALID, "bad plan configuration");
+  if (c.copy_backend != CSG_COPY_SDMA || c.split_k > 1 || c.tail_split > 1 || c.trace)
+    return fail(CSG_ERR_UNSUPPORTED, "attention plans copy with the SDMA engines and split or trace nothing");
+  const csg::Schedule& sch = s->s;
+  if (sch.chunks.size() > 4096) return fail(CSG_ERR_UNSUPPORTED, "at most 4096 chunks");
+  for (const csg::ChunkDesc& ch : sch.chunks)
+    if ((ch.row_end - ch.row_begin) % csg::kAttnBlockKV != 0)
+      return fail(CSG_ERR_UNSUPPORTED, "every key/value chunk must hold a multiple of %d rows", csg::kAttnBlockKV);
+  if (sch.total_rows > (int64_t{1} << 30) / n_kv_heads) return fail(CSG_ERR_INVALID, "sequence too long");
+  csg_plan* p = new (std::nothrow) csg_plan;
+  if (!p) return fail(CSG_ERR_NOMEM, "out of host memory");
+  p->attn = true;
+  p->M = q_rows;
+  p->N = n_heads;
+  p->K = head_dim;
+  p->in_dtype = p->out_dtype = CSG_BF16;
+  p->sched = sch;
+  p->cfg = c;
+  p->at_heads = n_heads;
+  p->at_kv_heads = n_kv_heads;
+  p->at_q_rows = static_cast<int32_t>(q_rows);
+  for (int32_t c_id : p->sched.order)
+    if (!p->sched.chunks[c_id].is_local) p->remote_order.push_back(c_id);
+  if (device >= 0) {
+    char arch[64];
+    csg_status st = csg_device_check(device, arch, sizeof arch);
+    if (st != CSG_OK) {
+      delete p;
+      return st;
+    }
+    p->device = device;
+    {
+      DeviceGuard g(device);
+      hipError_t e = g.err != hipSuccess ? g.err : csg::attn_grid(device, &p->grid);
+      if (e != hipSuccess) {
+        p->device = -1;
+        delete p;
+        return hip_fail(e, "occupancy query");
+      }
+    }
+    if (c.num_workgroups > 0) p->grid = c.num_workgroups;
+    st = setup_attn_device(p);
+    if (st != CSG_OK) {
+      std::string msg = g_last_error;
+      free_plan_device(p);
+      delete p;
+      g_last_error = msg;
+      return st;
+    }
+  }
+  *out = p;
+  return CSG_OK;
+}
+
+csg_status csg_ring_attn(csg_plan* p, const void* q, void* k_landing, void* v_landing, const void* k_staging,
+                         const void* v_staging, void* o, void* lse, csg_mode mode, void* compute_stream,
+                         void* copy_stream) {
+  if (!p) return fail(CSG_ERR_INVALID, "plan is NULL");
+  if (!p->attention()) return fail(CSG_ERR_INVALID, "plan is not a ring-attention plan");
+  if (p->device < 0) return fail(CSG_ERR_STATE, "host-only plan (created with device < 0) cannot run");
+  const bool copies = mode != CSG_MODE_COMPUTE_ONLY && !p->remote_order.empty();
+  if (!q || !k_landing || !v_landing || !o || !lse || (copies && (!k_staging || !v_staging)))
+    return fail(CSG_ERR_INVALID, "NULL buffer");
+  if (!aligned16(q) || !aligned16(k_landing) || !aligned16(v_landing) || !aligned16(k_staging) ||
+      !aligned16(v_staging) || !aligned16(o) || !aligned16(lse))
+    return fail(CSG_ERR_INVALID, "buffers must be 16-byte aligned");
+  hipStream_t compute = static_cast<hipStream_t>(compute_stream), copy = static_cast<hipStream_t>(copy_stream);
+  DeviceGuard g(p->device);
+  if (g.err != hipSuccess) return hip_fail(g.err, "hipSetDevice");
+  CallState cs;
+  const uint32_t prev_reader = p->last_kernel_epoch;  // the kernel that last read the key/value rows
+  csg_status st = begin_call(p, mode, &cs);
+  if (st != CSG_OK) return st;
+  CopyIssuer issuer(p, k_landing, k_staging, prev_reader);
+  issuer.landing2 = v_landing;
+  issuer.staging2 = v_staging;
+  if (copies) {
+    if ((st = ready_copies(p, copy, cs, false)) != CSG_OK) return st;
+    if ((st = issuer.run(false)) != CSG_OK) return st;
+  }
+  if ((st = launch_prologue_call(p, mode, compute)) != CSG_OK) return st;
+  if (mode != CSG_MODE_COPY_ONLY && (st = launch_attn(p, q, k_landing, v_landing, o, lse, compute)) != CSG_OK)
+    return st;
+  if (!copies) return CSG_OK;
+  if ((st = issuer.run(true)) != CSG_OK) return st;
+  return finish_copies(p, p->remote_order.size());
+}
+
 csg_status csg_gemm_ar(csg_plan* p, const void* a, const void* b_nk, void* c, void* c_outgoing,
                        const void* partials_staging, void* partials_landing, const void* reduced_staging,
                        csg_mode mode, void* compute_stream, void* copy_stream) {
   if (!p) return fail(CSG_ERR_INVALID, "plan is NULL");
-  if (p->op != CSG_GEMM_AR) return fail(CSG_ERR_INVALID, "plan is not a GEMM + all-reduce plan");
+  if (p->op != CSG_GEMM_AR || p->attention()) return fail(CSG_ERR_INVALID, "plan is not a GEMM + all-reduce plan");
   if (p->device < 0) return fail(CSG_ERR_STATE, "host-only plan (created with device < 0) cannot run");
   const bool copies = mode != CSG_MODE_COMPUTE_ONLY;
   if (!a || !b_nk || !c || !partials_landing ||

@@ -211,3 +211,19 @@ def test_allreduce_plans_map_like_reduce_scatter_and_validate():
     assert _status(csg.Plan, "ar", 256, 64, 64, "f32", "f32", split, device=-1) == csg.CSG_ERR_UNSUPPORTED
     assert _status(ar.gemm_ar, 16, 16, 16, 16, 16, 16, 16) == csg.CSG_ERR_STATE        # host-only plan
     assert _status(rs.gemm_ar, 16, 16, 16, 16, 16, 16, 16) == csg.CSG_ERR_INVALID      # wrong op
+
+
+def test_attention_plans_validate():
+    s = csg.Schedule.uniform(4, 1, 256, 2, "ring")                       # 128-row key chunks
+    p = csg.AttnPlan(8, 2, 128, 300, s, device=-1)
+    assert p.info.n_chunks == 8
+    assert _status(p.ring_attn, 16, 16, 16, 16, 16, 16, 16) == csg.CSG_ERR_STATE          # host-only plan
+    assert _status(p.ag_gemm, 16, 16, 16, 16) == csg.CSG_ERR_INVALID                      # not a GEMM plan
+    assert _status(csg.AttnPlan, 8, 2, 64, 300, s, device=-1) == csg.CSG_ERR_UNSUPPORTED    # head dim 128 only
+    assert _status(csg.AttnPlan, 8, 3, 128, 300, s, device=-1) == csg.CSG_ERR_INVALID       # heads % kv heads
+    assert _status(csg.AttnPlan, 8, 2, 128, 0, s, device=-1) == csg.CSG_ERR_INVALID
+    assert _status(csg.AttnPlan, 8, 2, 128, 300, s, cfg={"copy_backend": 1}, device=-1) == csg.CSG_ERR_UNSUPPORTED
+    odd = csg.Schedule.uniform(4, 1, 96, 1, "ring")                         # 96-row chunks
+    assert _status(csg.AttnPlan, 8, 2, 128, 300, odd, device=-1) == csg.CSG_ERR_UNSUPPORTED
+    gemm = csg.Plan("ag", 1024, 64, 64, "bf16", "bf16", s, device=-1)
+    assert _status(csg.csg_ring_attn, gemm.handle, 16, 16, 16, 16, 16, 16, 16) == csg.CSG_ERR_INVALID
