@@ -79,7 +79,11 @@ def main():
         sched = csg.Schedule.uniform(w.world, w.rank, w.shard_rows, w.chunks_per_shard, w.order, d.perm)
         group_rows = None
     cfg = {"copy_engines": args.lanes} if args.lanes else None
-    plan = csg.Plan(w.op, w.M, w.N, w.K, w.dtype, w.out_dtype, sched, group_rows=group_rows, cfg=cfg)
+    if w.op == "attn":
+        e = w.extras
+        plan = csg.AttnPlan(e["heads"], e["kv_heads"], e["head_dim"], w.M, sched, cfg=cfg)
+    else:
+        plan = csg.Plan(w.op, w.M, w.N, w.K, w.dtype, w.out_dtype, sched, group_rows=group_rows, cfg=cfg)
     if d.delays_us is not None:
         plan.set_copy_delays(d.delays_us)
     chunks, _ = sched.get()
@@ -92,7 +96,17 @@ def main():
     in_bytes = 2 if w.dtype == "bf16" else 4
     out_bytes = 2 if w.out_dtype == "bf16" else 4
     p_stage = p_land = reduced = None
-    if w.op == "ar":
+    if w.op == "attn":
+        # the other ranks' keys and values arrive; a_full = queries
+        e = w.extras
+        landing = None
+        k_stage, v_stage = to_dev(d.B.device_array), to_dev(d.V.device_array)
+        k_land, v_land = k_stage.clone(), v_stage.clone()
+        c = torch.empty((w.M, e["heads"], e["head_dim"]), dtype=torch.int16, device=dev)
+        lse = torch.empty((e["heads"], w.M), dtype=torch.float32, device=dev)
+        outgoing = None
+        moved_bytes = 2 * remote_rows * e["kv_heads"] * e["head_dim"] * 2
+    elif w.op == "ar":
         # reduce-scatter sends and all-gather arrivals of the non-local chunks, the other
         # ranks' partials of the own shard, and the sends of the reduced own chunks
         landing = None
@@ -122,7 +136,9 @@ def main():
 
     def call(mode, p=None):
         p = p or plan
-        if w.op == "ar":
+        if w.op == "attn":
+            p.ring_attn(a_full, k_land, v_land, k_stage, v_stage, c, lse, mode, compute, copy)
+        elif w.op == "ar":
             p.gemm_ar(a_full, b, c, outgoing, p_stage, p_land, reduced, mode, compute, copy)
         elif w.op == "rs":
             p.gemm_rs(a_full, b, c, outgoing, mode, compute, copy)
@@ -221,14 +237,15 @@ def main():
         "overlap_eff_isolated": round(overlap_eff_isolated, 4),
         "roofline": {"bound": "mfma", "achieved": round(w.flops / (k_overlap * 1e-3) / 1e12, 2), "peak": peak,
                      "unit": "TFLOP/s", "frac": round(w.flops / (k_overlap * 1e-3) / 1e12 / peak, 4),
-                     "traffic": kernel_traffic(w.name), "kernel": "chunk_gemm", "phase": "overlap (timed region)",
+                     "traffic": kernel_traffic(w.name), "kernel": "ring_attn" if w.op == "attn" else "chunk_gemm",
+                     "phase": "overlap (timed region)",
                      "kernel_ms_mean": round(k_overlap, 4)},
         "roofline_compute_only": {"bound": "mfma", "achieved": round(w.flops / (k_comp * 1e-3) / 1e12, 2),
                                   "peak": peak, "unit": "TFLOP/s",
                                   "frac": round(w.flops / (k_comp * 1e-3) / 1e12 / peak, 4),
                                   "kernel_ms_mean": round(k_comp, 4)},
     }
-    if not args.no_kernel_copies and w.op != "ar":  # GEMM + all-reduce copies with the engines only
+    if not args.no_kernel_copies and w.op not in ("ar", "attn"):  # these copy with the engines only
         rec["kernel_copy_backend"] = kernel_copy_sweep(w, sched, group_rows, d, timed_loop, moved_bytes, args)
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(w, d, chunks, args.cpu_seconds)
@@ -301,6 +318,29 @@ def cpu_baseline(w, d, chunks, target_s):
         rows_all.extend(range(ch[0], ch[1]))
     B = d.B.device_array
     A = d.A.device_array
+
+    if w.op == "attn":
+        # queries of the first rows, all heads, against every key (fp64 plain attention)
+        Q, K, V = d.A.values, d.B.values, d.V.values
+        e = w.extras
+        n = 8
+        t0 = time.perf_counter()
+        oracle.attention(Q[:n], K, V)
+        t = time.perf_counter() - t0
+        n = int(min(w.M, max(n, n * target_s / max(t, 1e-6))))
+        t0 = time.perf_counter()
+        oracle.attention(Q[:n], K, V)
+        t = time.perf_counter() - t0
+        flops = 4.0 * n * K.shape[0] * e["head_dim"] * e["heads"]
+        try:  # numpy's products run on its BLAS thread pool
+            from threadpoolctl import threadpool_info
+            cores = max(int(i.get("num_threads", 1)) for i in threadpool_info() if i.get("user_api") == "blas")
+        except Exception:
+            cores = 1
+        return {"value": round(flops / t / 1e12, 6), "unit": "TFLOP/s", "cores": cores,
+                "kind": "oracle", "seconds": round(t, 3),
+                "sample": "%d of %d query rows, all %d heads, all %d keys, fp64 numpy attention"
+                          % (n, w.M, e["heads"], K.shape[0])}
 
     def run(rows):
         t0 = time.perf_counter()
