@@ -46,6 +46,7 @@ constexpr int KP = D + 8;             // K tile row pitch (elements): 272 bytes
 constexpr int VP = BKV + 4;           // V^T tile row pitch (elements): 136 bytes
 constexpr int kMaxAttnChunks = 4096;  // per-workgroup ready cache: one bit per chunk
 constexpr float kLn2 = 0.6931471805599453f;
+constexpr float kRescaleSlack = 8.0f;  // log2 of the largest weight before a rescale
 
 static_assert(BQ == 32 * (kThreads / 64), "one wave per 32 query rows");
 
@@ -85,9 +86,10 @@ __device__ int wait_chunk(const AttnArgs& a, int c, int unit, uint32_t* ready_bi
 }
 
 // One block of 64 keys (and values) of key/value head g, starting at key row kv0, into
-// registers: K as 16-byte row pieces (16 consecutive lanes per row, coalesced), V as
-// 16-byte pieces taken key-major (consecutive lanes, consecutive keys) so that the
-// transposing LDS stores of a wave fall on consecutive addresses.
+// registers: K as 16-byte row pieces (16 consecutive lanes per row, coalesced); V as
+// 16-byte pieces of two adjacent keys (key pair tid % 32, head dims 8 (tid / 32) + 64 j),
+// so that the transposing LDS stores write both keys of a head dim in one 4-byte store
+// and a wave's stores fall on consecutive addresses.
 __device__ __forceinline__ void load_kv(const AttnArgs& a, int g, int kv0, int tid, u32x4_t (&kr)[4],
                                         u32x4_t (&vr)[4]) {
 #pragma unroll
@@ -95,9 +97,16 @@ __device__ __forceinline__ void load_kv(const AttnArgs& a, int g, int kv0, int t
     const int p = tid + kThreads * i;
     const int krow = p >> 4, kcol = (p & 15) * 8;
     kr[i] = *reinterpret_cast<const u32x4_t*>(a.K + (static_cast<int64_t>(kv0 + krow) * a.Hkv + g) * D + kcol);
-    const int vkey = p & 63, vcol = (p >> 6) * 8;
-    vr[i] = *reinterpret_cast<const u32x4_t*>(a.V + (static_cast<int64_t>(kv0 + vkey) * a.Hkv + g) * D + vcol);
   }
+  const int key = 2 * (tid & 31);
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const int vcol = ((tid >> 5) + 8 * j) * 8;
+      vr[2 * j + t] =
+          *reinterpret_cast<const u32x4_t*>(a.V + (static_cast<int64_t>(kv0 + key + t) * a.Hkv + g) * D + vcol);
+    }
 }
 
 __device__ __forceinline__ void store_kv(uint16_t* sK, uint16_t* sVT, int tid, const u32x4_t (&kr)[4],
@@ -106,13 +115,32 @@ __device__ __forceinline__ void store_kv(uint16_t* sK, uint16_t* sVT, int tid, c
   for (int i = 0; i < 4; ++i) {
     const int p = tid + kThreads * i;
     *reinterpret_cast<u32x4_t*>(sK + (p >> 4) * KP + (p & 15) * 8) = kr[i];
-    const int vkey = p & 63, vcol = (p >> 6) * 8;
+  }
+  const int key = 2 * (tid & 31);
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int vcol = ((tid >> 5) + 8 * j) * 8;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const uint32_t w = vr[i][e >> 1];
-      sVT[(vcol + e) * VP + vkey] = static_cast<uint16_t>((e & 1) ? (w >> 16) : (w & 0xffffu));
+      // head dim vcol + e of keys key and key + 1
+      const uint32_t lo = (vr[2 * j][e >> 1] >> ((e & 1) * 16)) & 0xffffu;
+      const uint32_t hi = (vr[2 * j + 1][e >> 1] >> ((e & 1) * 16)) & 0xffffu;
+      *reinterpret_cast<uint32_t*>(sVT + (vcol + e) * VP + key) = lo | (hi << 16);
     }
   }
+}
+
+// The value of lane ^ 32 of a wave (the other half of a query row's keys), by
+// v_permlane32_swap: swapping the halves of two copies of x leaves each lane holding x of
+// itself and of lane ^ 32, one in each copy, so their combination is symmetric in the
+// two lanes without an LDS round trip.
+__device__ __forceinline__ float max_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
 }  // namespace
@@ -207,30 +235,33 @@ __global__ __launch_bounds__(kThreads, 2) void ring_attn(AttnArgs a) {
             sc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], sc[kb], 0, 0, 0);
           }
 
-        // online softmax: this lane holds 32 of the row's 64 scores, lane ^ 32 the rest
+        // online softmax: this lane holds 32 of the row's 64 scores, lane ^ 32 the rest.
+        // The weights are exp2(scale_log2 s - m), m a reference that only moves when the
+        // row's scaled maximum exceeds it by more than kRescaleSlack (so weights stay
+        // below 2^kRescaleSlack): most blocks leave the accumulators unscaled. Both
+        // lanes of a row see the same maximum, so they keep the same reference.
         float mx = -__builtin_inff();
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            sc[kb][r] *= a.scale_log2;
-            mx = fmaxf(mx, sc[kb][r]);
-          }
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float m_new = fmaxf(m, mx);
-        const float alpha = __builtin_amdgcn_exp2f(m - m_new);
+          for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[kb][r]);
+        mx = max_halves(mx) * a.scale_log2;  // the scale is positive
+        if (mx > m + kRescaleSlack) {
+          const float alpha = __builtin_amdgcn_exp2f(m - mx);  // 0 on the first block
+          l *= alpha;
+#pragma unroll
+          for (int db = 0; db < D / 32; ++db) acc[db] *= alpha;
+          m = mx;
+        }
         float psum = 0.0f;
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            sc[kb][r] = __builtin_amdgcn_exp2f(sc[kb][r] - m_new);
+            sc[kb][r] = __builtin_amdgcn_exp2f(fmaf(sc[kb][r], a.scale_log2, -m));
             psum += sc[kb][r];
           }
-        l = l * alpha + psum;
-        m = m_new;
-#pragma unroll
-        for (int db = 0; db < D / 32; ++db) acc[db] *= alpha;
+        l += psum;
 
         // P^T as the second operand, 4 steps of 16 keys: step t takes registers
         // 8 (t % 2) .. + 7 of tile t / 2, which hold keys (t / 2) 32 + (t % 2) 16 +
@@ -271,7 +302,7 @@ __global__ __launch_bounds__(kThreads, 2) void ring_attn(AttnArgs a) {
 
     // O = acc / l over the whole row (both lanes' keys); each lane holds 16 head dims of
     // its row per 32-dim tile, in runs of four
-    const float l_tot = l + __shfl_xor(l, 32);
+    const float l_tot = sum_halves(l);
     const float inv = 1.0f / l_tot;
     if (q_ok) {
       uint16_t* orow = a.O + (static_cast<int64_t>(q_row) * a.H + h) * D;
