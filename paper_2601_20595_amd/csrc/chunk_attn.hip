@@ -37,13 +37,18 @@ typedef float f32x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+typedef short i16x8_t __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+typedef __attribute__((address_space(3))) unsigned char lds_u8_t;
+typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
 
 constexpr int D = kAttnHeadDim;
 constexpr int BQ = kAttnBlockQ;
 constexpr int BKV = kAttnBlockKV;
 constexpr int kThreads = 256;         // 4 waves x 32 query rows
-constexpr int KP = D + 8;             // K tile row pitch (elements): 272 bytes
-constexpr int VP = BKV + 4;           // V^T tile row pitch (elements): 136 bytes
+constexpr int kTileBytes = BKV * D * 2;   // one K or V tile: 16 KiB
+constexpr int kBufferDword3 = 0x00020000;  // raw buffer resource word 3 (gfx9 family)
 constexpr int kMaxAttnChunks = 4096;  // per-workgroup ready cache: one bit per chunk
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kRescaleSlack = 8.0f;  // log2 of the largest weight before a rescale
@@ -85,50 +90,71 @@ __device__ int wait_chunk(const AttnArgs& a, int c, int unit, uint32_t* ready_bi
   return 1;
 }
 
-// One block of 64 keys (and values) of key/value head g, starting at key row kv0, into
-// registers: K as 16-byte row pieces (16 consecutive lanes per row, coalesced); V as
-// 16-byte pieces of two adjacent keys (key pair tid % 32, head dims 8 (tid / 32) + 64 j),
-// so that the transposing LDS stores write both keys of a head dim in one 4-byte store
-// and a wave's stores fall on consecutive addresses.
-__device__ __forceinline__ void load_kv(const AttnArgs& a, int g, int kv0, int tid, u32x4_t (&kr)[4],
-                                        u32x4_t (&vr)[4]) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int p = tid + kThreads * i;
-    const int krow = p >> 4, kcol = (p & 15) * 8;
-    kr[i] = *reinterpret_cast<const u32x4_t*>(a.K + (static_cast<int64_t>(kv0 + krow) * a.Hkv + g) * D + kcol);
-  }
-  const int key = 2 * (tid & 31);
-#pragma unroll
-  for (int j = 0; j < 2; ++j)
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      const int vcol = ((tid >> 5) + 8 * j) * 8;
-      vr[2 * j + t] =
-          *reinterpret_cast<const u32x4_t*>(a.V + (static_cast<int64_t>(kv0 + key + t) * a.Hkv + g) * D + vcol);
-    }
+// K tile layout in LDS. Key row R (0..63) of the block has 16 pieces of 16 bytes (8
+// head dims each); logical piece p sits in 16-byte slot
+//     256 (p / 4) + 4 R + ((p % 4) ^ f(R)),   f(R) = ((R >> 2) ^ (R >> 1)) & 3.
+// One DMA instruction fills 64 consecutive slots, i.e. one group of four pieces for 16
+// rows, reading 64 contiguous bytes per row. A fragment read (16 consecutive rows, one
+// logical piece) touches 16 distinct 16-byte bank groups, and any 8 aligned consecutive
+// rows 8 distinct ones, so it is free of conflicts with 32 or 64 banks; and the slot's
+// dependence on the piece index is an additive constant plus a bit that only depends on
+// the piece's parity, so fragment reads use immediate offsets.
+__device__ __forceinline__ int k_swz(int r) { return ((r >> 2) ^ (r >> 1)) & 3; }
+
+// Buffer resource over [base, base + bytes) (bytes < 2^31), built from workgroup-
+// uniform values so that it lives in SGPRs.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int bytes) {
+  const uint64_t p = reinterpret_cast<uint64_t>(base);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(p));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(p >> 32));
+  void* ub = reinterpret_cast<void*>((static_cast<uint64_t>(hi) << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(ub, 0, __builtin_amdgcn_readfirstlane(bytes), kBufferDword3);
 }
 
-__device__ __forceinline__ void store_kv(uint16_t* sK, uint16_t* sVT, int tid, const u32x4_t (&kr)[4],
-                                         const u32x4_t (&vr)[4]) {
+// V tile layout in LDS: row-major, key row R (0..63) of 256 bytes, in which the 32-byte
+// unit u (head dims 16 u .. + 15) sits at unit u ^ s(R % 4), s(q) = 2 q + q / 2. The
+// value product reads V^T fragments with ds_read_b64_tr_b16, which transposes 4 x 16
+// blocks among each 16 lanes: lane j of the 16 supplies the address of 4 consecutive
+// elements, and lane i receives element i % 4 of lane 4 e + i / 4 as its element e.
+// With lane j pointing at key k0 + j / 4, head dims d0 + 4 (j % 4), lane i receives
+// head dim d0 + i of keys k0 .. k0 + 3. One such read touches 4 consecutive keys (R % 4
+// = 0..3) x 16 or 32 dims, which the swizzle spreads over distinct bank groups with 32
+// or 64 banks; the DMA writes rows contiguously as the K tile's does.
+__device__ __forceinline__ int v_swz(int q) { return 2 * q + (q >> 1); }
+
+// One 64-row block of key/value head g (rows [kv0, kv0 + 64) of the [rows][Hkv][D]
+// array src) into a K or V tile at LDS byte address lds_tile, by LDS DMA: wave w fills
+// LDS bytes 4096 w .. + 4095 with four 16-byte-per-lane loads of 1 KiB each. The tile
+// layouts make the lane's source offset voff0 plus q times a fixed step (step_bytes):
+// for K, instruction q covers rows 16 q .. + 15 (piece group w); for V, rows 16 w +
+// 4 q .. + 3. The whole offset sits in the VGPR operand, which the buffer range check
+// covers; the resource spans exactly the block's 64 rows of head g. Issued as inline asm
+// (M0 saved and restored) so that the compiler does not wait for it before every LDS
+// read: completion is waited for explicitly (wait_vm_all) before the barrier that
+// publishes the tile.
+__device__ __forceinline__ void dma_tile(const uint16_t* src, int hkv, int g, int kv0, uint32_t lds_tile, int wave,
+                                         int voff0, int step_bytes) {
+  const int64_t row = static_cast<int64_t>(hkv) * D;  // elements between consecutive keys
+  const __amdgpu_buffer_rsrc_t rs = make_rsrc(src + static_cast<int64_t>(kv0) * row + static_cast<int64_t>(g) * D,
+                                              static_cast<int>(((BKV - 1) * row + D) * 2));
+  const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_tile + 4096u * static_cast<uint32_t>(wave));
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int p = tid + kThreads * i;
-    *reinterpret_cast<u32x4_t*>(sK + (p >> 4) * KP + (p & 15) * 8) = kr[i];
-  }
-  const int key = 2 * (tid & 31);
-#pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int vcol = ((tid >> 5) + 8 * j) * 8;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      // head dim vcol + e of keys key and key + 1
-      const uint32_t lo = (vr[2 * j][e >> 1] >> ((e & 1) * 16)) & 0xffffu;
-      const uint32_t hi = (vr[2 * j + 1][e >> 1] >> ((e & 1) * 16)) & 0xffffu;
-      *reinterpret_cast<uint32_t*>(sVT + (vcol + e) * VP + key) = lo | (hi << 16);
-    }
+  for (int q = 0; q < 4; ++q) {
+    uint32_t saved;
+    int voff;
+    asm volatile(
+        "v_add_u32 %1, %3, %4\n\t"
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %2\n\t"
+        "buffer_load_dwordx4 %1, %5, 0 offen lds\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved), "=&v"(voff)
+        : "s"(lds0 + 1024u * q), "s"(q * step_bytes), "v"(voff0), "s"(rs)
+        : "memory");
   }
 }
+
+__device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // The value of lane ^ 32 of a wave (the other half of a query row's keys), by
 // v_permlane32_swap: swapping the halves of two copies of x leaves each lane holding x of
@@ -143,11 +169,90 @@ __device__ __forceinline__ float sum_halves(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// S^T of one block of 64 keys (two 32-key tiles) for the wave's 32 query rows: lane
+// (l32, hlf) ends with the scores of query row l32 against keys 32 kb + 8 (r / 4) +
+// 4 hlf + r % 4 in sc[kb][r]. The lane's first operand is row 32 kb + l32, piece
+// 2 s + hlf of the K tile: byte 4096 (s / 2) + 2048 kb + 64 l32 + 16 ((2 (s % 2) + hlf)
+// ^ f(l32)); kEven / kOdd are the lane's part of it for even and odd s.
+__device__ __forceinline__ void score_block(const unsigned char* kEven, const unsigned char* kOdd,
+                                            const bf16x8_t (&qf)[D / 16], f32x16_t (&sc)[2]) {
+  sc[0] = f32x16_t{};
+  sc[1] = f32x16_t{};
+#pragma unroll
+  for (int s = 0; s < D / 16; ++s)
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      const unsigned char* p = ((s & 1) ? kOdd : kEven) + 4096 * (s >> 1) + 2048 * kb;
+      const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(p);
+      sc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], sc[kb], 0, 0, 0);
+    }
+}
+
+// Online softmax of one block, branch-free. The weights are exp2(scale_log2 s - m), m a
+// reference that only moves when the row's scaled maximum exceeds it by more than
+// kRescaleSlack (so weights stay below 2^kRescaleSlack); both lanes of a row see the
+// same maximum and keep the same reference. Returns whether the reference moved: then
+// the accumulators are to be multiplied by alpha (0 on a unit's first block). The
+// weights leave as bf16 in the second-operand order of the value product: step t takes
+// registers 8 (t % 2) .. + 7 of tile t / 2, keys (t / 2) 32 + (t % 2) 16 +
+// {4 hlf + 0..3, 8 + 4 hlf + 0..3}.
+__device__ __forceinline__ bool softmax_block(const f32x16_t (&sc)[2], float scale_log2, float& m, float& l,
+                                              float& alpha, bf16x8_t (&pb)[4]) {
+  float mx = -__builtin_inff();
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[kb][r]);
+  mx = max_halves(mx) * scale_log2;  // the scale is positive
+  const bool grow = mx > m + kRescaleSlack;
+  const float m_new = grow ? mx : m;
+  alpha = __builtin_amdgcn_exp2f(m - m_new);
+  m = m_new;
+  float psum = 0.0f;
+  float w[2][16];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      w[kb][r] = __builtin_amdgcn_exp2f(fmaf(sc[kb][r], scale_log2, -m_new));
+      psum += w[kb][r];
+    }
+  l = l * alpha + psum;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const float* v = &w[t >> 1][8 * (t & 1)];
+    pb[t] = __builtin_convertvector((f32x8_t{v[0], v[1], v[2], v[3], v[4], v[5], v[6], v[7]}), bf16x8_t);
+  }
+  return grow;
+}
+
+// O^T += V^T . P^T for one block. The first operand of step t, head-dim tile db, is
+// V^T rows 32 db + l32, keys in pb[t]'s order: two transposing reads of 4 keys each
+// (keys (t / 2) 32 + (t % 2) 16 + 4 hlf + 0..3, then + 8). vt is the V tile; v_lane[db]
+// is the lane's byte offset in it for keys 4 hlf + (lane % 16) / 4 and head dims
+// 32 db + 16 ((lane / 16) % 2) + 4 (lane % 4); a block of 8 keys is 2048 bytes.
+__device__ __forceinline__ void value_block(const lds_u8_t* vt, const int (&v_lane)[D / 32], const bf16x8_t (&pb)[4],
+                                            f32x16_t (&acc)[D / 32]) {
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+      const lds_u8_t* p = vt + v_lane[db] + 256 * (32 * (t >> 1) + 16 * (t & 1));
+      const i16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(p));
+      const i16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(p + 2048));
+      const bf16x8_t vf = __builtin_bit_cast(
+          bf16x8_t, (i16x8_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]}));
+      acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[t], acc[db], 0, 0, 0);
+    }
+  }
+}
+
 }  // namespace
 
 __global__ __launch_bounds__(kThreads, 2) void ring_attn(AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t sK[BKV * KP];
-  __shared__ __attribute__((aligned(16))) uint16_t sVT[D * VP];
+  // K and V tiles, double-buffered
+  __shared__ __attribute__((aligned(1024))) unsigned char sK[2 * kTileBytes];
+  __shared__ __attribute__((aligned(1024))) unsigned char sV[2 * kTileBytes];
   __shared__ uint32_t ready_bits[kMaxAttnChunks / 32];
   __shared__ int s_unit;
   __shared__ int s_state;
@@ -155,6 +260,29 @@ __global__ __launch_bounds__(kThreads, 2) void ring_attn(AttnArgs a) {
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, hlf = lane >> 5;
+  // K tile: this lane's DMA source offset (row L / 4, piece 4 wave + ((L % 4) ^ f(row)),
+  // 16 rows further per instruction) and its fragment-read offsets for even and odd
+  // pieces. V tile: DMA source offset (row 16 wave + L / 16, unit ((L % 16) / 2) ^
+  // s(row % 4), half L % 2; 4 rows further per instruction) and transposing-read
+  // offsets per head-dim tile.
+  const int key_bytes = a.Hkv * D * 2;
+  const int k_voff0 = (lane >> 2) * key_bytes + (4 * wave + ((lane & 3) ^ k_swz(lane >> 2))) * 16;
+  const int v_voff0 = (16 * wave + (lane >> 4)) * key_bytes + ((((lane & 15) >> 1) ^ v_swz(lane >> 4)) * 32) +
+                      (lane & 1) * 16;
+  const uint32_t sK_addr =
+      __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_ptr_t)sK)));
+  const uint32_t sV_addr =
+      __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_ptr_t)sV)));
+  const int k_even = 64 * l32 + 16 * (hlf ^ k_swz(l32));
+  const int k_odd = 64 * l32 + 16 * ((2 + hlf) ^ k_swz(l32));
+  int v_lane[D / 32];
+  {
+    const int i = lane & 15, h = (lane >> 4) & 1;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+      v_lane[db] = 256 * ((i >> 2) + 4 * hlf) + 32 * ((2 * db + h) ^ v_swz(i >> 2)) + 8 * (i & 3);
+  }
+  const lds_u8_t* sV_lds = (const lds_u8_t*)(sV);
   if (blockIdx.x == 0 && a.next_ticket) {
     // clear the next call's state set (its prologue, folded into this kernel)
     for (int c = tid; c < a.n_chunks; c += kThreads) a.next_counters[c] = 0u;
@@ -217,80 +345,55 @@ __global__ __launch_bounds__(kThreads, 2) void ring_attn(AttnArgs a) {
         aborted = true;
         break;
       }
+      // Blocks j = 0 .. nb - 1 of the chunk, software-pipelined by one block: while the
+      // matrix cores compute the scores of block j + 1, the vector unit computes the
+      // softmax of block j (the two are independent). Tiles are DMA'd into LDS a step
+      // ahead of use (K of block j + 2 and V of block j + 1 during step j) into double
+      // buffers (K of block j in buffer j % 2, V likewise), so one barrier per block
+      // publishes the step's tiles and frees the previous step's.
       const int r0 = a.chunk_rows[2 * c], r1 = a.chunk_rows[2 * c + 1];
-      u32x4_t kr[4], vr[4];
-      load_kv(a, g, r0, tid, kr, vr);
-      for (int kv0 = r0; kv0 < r1; kv0 += BKV) {
-        store_kv(sK, sVT, tid, kr, vr);
+      const int nb = (r1 - r0) / BKV;
+      if (nb > 0) {
+        dma_tile(a.K, a.Hkv, g, r0, sK_addr, wave, k_voff0, 16 * key_bytes);
+        dma_tile(a.V, a.Hkv, g, r0, sV_addr, wave, v_voff0, 4 * key_bytes);
+        if (nb > 1) dma_tile(a.K, a.Hkv, g, r0 + BKV, sK_addr + kTileBytes, wave, k_voff0, 16 * key_bytes);
+        wait_vm_all();
         __syncthreads();
-        if (kv0 + BKV < r1) load_kv(a, g, kv0 + BKV, tid, kr, vr);  // next block, while this one computes
-
-        // S^T for this block: two 32-key tiles, this wave's 32 query rows
-        f32x16_t sc[2] = {f32x16_t{}, f32x16_t{}};
+        f32x16_t sc[2];
+        score_block(sK + k_even, sK + k_odd, qf, sc);
+        for (int j = 0; j < nb; ++j) {
+          const int kv0 = r0 + j * BKV;
+          const int buf = j & 1, nbuf = buf ^ 1;
+          wait_vm_all();    // this wave's parts of V j and K j + 1 have landed
+          __syncthreads();  // ... everyone's; and everyone is done with K j and V j - 1
+          if (j + 2 < nb)
+            dma_tile(a.K, a.Hkv, g, kv0 + 2 * BKV, sK_addr + buf * kTileBytes, wave, k_voff0, 16 * key_bytes);
+          if (j + 1 < nb)
+            dma_tile(a.V, a.Hkv, g, kv0 + BKV, sV_addr + nbuf * kTileBytes, wave, v_voff0, 4 * key_bytes);
+          // scores of block j + 1 (on the chunk's last block, of whatever the other
+          // buffer holds: computed and discarded, which keeps this code branch-free so
+          // that the compiler can interleave the two independent streams)
+          f32x16_t sn[2];
+          score_block(sK + nbuf * kTileBytes + k_even, sK + nbuf * kTileBytes + k_odd, qf, sn);
+          float alpha;
+          bf16x8_t pb[4];
+          const bool grow = softmax_block(sc, a.scale_log2, m, l, alpha, pb);
+          // the weights are complete here, ahead of the rescale branch, so that their
+          // exponentials stay in the same basic block as the score products
+          asm volatile("" : "+v"(pb[0]), "+v"(pb[1]), "+v"(pb[2]), "+v"(pb[3]));
+          sc[0] = sn[0];
+          sc[1] = sn[1];
+          if (grow) {
 #pragma unroll
-        for (int s = 0; s < D / 16; ++s)
-#pragma unroll
-          for (int kb = 0; kb < 2; ++kb) {
-            const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(sK + (32 * kb + l32) * KP + 16 * s + 8 * hlf);
-            sc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], sc[kb], 0, 0, 0);
+            for (int db = 0; db < D / 32; ++db) acc[db] *= alpha;
           }
-
-        // online softmax: this lane holds 32 of the row's 64 scores, lane ^ 32 the rest.
-        // The weights are exp2(scale_log2 s - m), m a reference that only moves when the
-        // row's scaled maximum exceeds it by more than kRescaleSlack (so weights stay
-        // below 2^kRescaleSlack): most blocks leave the accumulators unscaled. Both
-        // lanes of a row see the same maximum, so they keep the same reference.
-        float mx = -__builtin_inff();
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[kb][r]);
-        mx = max_halves(mx) * a.scale_log2;  // the scale is positive
-        if (mx > m + kRescaleSlack) {
-          const float alpha = __builtin_amdgcn_exp2f(m - mx);  // 0 on the first block
-          l *= alpha;
-#pragma unroll
-          for (int db = 0; db < D / 32; ++db) acc[db] *= alpha;
-          m = mx;
+          value_block(sV_lds + buf * kTileBytes, v_lane, pb, acc);
         }
-        float psum = 0.0f;
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            sc[kb][r] = __builtin_amdgcn_exp2f(fmaf(sc[kb][r], a.scale_log2, -m));
-            psum += sc[kb][r];
-          }
-        l += psum;
-
-        // P^T as the second operand, 4 steps of 16 keys: step t takes registers
-        // 8 (t % 2) .. + 7 of tile t / 2, which hold keys (t / 2) 32 + (t % 2) 16 +
-        // {4 hlf + 0..3, 8 + 4 hlf + 0..3}
-        bf16x8_t pb[4];
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          const f32x8_t v{sc[t >> 1][8 * (t & 1) + 0], sc[t >> 1][8 * (t & 1) + 1], sc[t >> 1][8 * (t & 1) + 2],
-                          sc[t >> 1][8 * (t & 1) + 3], sc[t >> 1][8 * (t & 1) + 4], sc[t >> 1][8 * (t & 1) + 5],
-                          sc[t >> 1][8 * (t & 1) + 6], sc[t >> 1][8 * (t & 1) + 7]};
-          pb[t] = __builtin_convertvector(v, bf16x8_t);
-        }
-        // O^T += V^T . P^T, V^T rows read in the same key order
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          const int kvb = 32 * (t >> 1) + 16 * (t & 1) + 4 * hlf;
-#pragma unroll
-          for (int db = 0; db < D / 32; ++db) {
-            const uint16_t* vrow = sVT + (32 * db + l32) * VP + kvb;
-            const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(vrow);
-            const u32x2_t hi = *reinterpret_cast<const u32x2_t*>(vrow + 8);
-            const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, u32x4_t{lo[0], lo[1], hi[0], hi[1]});
-            acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[t], acc[db], 0, 0, 0);
-          }
-        }
-        __syncthreads();  // this block's LDS reads are done before the next block's stores
       }
-      // every load of this chunk by this workgroup has landed (each block's loads are
-      // waited for before its LDS stores, and all threads passed the barrier above)
+      // every load of this chunk's rows that the workgroup uses has landed (each block's
+      // loads are waited for before its LDS stores, and every thread has passed the
+      // barrier after the chunk's last stores); prefetches still in flight re-read the
+      // chunk's last block and are discarded
       if (tid == 0) {
         const uint32_t done =
             __hip_atomic_fetch_add(a.counters + c, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) + 1u;
