@@ -39,6 +39,7 @@ typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
 typedef short i16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 typedef __attribute__((address_space(3))) unsigned char lds_u8_t;
 typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
@@ -49,9 +50,12 @@ constexpr int BKV = kAttnBlockKV;
 constexpr int kThreads = 256;         // 4 waves x 32 query rows
 constexpr int kTileBytes = BKV * D * 2;   // one K or V tile: 16 KiB
 constexpr int kBufferDword3 = 0x00020000;  // raw buffer resource word 3 (gfx9 family)
+__device__ const bf16x2_t kBf16Ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
 constexpr int kMaxAttnChunks = 4096;  // per-workgroup ready cache: one bit per chunk
 constexpr float kLn2 = 0.6931471805599453f;
-constexpr float kRescaleSlack = 8.0f;  // log2 of the largest weight before a rescale
+// Largest row sum of one block's weights accepted against the running reference; a
+// larger (or non-finite) sum moves the reference to the row's maximum instead.
+constexpr float kRowSumLimit = 65536.0f;
 
 static_assert(BQ == 32 * (kThreads / 64), "one wave per 32 query rows");
 
@@ -188,42 +192,59 @@ __device__ __forceinline__ void score_block(const unsigned char* kEven, const un
     }
 }
 
-// Online softmax of one block, branch-free. The weights are exp2(scale_log2 s - m), m a
-// reference that only moves when the row's scaled maximum exceeds it by more than
-// kRescaleSlack (so weights stay below 2^kRescaleSlack); both lanes of a row see the
-// same maximum and keep the same reference. Returns whether the reference moved: then
-// the accumulators are to be multiplied by alpha (0 on a unit's first block). The
-// weights leave as bf16 in the second-operand order of the value product: step t takes
-// registers 8 (t % 2) .. + 7 of tile t / 2, keys (t / 2) 32 + (t % 2) 16 +
-// {4 hlf + 0..3, 8 + 4 hlf + 0..3}.
-__device__ __forceinline__ bool softmax_block(const f32x16_t (&sc)[2], float scale_log2, float& m, float& l,
-                                              float& alpha, bf16x8_t (&pb)[4]) {
-  float mx = -__builtin_inff();
-#pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[kb][r]);
-  mx = max_halves(mx) * scale_log2;  // the scale is positive
-  const bool grow = mx > m + kRescaleSlack;
-  const float m_new = grow ? mx : m;
-  alpha = __builtin_amdgcn_exp2f(m - m_new);
-  m = m_new;
+// Weights of one block against the reference m: exp2(scale_log2 s - m), packed to bf16
+// in the second-operand order of the value product (step t takes registers
+// 8 (t % 2) .. + 7 of tile t / 2, keys (t / 2) 32 + (t % 2) 16 + {4 hlf + 0..3,
+// 8 + 4 hlf + 0..3}). Returns this lane's sum of the packed (bf16) weights, so that the
+// normaliser adds up exactly the weights that the value product multiplies.
+__device__ __forceinline__ float block_weights(const f32x16_t (&sc)[2], float scale_log2, float m,
+                                               bf16x8_t (&pb)[4]) {
   float psum = 0.0f;
-  float w[2][16];
-#pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      w[kb][r] = __builtin_amdgcn_exp2f(fmaf(sc[kb][r], scale_log2, -m_new));
-      psum += w[kb][r];
-    }
-  l = l * alpha + psum;
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
-    const float* v = &w[t >> 1][8 * (t & 1)];
-    pb[t] = __builtin_convertvector((f32x8_t{v[0], v[1], v[2], v[3], v[4], v[5], v[6], v[7]}), bf16x8_t);
+    const int kb = t >> 1, o = 8 * (t & 1);
+    f32x8_t w;
+#pragma unroll
+    for (int r = 0; r < 8; ++r) w[r] = __builtin_amdgcn_exp2f(fmaf(sc[kb][o + r], scale_log2, -m));
+    pb[t] = __builtin_convertvector(w, bf16x8_t);
+    const bf16x2_t* pairs = reinterpret_cast<const bf16x2_t*>(&pb[t]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) psum = __builtin_amdgcn_fdot2_f32_bf16(pairs[i], kBf16Ones, psum, false);
   }
-  return grow;
+  return psum;
+}
+
+// Online softmax of one block. The running reference m of a query row moves only when
+// it must: the block's weights are first taken against the current m, and only if the
+// row's sum of them exceeds kRowSumLimit (or is not finite, as on a unit's first block,
+// where m is -inf) does m move to the row's maximum scaled score, with the weights
+// recomputed and the running sums rescaled. Both lanes of a row (lane and lane ^ 32)
+// see the same row sum and the same maximum, so they keep the same m. The rare path is
+// taken by the whole wave (with unchanged m on rows that do not need it), so its
+// cross-lane exchange runs with every lane active. Returns the factor by which the
+// accumulators are to be multiplied (1: unchanged); l is this lane's partial sum.
+__device__ __forceinline__ float softmax_block(const f32x16_t (&sc)[2], float scale_log2, float& m, float& l,
+                                               bf16x8_t (&pb)[4], bool& rescale) {
+  float psum = block_weights(sc, scale_log2, m, pb);
+  const float row = sum_halves(psum);
+  const bool move = !(row <= kRowSumLimit);
+  float alpha = 1.0f;
+  rescale = __builtin_amdgcn_ballot_w64(move) != 0;
+  if (rescale) {
+    float mx = -__builtin_inff();
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[kb][r]);
+    mx = max_halves(mx) * scale_log2;  // the scale is positive
+    const float m_new = move ? fmaxf(m, mx) : m;
+    alpha = __builtin_amdgcn_exp2f(m - m_new);  // 0 on a unit's first block, 1 on unmoved rows
+    m = m_new;
+    l *= alpha;
+    psum = block_weights(sc, scale_log2, m, pb);
+  }
+  l += psum;
+  return alpha;
 }
 
 // O^T += V^T . P^T for one block. The first operand of step t, head-dim tile db, is
@@ -233,17 +254,23 @@ __device__ __forceinline__ bool softmax_block(const f32x16_t (&sc)[2], float sca
 // 32 db + 16 ((lane / 16) % 2) + 4 (lane % 4); a block of 8 keys is 2048 bytes.
 __device__ __forceinline__ void value_block(const lds_u8_t* vt, const int (&v_lane)[D / 32], const bf16x8_t (&pb)[4],
                                             f32x16_t (&acc)[D / 32]) {
-#pragma unroll
-  for (int t = 0; t < 4; ++t) {
+  bf16x8_t vf[2][D / 32];  // fragments of steps t and t + 1: the reads run a step ahead
+  auto load = [&](bf16x8_t (&f)[D / 32], int t) {
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) {
       const lds_u8_t* p = vt + v_lane[db] + 256 * (32 * (t >> 1) + 16 * (t & 1));
       const i16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(p));
       const i16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(p + 2048));
-      const bf16x8_t vf = __builtin_bit_cast(
-          bf16x8_t, (i16x8_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]}));
-      acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[t], acc[db], 0, 0, 0);
+      f[db] = __builtin_bit_cast(bf16x8_t, (i16x8_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]}));
     }
+  };
+  load(vf[0], 0);
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    if (t + 1 < 4) load(vf[(t + 1) & 1], t + 1);
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+      acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[t & 1][db], pb[t], acc[db], 0, 0, 0);
   }
 }
 
@@ -359,9 +386,10 @@ __global__ __launch_bounds__(kThreads, 2) void ring_attn(AttnArgs a) {
         if (nb > 1) dma_tile(a.K, a.Hkv, g, r0 + BKV, sK_addr + kTileBytes, wave, k_voff0, 16 * key_bytes);
         wait_vm_all();
         __syncthreads();
-        f32x16_t sc[2];
-        score_block(sK + k_even, sK + k_odd, qf, sc);
-        for (int j = 0; j < nb; ++j) {
+        // One step: block j's softmax and value product, block j + 1's scores. The scores
+        // of the current and next block alternate between sa and sb (the loop runs two
+        // steps per iteration), so no register copies are needed.
+        auto step = [&](int j, const f32x16_t (&cur)[2], f32x16_t (&nxt)[2]) {
           const int kv0 = r0 + j * BKV;
           const int buf = j & 1, nbuf = buf ^ 1;
           wait_vm_all();    // this wave's parts of V j and K j + 1 have landed
@@ -373,22 +401,24 @@ __global__ __launch_bounds__(kThreads, 2) void ring_attn(AttnArgs a) {
           // scores of block j + 1 (on the chunk's last block, of whatever the other
           // buffer holds: computed and discarded, which keeps this code branch-free so
           // that the compiler can interleave the two independent streams)
-          f32x16_t sn[2];
-          score_block(sK + nbuf * kTileBytes + k_even, sK + nbuf * kTileBytes + k_odd, qf, sn);
-          float alpha;
+          score_block(sK + nbuf * kTileBytes + k_even, sK + nbuf * kTileBytes + k_odd, qf, nxt);
           bf16x8_t pb[4];
-          const bool grow = softmax_block(sc, a.scale_log2, m, l, alpha, pb);
-          // the weights are complete here, ahead of the rescale branch, so that their
-          // exponentials stay in the same basic block as the score products
-          asm volatile("" : "+v"(pb[0]), "+v"(pb[1]), "+v"(pb[2]), "+v"(pb[3]));
-          sc[0] = sn[0];
-          sc[1] = sn[1];
-          if (grow) {
+          bool rescale;
+          const float alpha = softmax_block(cur, a.scale_log2, m, l, pb, rescale);
+          if (rescale) {
 #pragma unroll
             for (int db = 0; db < D / 32; ++db) acc[db] *= alpha;
           }
           value_block(sV_lds + buf * kTileBytes, v_lane, pb, acc);
+        };
+        f32x16_t sa[2], sb[2];
+        score_block(sK + k_even, sK + k_odd, qf, sa);
+        int j = 0;
+        for (; j + 1 < nb; j += 2) {
+          step(j, sa, sb);
+          step(j + 1, sb, sa);
         }
+        if (j < nb) step(j, sa, sb);
       }
       // every load of this chunk's rows that the workgroup uses has landed (each block's
       // loads are waited for before its LDS stores, and every thread has passed the

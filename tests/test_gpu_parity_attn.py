@@ -104,6 +104,30 @@ def test_ring_attention_parity(case, mode):
     _check(o, lse, d)
 
 
+@pytest.mark.parametrize("growing", [True, False], ids=["growing", "shrinking"])
+def test_ring_attention_scores_drifting_across_chunks(growing):
+    """Key rows of the chunk at arrival position p are scaled by 1 + 2p (growing) or by
+    1 + 2 (n - 1 - p) (shrinking), so the row maxima rise by far more than the softmax's
+    running reference tolerates at every chunk (the reference has to move, and the
+    accumulated sums be rescaled, again and again), or fall steeply (later weights
+    underflow against an early maximum). The scaled keys are rounded to bf16 and the
+    oracle sees exactly those values."""
+    _say("ring attention drifting scores growing=%s" % growing)
+    W, r, Sh, Qc, kind, Sq, H, Hkv = 4, 1, 256, 2, "ring", 256, 4, 2
+    w, d, chunks, order, s = _case(W, r, Sh, Qc, kind, Sq, H, Hkv, cfg_id=143)
+    n = len(order)
+    kv = d.B.values.copy()
+    for p, c in enumerate(order):
+        ch = chunks[int(c)]
+        f = 1 + 2 * (p if growing else n - 1 - p)
+        kv[ch.row_begin:ch.row_end] *= f
+    bits = si.f32_to_bf16_bits(kv)
+    d.B = si.Matrix(values=si.bf16_bits_to_f32(bits), dtype="bf16", bits=bits)
+    plan = csg.AttnPlan(H, Hkv, 128, Sq, s, cfg={"timeout_ms": 1000})
+    o, lse = run_attn(plan, d, chunks)
+    _check(o, lse, d)
+
+
 def test_ring_attention_repeated_calls():
     _say("ring attention repeated calls")
     w, d, chunks, order, s = _case(4, 3, 256, 2, "ring", 200, 8, 4)
