@@ -207,6 +207,7 @@ def main():
     peak = MFMA_PEAK_TFLOPS[w.dtype]
     k_overlap = float(np.mean(ker))
     k_comp = float(np.mean(ker_c))
+    kernel_name = "ring_attn" if w.op == "attn" else "chunk_gemm"
     rec = {
         "metric": "chunk-scheduled GEMM TFLOP/s @1 GPU; overlap eff = max(comp,copy)/total",
         "value": round(value, 2),
@@ -237,7 +238,7 @@ def main():
         "overlap_eff_isolated": round(overlap_eff_isolated, 4),
         "roofline": {"bound": "mfma", "achieved": round(w.flops / (k_overlap * 1e-3) / 1e12, 2), "peak": peak,
                      "unit": "TFLOP/s", "frac": round(w.flops / (k_overlap * 1e-3) / 1e12 / peak, 4),
-                     "traffic": kernel_traffic(w.name), "kernel": "ring_attn" if w.op == "attn" else "chunk_gemm",
+                     "traffic": kernel_traffic(w.name, kernel_name), "kernel": kernel_name,
                      "phase": "overlap (timed region)",
                      "kernel_ms_mean": round(k_overlap, 4)},
         "roofline_compute_only": {"bound": "mfma", "achieved": round(w.flops / (k_comp * 1e-3) / 1e12, 2),
@@ -280,30 +281,35 @@ def kernel_copy_sweep(w, sched, group_rows, d, timed_loop, moved_bytes, args, sw
     return out
 
 
-KERNEL_SOURCES = ("paper_2601_20595_amd/csrc/chunk_gemm.hip", "paper_2601_20595_amd/csrc/kernels.hpp")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "chunk_gemm_traffic.json")
+# Per measured kernel: its committed HBM-traffic summary and the sources it was taken from.
+KERNEL_TRAFFIC = {
+    "chunk_gemm": (os.path.join(ROOT, "profiles", "chunk_gemm_traffic.json"),
+                   ("paper_2601_20595_amd/csrc/chunk_gemm.hip", "paper_2601_20595_amd/csrc/kernels.hpp")),
+    "ring_attn": (os.path.join(ROOT, "profiles", "ring_attn_traffic.json"),
+                  ("paper_2601_20595_amd/csrc/chunk_attn.hip", "paper_2601_20595_amd/csrc/attn.hpp")),
+}
 
 
-def kernel_sources_sha256() -> str:
+def kernel_sources_sha256(kernel: str = "chunk_gemm") -> str:
     import hashlib
     h = hashlib.sha256()
-    for rel in KERNEL_SOURCES:
+    for rel in KERNEL_TRAFFIC[kernel][1]:
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
     return h.hexdigest()
 
 
-def kernel_traffic(workload: str):
-    """HBM bytes per launch of the GEMM kernel (FETCH_SIZE + WRITE_SIZE, scaled by the
+def kernel_traffic(workload: str, kernel: str = "chunk_gemm"):
+    """HBM bytes per launch of the kernel (FETCH_SIZE + WRITE_SIZE, scaled by the
     calibration copy) from the committed counter summary, or None when that summary is
     missing, covers another workload, or was taken from a different kernel source."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(KERNEL_TRAFFIC[kernel][0]) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
     entry = t.get("workloads", {}).get(workload)
-    if not entry or t.get("source_sha256") != kernel_sources_sha256():
+    if not entry or t.get("source_sha256") != kernel_sources_sha256(kernel):
         return None
     return entry.get("bytes_per_launch")
 

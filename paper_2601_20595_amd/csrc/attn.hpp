@@ -27,7 +27,7 @@ struct AttnArgs {
   const int64_t* const* ready;  // per chunk id: 0 once its keys and values have landed
   uint32_t* counters;         // per chunk id: units done reading it
   uint32_t* out_flags;        // per chunk id: the call number once every unit has read it
-  uint32_t* ticket;           // work-unit ticket
+  uint32_t* ticket;           // [kXcdLists] work-unit tickets, one per die's range of units
   DeviceDiag* diag;
   uint64_t timeout_ticks;
   uint32_t epoch;

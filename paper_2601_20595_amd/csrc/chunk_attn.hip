@@ -160,6 +160,25 @@ __device__ __forceinline__ void dma_tile(const uint16_t* src, int hkv, int g, in
 
 __device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// Next work unit for a workgroup on die xcd (thread 0 only). The unit list, ordered by
+// key/value head, is split into kXcdLists contiguous ranges, one per die, so that the
+// units running on a die share key/value heads and stream the same key/value blocks
+// through that die's L2 (with 8 key/value heads, one head per die). A die whose range
+// is exhausted takes from the following dies' ranges; n_units when none has any left.
+__device__ int next_unit(const AttnArgs& a, uint32_t xcd) {
+  for (int d = 0; d < kXcdLists; ++d) {
+    const int x = static_cast<int>((xcd + d) % kXcdLists);
+    const int b0 = static_cast<int>(static_cast<int64_t>(a.n_units) * x / kXcdLists);
+    const int len = static_cast<int>(static_cast<int64_t>(a.n_units) * (x + 1) / kXcdLists) - b0;
+    if (len <= 0) continue;
+    if (__hip_atomic_load(a.ticket + x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= static_cast<uint32_t>(len))
+      continue;
+    const uint32_t t = atomicAdd(a.ticket + x, 1u);
+    if (t < static_cast<uint32_t>(len)) return b0 + static_cast<int>(t);
+  }
+  return a.n_units;
+}
+
 // The value of lane ^ 32 of a wave (the other half of a query row's keys), by
 // v_permlane32_swap: swapping the halves of two copies of x leaves each lane holding x of
 // itself and of lane ^ 32, one in each copy, so their combination is symmetric in the
@@ -313,8 +332,8 @@ __global__ __launch_bounds__(kThreads, 2) void ring_attn(AttnArgs a) {
   if (blockIdx.x == 0 && a.next_ticket) {
     // clear the next call's state set (its prologue, folded into this kernel)
     for (int c = tid; c < a.n_chunks; c += kThreads) a.next_counters[c] = 0u;
+    if (tid < kXcdLists) a.next_ticket[tid] = 0u;
     if (tid == 0) {
-      a.next_ticket[0] = 0u;
       a.next_diag->timed_out = 0u;
       a.next_diag->chunk = -1;
       a.next_diag->tile = -1;
@@ -325,6 +344,9 @@ __global__ __launch_bounds__(kThreads, 2) void ring_attn(AttnArgs a) {
     }
   }
   for (int i = tid; i < kMaxAttnChunks / 32; i += kThreads) ready_bits[i] = 0;
+  uint32_t xcd;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID, 0, 4)" : "=s"(xcd));
+  xcd %= kXcdLists;
   const int n_qb = (a.Sq + BQ - 1) / BQ;
   const int G = a.H / a.Hkv;
   uint32_t units = 0;
@@ -332,7 +354,7 @@ __global__ __launch_bounds__(kThreads, 2) void ring_attn(AttnArgs a) {
   for (;;) {
     __syncthreads();  // everyone is done with s_unit / s_state / LDS of the previous unit
     if (tid == 0) {
-      int u = static_cast<int>(atomicAdd(a.ticket, 1u));
+      int u = next_unit(a, xcd);
       if (load_flag(&a.diag->abort)) u = a.n_units;
       s_unit = u;
     }
@@ -340,8 +362,8 @@ __global__ __launch_bounds__(kThreads, 2) void ring_attn(AttnArgs a) {
     const int u = __builtin_amdgcn_readfirstlane(s_unit);
     if (u >= a.n_units) break;
     ++units;
-    // unit -> (key/value head g, query block, head of g's group): units that run at the
-    // same time mostly share key/value heads
+    // unit -> (key/value head g, query block, head of g's group): consecutive units, and
+    // so a die's range of them, share key/value heads
     const int per_g = n_qb * G;
     const int g = u / per_g, rem = u - g * per_g;
     const int qb = rem / G, h = g * G + (rem - (rem / G) * G);
