@@ -4,8 +4,11 @@
 One step = one call of the whole path on one batch of synthetic input: the
 prologue, the SDMA chunk copies whose completion signals are the per-chunk flags,
 and the persistent chunk-ordered GEMM kernel, in overlap mode. Steps run back to
-back, as in a layer loop: a step's copies of a chunk may start as soon as the
-previous step's kernel has finished reading that chunk's rows. The default workload is the
+back, as in a layer loop where each layer gathers into its own activation: the
+all-gather and grouped workloads alternate between two landing buffers
+(--landing-buffers), so a step's copies wait only for the kernel two steps back to
+have read the rows they overwrite (the library tracks that per buffer), and the same
+loop with one landing buffer is reported beside it. The default workload is the
 all-gather GEMM of 8 simulated ranks (A 8192 x 4096 bf16 in 8 shards of 4
 chunks, ring arrival; B 4096 x 1792; fp32 accumulation, bf16 output).
 
@@ -45,6 +48,10 @@ def parse():
     ap.add_argument("--lanes", type=int, default=0, help="SDMA copy lanes (0 = library default)")
     ap.add_argument("--no-kernel-copies", action="store_true",
                     help="skip the comparison with chunks moved by the kernel's own workgroups")
+    ap.add_argument("--landing-buffers", type=int, default=2,
+                    help="all-gather and grouped workloads: consecutive steps gather into this many landing "
+                         "buffers in turn (as consecutive layers gather into their own activations); 1 = every "
+                         "step into the same buffer")
     return ap.parse_args()
 
 
@@ -124,6 +131,9 @@ def main():
         landing = a_full.clone()
         outgoing = None
         moved_bytes = remote_rows * w.K * in_bytes
+    # landing buffers used in turn by consecutive steps (all-gather and grouped)
+    landings = [landing] + [landing.clone() for _ in range(max(args.landing_buffers, 1) - 1)] if landing is not None \
+        else [None]
     compute = torch.cuda.Stream(device=dev)
     copy = torch.cuda.Stream(device=dev)
     # plain device-to-device copy of known size, run once before the timed region: the
@@ -134,8 +144,9 @@ def main():
     del cal_src, cal_dst
     torch.cuda.synchronize()
 
-    def call(mode, p=None):
+    def call(mode, p=None, step=0):
         p = p or plan
+        landing = landings[step % len(landings)]
         if w.op == "attn":
             p.ring_attn(a_full, k_land, v_land, k_stage, v_stage, c, lse, mode, compute, copy)
         elif w.op == "ar":
@@ -154,13 +165,13 @@ def main():
         Returns wall seconds for `steps` calls and the kernel durations (ms) the
         library timed on the compute stream."""
         p = p or plan
-        for _ in range(warmup):
-            call(mode, p)
+        for i in range(warmup):
+            call(mode, p, i)
         p.check()
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        for _ in range(steps):
-            call(mode, p)
+        for i in range(steps):
+            call(mode, p, i)
         p.check()                 # every copy the steps issued has completed
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
@@ -194,6 +205,15 @@ def main():
     ms_comp = wall_c * 1e3 / args.steps
     ms_copy = wall_x * 1e3 / args.steps
     overlap_eff = max(ms_comp, ms_copy) / ms_per_step
+    ms_one_landing = None
+    if len(landings) > 1:
+        # the same overlap loop with every step gathering into one landing buffer: a
+        # step's copy of a chunk then waits for the previous step's kernel to have read it
+        kept = list(landings)
+        landings[:] = kept[:1]
+        wall_1, _ = timed_loop("overlap", args.steps, args.warmup)
+        landings[:] = kept
+        ms_one_landing = wall_1 * 1e3 / args.steps
     # isolated calls: each mode timed alike (the call until its kernel and copies are
     # done, GPU idle before)
     tot, _ = bracketed("overlap", args.steps, args.warmup)
@@ -224,11 +244,13 @@ def main():
         "config": {"workload": w.name, "op": w.op, "M": w.M, "N": w.N, "K": w.K, "world": w.world,
                    "chunks": len(chunks), "moved_bytes": moved_bytes, "arch": arch,
                    "num_workgroups": plan.info.num_workgroups,
-                   "tile": [plan.info.bm, plan.info.bn, plan.info.bk]},
+                   "tile": [plan.info.bm, plan.info.bn, plan.info.bk],
+                   "landing_buffers": len(landings) if landing is not None else None},
         # steady state: ms per step of back-to-back loops in each mode
         "ms_per_step_compute_only": round(ms_comp, 4),
         "ms_per_step_copy_only": round(ms_copy, 4),
         "overlap_eff": round(overlap_eff, 4),
+        "ms_per_step_one_landing_buffer": None if ms_one_landing is None else round(ms_one_landing, 4),
         "compute_only_tflops": round(w.flops / (ms_comp * 1e-3) / 1e12, 2),
         "copy_only_GBps": round(moved_bytes / (ms_copy * 1e-3) / 1e9, 2),
         # one isolated call per mode (median)

@@ -269,14 +269,20 @@ csg_status csg_plan_set_copy_delays(csg_plan* p, const float* delay_us_host, int
 /* AllGather + GEMM on one rank. a_landing is the full M x K A whose local rows are
  * already in place; a_staging has the same layout and holds the remote rows (the
  * simulated peers' shards). The prologue and the persistent kernel are queued on
- * `compute`; then, once the work queued earlier on `copy` and the plan's previous
- * kernel have completed, the calling thread issues, for each remote chunk in
- * arrival order, an SDMA copy staging -> landing whose completion signal is the
- * chunk's ready flag, and returns when all of them have completed. The
- * kernel runs tiles in chunk order, each waiting for its chunks. Work queued on
- * `compute` afterwards is ordered after the kernel. Asynchronous failures (a flag
- * wait that timed out) surface through csg_plan_check. CSG_ERR_TIMEOUT if a host
- * wait expired.
+ * `compute`; then, once the work queued earlier on `copy` has completed, the
+ * calling thread issues, for each remote chunk in arrival order, an SDMA copy
+ * staging -> landing whose completion signal is the chunk's ready flag. Before a
+ * copy overwrites landing rows it waits for the plan's earlier kernels that read
+ * them: after a call on the same a_landing, until that call's kernel has read the
+ * chunk; after a call on a different buffer that overlaps it, until that kernel has
+ * read every chunk; a buffer no earlier call of the plan overlaps (say, the other
+ * of two activations used in turn) needs no wait. In overlap mode the call returns
+ * once every copy is issued (the kernel waits for each, and csg_plan_check for
+ * all); in copy-only mode it returns when the copies have completed. The kernel runs
+ * tiles in chunk order, each waiting for its chunks. Work queued on `compute`
+ * afterwards is ordered after the kernel. Asynchronous failures (a flag wait that
+ * timed out) surface through csg_plan_check. CSG_ERR_TIMEOUT if a host wait
+ * expired.
  * With CSG_COPY_KERNEL the call only queues the prologue and the kernel on
  * `compute` (its copy workgroups move the chunks; copy-only: they alone run) and
  * returns; `copy` is not used. */

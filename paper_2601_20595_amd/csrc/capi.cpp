@@ -135,6 +135,16 @@ struct csg_plan {
                                        // flags; consumers: the call whose kernel has finished reading
                                        // the chunk's rows
   uint32_t last_kernel_epoch = 0;      // call number of the latest kernel launched (0: none)
+  // Consumer landing buffers recently read by this plan's kernels: the latest reader's
+  // call number per distinct range (newest last), and the newest reader among ranges
+  // dropped from the list. Copies into a range wait only for kernels that read it.
+  struct LandingUse {
+    uintptr_t base;
+    size_t bytes;
+    uint32_t epoch;
+  };
+  std::vector<LandingUse> landing_uses;
+  uint32_t landing_dropped = 0;
   uint32_t* h_out_flags_dev = nullptr; // its device address
   uint32_t* d_scratch = nullptr;       // target of the engines' warm-up copies
   csg::SdmaEngines sdma;
@@ -471,6 +481,7 @@ csg_status host_wait(csg_plan* p, hipEvent_t e, const char* what) {
 struct CallState {
   int prev_parity = 0;
   bool prev_kernel = false;
+  bool wrapped = false;  // the call number restarted: every earlier kernel has finished
 };
 
 // The signals this call's copies complete: one set per call parity.
@@ -508,6 +519,10 @@ csg_status begin_call(csg_plan* p, csg_mode mode, CallState* cs) {
         return st;
     std::memset(p->h_out_flags, 0, static_cast<size_t>(std::max(p->n_chunks(), 1)) * 4);
     p->epoch = 1;
+    // every earlier kernel has finished: no copy of this call waits for one
+    p->landing_uses.clear();
+    p->landing_dropped = 0;
+    cs->wrapped = true;
   }
   ++p->epoch;
   p->host_diag = csg_diag{0, -1, -1, 0, p->epoch, 0};
@@ -701,13 +716,53 @@ csg_status launch_gemm(csg_plan* p, const void* A, const void* B, void* C, csg_m
   return CSG_OK;
 }
 
+constexpr size_t kLandingHistory = 4;
+
+// The kernel that copies into landing rows [base, base + bytes) have to wait for, and
+// whether they may do so chunk by chunk. The newest kernel that read an overlapping range
+// decides (the plan's kernels run in call order on one stream, so once it has started
+// reading, every older kernel has finished): when it read exactly this range, a chunk's
+// copy waits for that kernel to finish reading the chunk; when it read a different,
+// overlapping range (or the range is unknown because the history dropped it), every
+// copy waits until that kernel has finished reading all chunks. 0: no kernel to wait for.
+uint32_t landing_reader(const csg_plan* p, const void* base, size_t bytes, bool* per_chunk) {
+  const uintptr_t b = reinterpret_cast<uintptr_t>(base);
+  uint32_t e = p->landing_dropped;
+  *per_chunk = false;
+  for (const csg_plan::LandingUse& u : p->landing_uses) {
+    const bool overlap = u.base < b + bytes && b < u.base + u.bytes;
+    if (overlap && u.epoch > e) {
+      e = u.epoch;
+      *per_chunk = u.base == b && u.bytes == bytes;
+    }
+  }
+  return e;
+}
+
+// Records that this call's kernel (p->epoch) reads landing rows [base, base + bytes).
+void note_landing_reader(csg_plan* p, const void* base, size_t bytes) {
+  const uintptr_t b = reinterpret_cast<uintptr_t>(base);
+  auto& uses = p->landing_uses;
+  for (size_t i = 0; i < uses.size(); ++i)
+    if (uses[i].base == b && uses[i].bytes == bytes) {
+      uses.erase(uses.begin() + static_cast<std::ptrdiff_t>(i));
+      break;
+    }
+  uses.push_back({b, bytes, p->epoch});
+  if (uses.size() > kLandingHistory) {
+    p->landing_dropped = std::max(p->landing_dropped, uses.front().epoch);
+    uses.erase(uses.begin());
+  }
+}
+
 // Consumer copies: staging -> landing per remote chunk, on engine (i mod engines)
 // for the i-th remote chunk in arrival order; each completes the chunk's (armed)
 // ready signal. Before overwriting a chunk's rows the issuer waits until the kernel
 // that read them last (call prev_reader) is done with them: that kernel reports it per
 // chunk (its consumed words), and its completion event settles it for every chunk
-// (also when it gave up early). Copy delays release chunk i at the sum of the first i
-// delays after the call started.
+// (also when it gave up early). With all_chunks the first copy waits until that kernel
+// has finished reading every chunk (it read an overlapping but different range). Copy
+// delays release chunk i at the sum of the first i delays after the call started.
 struct CopyIssuer {
   csg_plan* p;
   void* landing;
@@ -719,17 +774,58 @@ struct CopyIssuer {
   bool prev_done;
   void* landing2 = nullptr;        // ring attention: values (landing / staging: keys)
   const void* staging2 = nullptr;
+  bool all_chunks = false;
 
   CopyIssuer(csg_plan* plan, void* l, const void* s, uint32_t prev)
       : p(plan), landing(l), staging(s), prev_reader(prev), t0(Clock::now()), prev_done(prev == 0) {}
+
+  // Waits until kernel prev_reader has finished reading chunk cid (false with !block
+  // when it has not yet).
+  csg_status wait_read(int32_t cid, bool block, bool* ready) {
+    const int prev_parity = static_cast<int>(prev_reader & 1);
+    const auto budget = std::chrono::milliseconds(p->cfg.timeout_ms) * 4;
+    const volatile uint32_t* f = p->h_out_flags + cid;
+    const Clock::time_point tw = Clock::now();
+    uint32_t spins = 0;
+    *ready = true;
+    while (!prev_done && *f < prev_reader) {
+      if (!block) {
+        *ready = false;
+        return CSG_OK;
+      }
+      if ((++spins & 255u) == 0) {
+        const hipError_t q = hipEventQuery(p->ev_kernel_done[prev_parity]);
+        if (q == hipSuccess) {
+          prev_done = true;
+          break;
+        }
+        if (q != hipErrorNotReady) return hip_fail(q, "the previous call's kernel");
+      }
+      if (Clock::now() - tw > budget) {
+        p->host_diag = csg_diag{1, cid, -1, *f, p->epoch, 0};
+        return fail(CSG_ERR_TIMEOUT, "the previous kernel did not finish reading chunk %d in time", cid);
+      }
+    }
+    return CSG_OK;
+  }
 
   // Issues copies in arrival order. Without `block` it stops at the first copy that
   // would have to wait (for its release time or for the previous kernel).
   csg_status run(bool block) {
     const int64_t row_bytes = p->attention() ? int64_t{p->at_kv_heads} * csg::kAttnHeadDim * 2 : p->K * in_bytes(p);
     const std::vector<hsa_signal_t>& sigs = call_signals(p);
-    const int prev_parity = static_cast<int>(prev_reader & 1);
-    const auto budget = std::chrono::milliseconds(p->cfg.timeout_ms) * 4;
+    if (all_chunks && !prev_done) {
+      for (int32_t cid = 0; cid < p->n_chunks(); ++cid) {
+        bool ready = true;
+        const csg_status st = wait_read(cid, block, &ready);
+        if (st != CSG_OK) {
+          (void)finish_copies(p, next);
+          return st;
+        }
+        if (!ready) return CSG_OK;
+      }
+      prev_done = true;
+    }
     for (; next < p->remote_order.size(); ++next) {
       const size_t i = next;
       const int32_t cid = p->remote_order[i];
@@ -741,28 +837,13 @@ struct CopyIssuer {
         spin_until(due);
       }
       if (!prev_done) {
-        const volatile uint32_t* f = p->h_out_flags + cid;
-        const Clock::time_point tw = Clock::now();
-        uint32_t spins = 0;
-        while (*f < prev_reader) {
-          if (!block) return CSG_OK;
-          if ((++spins & 255u) == 0) {
-            const hipError_t q = hipEventQuery(p->ev_kernel_done[prev_parity]);
-            if (q == hipSuccess) {
-              prev_done = true;
-              break;
-            }
-            if (q != hipErrorNotReady) {
-              (void)finish_copies(p, i);
-              return hip_fail(q, "the previous call's kernel");
-            }
-          }
-          if (Clock::now() - tw > budget) {
-            (void)finish_copies(p, i);
-            p->host_diag = csg_diag{1, cid, -1, *f, p->epoch, 0};
-            return fail(CSG_ERR_TIMEOUT, "the previous kernel did not finish reading chunk %d in time", cid);
-          }
+        bool ready = true;
+        const csg_status st = wait_read(cid, block, &ready);
+        if (st != CSG_OK) {
+          (void)finish_copies(p, i);
+          return st;
         }
+        if (!ready) return CSG_OK;
       }
       if (!p->delays_us.empty()) release_us += p->delays_us[i];
       const int64_t off = c.row_begin * row_bytes;
@@ -915,12 +996,15 @@ csg_status consumer_call(csg_plan* p, void* landing, const void* staging, const 
   if (g.err != hipSuccess) return hip_fail(g.err, "hipSetDevice");
   if (p->kernel_copies()) return kernel_copy_call(p, landing, staging, b, c, nullptr, mode, compute);
   CallState cs;
-  // the kernel that last read the landing rows (before this call's own)
-  const uint32_t prev_reader = p->last_kernel_epoch;
+  // the kernel that last read these landing rows (before this call's own)
+  const size_t landing_bytes = static_cast<size_t>(p->M) * static_cast<size_t>(p->K) * in_bytes(p);
+  bool per_chunk = false;
+  const uint32_t prev_reader = landing_reader(p, landing, landing_bytes, &per_chunk);
   csg_status st = begin_call(p, mode, &cs);
   if (st != CSG_OK) return st;
   const bool copies = mode != CSG_MODE_COMPUTE_ONLY && !p->remote_order.empty();
-  CopyIssuer issuer(p, landing, staging, prev_reader);
+  CopyIssuer issuer(p, landing, staging, cs.wrapped ? 0u : prev_reader);
+  issuer.all_chunks = !per_chunk;
   if (copies) {
     // the copies that need not wait go first (they take the longest to land), then the
     // kernel is queued: it starts as soon as the previous kernel ends and waits for its
@@ -929,9 +1013,21 @@ csg_status consumer_call(csg_plan* p, void* landing, const void* staging, const 
     if ((st = issuer.run(false)) != CSG_OK) return st;
   }
   if ((st = launch_prologue_call(p, mode, compute)) != CSG_OK) return st;
-  if (mode != CSG_MODE_COPY_ONLY && (st = launch_gemm(p, landing, b, c, mode, compute)) != CSG_OK) return st;
+  if (mode != CSG_MODE_COPY_ONLY) {
+    if ((st = launch_gemm(p, landing, b, c, mode, compute)) != CSG_OK) return st;
+    note_landing_reader(p, landing, landing_bytes);
+  }
   if (!copies) return CSG_OK;
   if ((st = issuer.run(true)) != CSG_OK) return st;
+  if (mode == CSG_MODE_OVERLAP) {
+    // Every copy is issued. This call's kernel waits for each of them (a chunk's tiles
+    // wait for its signal), the signal set is armed again only after that kernel has
+    // finished (two calls on), and a later copy into these landing rows waits for the
+    // kernel to have read them: nothing needs the copies to have completed when the call
+    // returns, and the engines move on to the next call's copies without a gap.
+    p->copies_in_flight = false;
+    return CSG_OK;
+  }
   return finish_copies(p, p->remote_order.size());
 }
 
@@ -1416,7 +1512,7 @@ csg_status csg_ring_attn(csg_plan* p, const void* q, void* k_landing, void* v_la
   const uint32_t prev_reader = p->last_kernel_epoch;  // the kernel that last read the key/value rows
   csg_status st = begin_call(p, mode, &cs);
   if (st != CSG_OK) return st;
-  CopyIssuer issuer(p, k_landing, k_staging, prev_reader);
+  CopyIssuer issuer(p, k_landing, k_staging, cs.wrapped ? 0u : prev_reader);
   issuer.landing2 = v_landing;
   issuer.staging2 = v_staging;
   if (copies) {

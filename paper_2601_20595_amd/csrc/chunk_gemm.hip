@@ -987,6 +987,9 @@ __global__ __launch_bounds__(kPrologueThreads) void chunk_prologue(PrologueArgs 
 // Variant table
 // ---------------------------------------------------------------------------------
 using LoopBf16_256 = Bf16Loop<256, 256>;
+using LoopBf16_256x128 = Bf16Loop<256, 128>;
+using LoopBf16_128x256 = Bf16Loop<128, 256>;
+using LoopBf16_128 = Bf16Loop<128, 128>;
 using LoopF32_64 = F32Loop<64, 64>;
 
 // The timing events (either may be null) take the dispatch's own start and end
@@ -1029,6 +1032,11 @@ const Variant kVariants[] = {
     // GEMM + all-reduce: producers with the fused reduction
     CSG_VARIANT(InType::BF16, LoopBf16_256, true, true, true),    CSG_VARIANT(InType::BF16, LoopBf16_256, false, true, true),
     CSG_VARIANT(InType::F32, LoopF32_64, false, true, true),
+    // smaller bf16 tiles for the consumers (more, shorter tiles: a chunk's tiles finish
+    // sooner after it lands)
+    CSG_VARIANT(InType::BF16, LoopBf16_256x128, true, false, false),
+    CSG_VARIANT(InType::BF16, LoopBf16_128x256, true, false, false),
+    CSG_VARIANT(InType::BF16, LoopBf16_128, true, false, false),
 };
 
 const Variant* find_variant(const KernelKey& k) {

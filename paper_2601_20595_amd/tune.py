@@ -13,7 +13,10 @@ exposes, for one operator at one shape:
   - tile dispatch (per-die tickets or a static stride);
   - split-K for every tile, or for the tiles on the overlap's critical path;
   - the copy realization: copy engines, or the kernel's own workgroups with a
-    given number of copy workgroups.
+    given number of copy workgroups;
+  - the tile shape (bf16 consumers: 256x256, 256x128, 128x256, 128x128), off by
+    default: smaller tiles finish a chunk sooner after it lands, at a lower MFMA
+    efficiency per tile.
 
 Each candidate is timed as back-to-back calls in overlap mode (the steady state
 of a loop over layers), bracketed by csg_plan_check, which waits for the plan's
@@ -73,13 +76,14 @@ def _cfg(**kw) -> Tuple[Tuple[str, int], ...]:
 def search_space(op: str, chunk_splits: Sequence[Optional[int]] = (None,), dispatch: Sequence[int] = (1, 2),
                  split_k: Sequence[int] = (1, 2), tail: Sequence[Tuple[int, int]] = ((0, 0), (2, 8)),
                  copy_workgroups: Sequence[int] = (32, 64, 128), sdma: bool = True,
-                 kernel_copies: bool = True) -> List[Candidate]:
+                 kernel_copies: bool = True, tiles: Sequence[Optional[Tuple[int, int]]] = (None,)) -> List[Candidate]:
     """Candidates in a fixed order (the first one is the library's default plan).
 
     op: "ag", "rs" or "grouped". GEMM-RS has no copy workgroups (its kernel
     realization sends from the epilogue), so one kernel candidate replaces the
     copy-workgroup sweep. Split-K combined with a tail split is left out (the tail
-    split already covers the critical tiles)."""
+    split already covers the critical tiles). tiles: (bm, bn) shapes to try, None for
+    the library's default tile."""
     if op not in ("ag", "rs", "grouped"):
         raise ValueError("unknown op %r" % op)
     backends: List[Tuple[int, Optional[int]]] = []
@@ -92,11 +96,14 @@ def search_space(op: str, chunk_splits: Sequence[Optional[int]] = (None,), dispa
             backends += [(1, cw) for cw in copy_workgroups]
     out: List[Candidate] = []
     seen = set()
-    for q, (be, cw), disp, sk, (ts, tc) in itertools.product(chunk_splits, backends, dispatch, split_k, tail):
+    for q, (be, cw), disp, sk, (ts, tc), tile in itertools.product(chunk_splits, backends, dispatch, split_k, tail,
+                                                                    tiles):
         if sk > 1 and ts > 1:
             continue
+        bm, bn = tile if tile is not None else (None, None)
         c = Candidate(q, _cfg(copy_backend=be or None, copy_workgroups=cw, tile_dispatch=disp if disp != 1 else None,
-                              split_k=sk if sk > 1 else None, tail_split=ts or None, tail_chunks=tc or None))
+                              split_k=sk if sk > 1 else None, tail_split=ts or None, tail_chunks=tc or None,
+                              bm=bm, bn=bn, bk=64 if tile is not None else None))
         if c not in seen:
             seen.add(c)
             out.append(c)

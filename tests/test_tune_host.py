@@ -25,6 +25,10 @@ def test_search_space_shape():
     assert len(tune.search_space("grouped", kernel_copies=False)) == 2 * 3
     with pytest.raises(ValueError):
         tune.search_space("gemm")
+    tiled = tune.search_space("ag", kernel_copies=False, tiles=(None, (256, 128), (128, 128)))
+    assert len(tiled) == 3 * len(tune.search_space("ag", kernel_copies=False))
+    shapes = {(c.cfg_dict().get("bm"), c.cfg_dict().get("bn"), c.cfg_dict().get("bk")) for c in tiled}
+    assert shapes == {(None, None, None), (256, 128, 64), (128, 128, 64)}
 
 
 class _FakePlan:
