@@ -220,7 +220,7 @@ __device__ __forceinline__ void warm_lines(const __amdgpu_buffer_rsrc_t& rs, int
 
 template <int BM_, int BN_>
 struct Bf16Loop {
-  static constexpr int BM = BM_, BN = BN_, BK = 64;
+  static constexpr int BM = BM_, BN = BN_, BK = 64, IN_BYTES = 2;
   // 8 waves, two per SIMD: while one wave of a SIMD waits on LDS or issues its DMA,
   // the other keeps the matrix core busy. Waves are laid out 2 (M) x 4 (N).
   static constexpr int WAVES_M = 2, WAVES_N = 4, WAVES = WAVES_M * WAVES_N, THREADS = WAVES * 64;
@@ -331,7 +331,7 @@ struct Bf16Loop {
 // ---------------------------------------------------------------------------------
 template <int BM_, int BN_>
 struct F32Loop {
-  static constexpr int BM = BM_, BN = BN_, BK = 16;
+  static constexpr int BM = BM_, BN = BN_, BK = 16, IN_BYTES = 4;
   static constexpr int WAVES_M = 2, WAVES_N = 2, THREADS = 256;
   static constexpr int WTM = BM / 2, WTN = BN / 2, MI = WTM / 32, NI = WTN / 32;
   static constexpr int LDK = BK + 4;                      // floats per LDS row
@@ -642,7 +642,7 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
     }
   }
   for (int i = tid; i < kMaxChunks / 32; i += kThreads) ready_bits[i] = 0;
-  const int in_bytes = (Loop::BK == 64) ? 2 : 4;
+  const int in_bytes = Loop::IN_BYTES;
   uint32_t xcd;
   asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID, 0, 4)" : "=s"(xcd));
   xcd %= kXcdLists;

@@ -310,25 +310,25 @@ def test_ag_split_k_and_dispatch_parity(case):
 # Smaller bf16 tiles (256x128, 128x256, 128x128): the same results, to the same bar
 # ---------------------------------------------------------------------------------
 TILE_AG = [
-    # W, r, S, Q, kind, N, K, bm, bn, split
-    (4, 0, 300, 2, "ring", 600, 512, 256, 128, 1),          # ragged M and N, straddling tiles
-    (4, 3, 256, 4, "swizzle1d", 520, 320, 128, 256, 1),     # 2 chunks per 128-row tile
-    (2, 1, 512, 1, "permutation", 256, 1024, 128, 128, 1),
-    (4, 2, 96, 2, "ring", 200, 192, 128, 128, 1),           # 48-row chunks, ragged N
-    (4, 0, 300, 2, "ring", 600, 512, 128, 128, 2),          # with split-K
+    # W, r, S, Q, kind, N, K, bm, bn, bk, split
+    (4, 0, 300, 2, "ring", 600, 512, 256, 128, 64, 1),          # ragged M and N, straddling tiles
+    (4, 3, 256, 4, "swizzle1d", 520, 320, 128, 256, 64, 1),     # 2 chunks per 128-row tile
+    (2, 1, 512, 1, "permutation", 256, 1024, 128, 128, 64, 1),
+    (4, 2, 96, 2, "ring", 200, 192, 128, 128, 64, 1),           # 48-row chunks, ragged N
+    (4, 0, 300, 2, "ring", 600, 512, 128, 128, 64, 2),          # with split-K
 ]
 
 
-@pytest.mark.parametrize("case", TILE_AG, ids=lambda c: "W%d-r%d-S%d-Q%d-%s-N%d-K%d-%dx%d-split%d" % c)
+@pytest.mark.parametrize("case", TILE_AG, ids=lambda c: "W%d-r%d-S%d-Q%d-%s-N%d-K%d-%dx%dx%d-split%d" % c)
 @pytest.mark.parametrize("mode", ["overlap", "compute_only"])
 def test_ag_tile_shape_parity(case, mode):
-    W, r, S, Q, kind, N, K, bm, bn, split = case
+    W, r, S, Q, kind, N, K, bm, bn, bk, split = case
     _say("ag tile shape %s mode=%s" % (case, mode))
     w, d, perm, chunks, order = _small_ag(W, r, S, Q, kind, N, K, "bf16", "bf16")
     s = csg.Schedule.uniform(W, r, S, Q, kind, perm)
     plan = csg.Plan("ag", W * S, N, K, "bf16", "bf16", s,
-                    cfg={"timeout_ms": 1000, "bm": bm, "bn": bn, "bk": 64, "split_k": split})
-    assert (plan.info.bm, plan.info.bn) == (bm, bn)
+                    cfg={"timeout_ms": 1000, "bm": bm, "bn": bn, "bk": bk, "split_k": split})
+    assert (plan.info.bm, plan.info.bn, plan.info.bk) == (bm, bn, bk)
     R = oracle.ag_gemm(d.A.device_array, d.B.device_array, chunks, order)
     c, _ = run_ag(plan, chunks, d.A, d.B, "bf16", mode=mode)
     assert_close(out_to_f64(c, "bf16"), R, tol_for("bf16", "bf16"), "ag tile shape")
