@@ -218,20 +218,20 @@ __device__ __forceinline__ void warm_lines(const __amdgpu_buffer_rsrc_t& rs, int
   }
 }
 
-template <int BM_, int BN_>
+template <int BM_, int BN_, int WAVES_M_ = 2, int WAVES_N_ = 4>
 struct Bf16Loop {
   static constexpr int BM = BM_, BN = BN_, BK = 64, IN_BYTES = 2;
   // 8 waves, two per SIMD: while one wave of a SIMD waits on LDS or issues its DMA,
-  // the other keeps the matrix core busy. Waves are laid out 2 (M) x 4 (N).
-  static constexpr int WAVES_M = 2, WAVES_N = 4, WAVES = WAVES_M * WAVES_N, THREADS = WAVES * 64;
+  // the other keeps the matrix core busy. Waves are laid out WAVES_M (M) x WAVES_N (N):
+  // 2 x 4 by default; 8 x 1 for tiles whose N side (224 = 7 x 32) splits no further.
+  static constexpr int WAVES_M = WAVES_M_, WAVES_N = WAVES_N_, WAVES = WAVES_M * WAVES_N, THREADS = WAVES * 64;
   static constexpr int WTM = BM / WAVES_M, WTN = BN / WAVES_N, MI = WTM / 32, NI = WTN / 32;
   static constexpr int ROWB = 128;                           // bytes per LDS row (64 bf16)
   static constexpr int STAGE_A = BM * ROWB, STAGE_B = BN * ROWB;
   static constexpr int STAGE = STAGE_A + STAGE_B;
   static constexpr int LDS_BYTES = 2 * STAGE;
-  static constexpr int A_ROWS_W = BM / WAVES, B_ROWS_W = BN / WAVES;  // rows each wave loads per stage
-  static constexpr int A_LOADS = A_ROWS_W / 8, B_LOADS = B_ROWS_W / 8; // DMA issues (8 rows each)
-  static_assert(A_ROWS_W % 8 == 0 && B_ROWS_W % 8 == 0 && WTM % 32 == 0 && WTN % 32 == 0, "bf16 tile shape");
+  static constexpr int A_GROUPS = BM / 8, B_GROUPS = BN / 8;  // a stage is loaded in groups of 8 rows
+  static_assert(WAVES == 8 && BM % 8 == 0 && BN % 8 == 0 && WTM % 32 == 0 && WTN % 32 == 0, "bf16 tile shape");
 
   // LDS swizzle: logical 16-byte vector v of tile row r sits at physical vector
   // v ^ swz(r), swz(r) = (r & 7) ^ ((r >> 3) & 1). Any 8 consecutive aligned rows,
@@ -240,30 +240,47 @@ struct Bf16Loop {
   // rows touches 16 distinct 4-bank groups whether LDS is 32 or 64 banks wide.
   __device__ static int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
-  // Issue one stage (the BK columns starting at byte kbase of every row): wave w
-  // fills rows [w*BM/8, (w+1)*BM/8) of A and likewise of B. Lane l of an 8-row group
-  // writes LDS slot l (row l/8, physical vector l%8), so it fetches logical vector
-  // (l%8) ^ swz(row) of that row.
+  // One operand's share of a stage, kGroups groups of 8 rows starting at LDS byte
+  // address rows0. When the groups divide evenly, wave w takes a contiguous run of
+  // them; otherwise pairs of groups are dealt round robin (pair p to wave p % WAVES).
+  // Either way a group's parity, which decides the lane's swizzled offset, is known at
+  // compile time.
+  template <int kGroups>
+  __device__ static void issue_rows(const __amdgpu_buffer_rsrc_t& rs, uint32_t rows0, int wave, int v_even,
+                                    int v_odd, int K, int kbase) {
+    if constexpr (kGroups % (2 * WAVES) == 0) {
+      constexpr int kPer = kGroups / WAVES;  // even
+      const int g0 = wave * kPer;
+      const uint32_t l0 = __builtin_amdgcn_readfirstlane(rows0 + g0 * 8 * ROWB);
+#pragma unroll
+      for (int q = 0; q < kPer; ++q) dma16(rs, l0 + q * 8 * ROWB, (q & 1) ? v_odd : v_even, (g0 + q) * 8 * K * 2 + kbase);
+    } else {
+      static_assert(kGroups % 2 == 0, "an even number of 8-row groups");
+      constexpr int kPairs = kGroups / 2;
+#pragma unroll
+      for (int q = 0; q < (kPairs + WAVES - 1) / WAVES; ++q) {
+        const int pr = wave + q * WAVES;
+        if (pr < kPairs) {
+          const uint32_t l0 = __builtin_amdgcn_readfirstlane(rows0 + pr * 16 * ROWB);
+          dma16(rs, l0, v_even, pr * 16 * K * 2 + kbase);
+          dma16(rs, l0 + 8 * ROWB, v_odd, (pr * 16 + 8) * K * 2 + kbase);
+        }
+      }
+    }
+  }
+
+  // Issue one stage (the BK columns starting at byte kbase of every row), A then B.
+  // Lane l of an 8-row group writes LDS slot l (row l/8, physical vector l%8), so it
+  // fetches logical vector (l%8) ^ swz(row) of that row; row = 8 g + l/8, so
+  // swz(row) = (l/8) ^ (g & 1).
   __device__ static void issue(uint32_t lds_base, int buf, int kbase, const __amdgpu_buffer_rsrc_t& rsA,
                                const __amdgpu_buffer_rsrc_t& rsB, int K, int wave, int lane) {
     const int lr = lane >> 3;
-    const int wrow_a = wave * A_ROWS_W, wrow_b = wave * B_ROWS_W;
-    const uint32_t la = __builtin_amdgcn_readfirstlane(lds_base + buf * STAGE + wrow_a * ROWB);
-    const uint32_t lb = __builtin_amdgcn_readfirstlane(lds_base + buf * STAGE + STAGE_A + wrow_b * ROWB);
-    // row = group base (a multiple of 8) + lr, so swz(row) = lr ^ ((row >> 3) & 1): the
-    // lane part of the offset only depends on the parity of the 8-row group
+    const uint32_t stage = lds_base + buf * STAGE;
     const int v_even = lr * K * 2 + (((lane & 7) ^ lr) * 16);
     const int v_odd = lr * K * 2 + (((lane & 7) ^ lr ^ 1) * 16);
-#pragma unroll
-    for (int q = 0; q < A_LOADS; ++q) {
-      const int g8 = wrow_a + q * 8;
-      dma16(rsA, la + q * 8 * ROWB, ((g8 >> 3) & 1) ? v_odd : v_even, g8 * K * 2 + kbase);
-    }
-#pragma unroll
-    for (int q = 0; q < B_LOADS; ++q) {
-      const int g8 = wrow_b + q * 8;
-      dma16(rsB, lb + q * 8 * ROWB, ((g8 >> 3) & 1) ? v_odd : v_even, g8 * K * 2 + kbase);
-    }
+    issue_rows<A_GROUPS>(rsA, stage, wave, v_even, v_odd, K, kbase);
+    issue_rows<B_GROUPS>(rsB, stage + STAGE_A, wave, v_even, v_odd, K, kbase);
   }
 
   __device__ static void run(unsigned char* lds, const TileGeom& g, f32x16 (&acc)[MI][NI], int wave, int lane) {
@@ -311,12 +328,14 @@ struct Bf16Loop {
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[cur][j], fa[cur][i], acc[i][j], 0, 0, 0);
         if (ks + 1 < BK / 16) {
           // interleave the next sub-step's LDS reads with this sub-step's MFMAs
+          constexpr int kPairs = MI * NI < MI + NI ? MI * NI : MI + NI;
 #pragma unroll
-          for (int q = 0; q < MI + NI; ++q) {
+          for (int q = 0; q < kPairs; ++q) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
           }
-          __builtin_amdgcn_sched_group_barrier(0x008, MI * NI - (MI + NI), 0);
+          if (MI * NI > kPairs) __builtin_amdgcn_sched_group_barrier(0x008, MI * NI - kPairs, 0);
+          if (MI + NI > kPairs) __builtin_amdgcn_sched_group_barrier(0x100, MI + NI - kPairs, 0);
         }
       }
       wait_dma_all();   // the next stage has landed in LDS
@@ -990,6 +1009,7 @@ using LoopBf16_256 = Bf16Loop<256, 256>;
 using LoopBf16_256x128 = Bf16Loop<256, 128>;
 using LoopBf16_128x256 = Bf16Loop<128, 256>;
 using LoopBf16_128 = Bf16Loop<128, 128>;
+using LoopBf16_256x224 = Bf16Loop<256, 224, 8, 1>;
 using LoopF32_64 = F32Loop<64, 64>;
 
 // The timing events (either may be null) take the dispatch's own start and end
@@ -1037,6 +1057,9 @@ const Variant kVariants[] = {
     CSG_VARIANT(InType::BF16, LoopBf16_256x128, true, false, false),
     CSG_VARIANT(InType::BF16, LoopBf16_128x256, true, false, false),
     CSG_VARIANT(InType::BF16, LoopBf16_128, true, false, false),
+    // 256 x 224 tiles: N = 7 x 256 and 14 x 256 shapes fill every CU in whole waves
+    CSG_VARIANT(InType::BF16, LoopBf16_256x224, true, false, false),
+    CSG_VARIANT(InType::BF16, LoopBf16_256x224, false, false, false),
 };
 
 const Variant* find_variant(const KernelKey& k) {

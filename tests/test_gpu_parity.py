@@ -316,6 +316,9 @@ TILE_AG = [
     (2, 1, 512, 1, "permutation", 256, 1024, 128, 128, 64, 1),
     (4, 2, 96, 2, "ring", 200, 192, 128, 128, 64, 1),           # 48-row chunks, ragged N
     (4, 0, 300, 2, "ring", 600, 512, 128, 128, 64, 2),          # with split-K
+    (4, 0, 300, 2, "ring", 600, 512, 256, 224, 64, 1),          # 8 x 1 waves: ragged M and N
+    (4, 3, 256, 4, "swizzle1d", 896, 320, 256, 224, 64, 1),     # N = 4 x 224
+    (2, 1, 512, 1, "permutation", 448, 1024, 256, 224, 64, 2),  # with split-K
 ]
 
 
@@ -334,6 +337,18 @@ def test_ag_tile_shape_parity(case, mode):
     assert_close(out_to_f64(c, "bf16"), R, tol_for("bf16", "bf16"), "ag tile shape")
     c2, _ = run_ag(plan, chunks, d.A, d.B, "bf16", mode=mode, repeats=3)
     assert torch.equal(c.cpu(), c2.cpu())
+
+
+def test_ag_256x224_fp32_output_integer_inputs_bit_exact():
+    W, r, S, Q, kind, N, K = 4, 1, 256, 2, "ring", 448, 640
+    _say("ag 256x224 fp32 out, integer inputs")
+    w, d, perm, chunks, order = _small_ag(W, r, S, Q, kind, N, K, "bf16", "f32", dist="int")
+    s = csg.Schedule.uniform(W, r, S, Q, kind, perm)
+    plan = csg.Plan("ag", W * S, N, K, "bf16", "f32", s, cfg={"timeout_ms": 1000, "bm": 256, "bn": 224, "bk": 64})
+    assert (plan.info.bm, plan.info.bn) == (256, 224)
+    c, _ = run_ag(plan, chunks, d.A, d.B, "f32")
+    R = oracle.ag_gemm(d.A.device_array, d.B.device_array, chunks, order)
+    assert np.array_equal(out_to_f64(c, "f32"), R)
 
 
 TAIL_CASES = [
