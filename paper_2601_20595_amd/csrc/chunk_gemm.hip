@@ -314,21 +314,33 @@ struct Bf16Loop {
     wait_dma_all();
     __syncthreads();
     load_frags(0, 0, 0);
+    constexpr int kSteps = BK / 16;
+    constexpr int kPairs = MI * NI < MI + NI ? MI * NI : MI + NI;
     for (int t = 0; t < nk; ++t) {
       const int buf = t & 1;
-      if (t + 1 < nk) issue(lds_base, buf ^ 1, (t + 1) * BK * 2, rsA, rsB, K, wave, lane);
+      const bool more = t + 1 < nk;
+      if (more) issue(lds_base, buf ^ 1, (t + 1) * BK * 2, rsA, rsB, K, wave, lane);
 #pragma unroll
-      for (int ks = 0; ks < BK / 16; ++ks) {
+      for (int ks = 0; ks < kSteps; ++ks) {
         const int cur = ks & 1;
-        if (ks + 1 < BK / 16) load_frags(cur ^ 1, buf, ks + 1);  // next sub-step's fragments in flight
+        if (ks + 1 < kSteps) {
+          load_frags(cur ^ 1, buf, ks + 1);  // next sub-step's fragments in flight
+        } else {
+          // This stage's last fragments are in registers. Wait until the next stage has
+          // landed and every wave is done reading this one, then read the next stage's
+          // first fragments under this sub-step's MFMAs: the matrix core has queued work
+          // on both sides of the barrier instead of draining at it.
+          wait_dma_all();
+          __syncthreads();
+          if (more) load_frags(cur ^ 1, buf ^ 1, 0);
+        }
 #pragma unroll
         for (int i = 0; i < MI; ++i)
 #pragma unroll
           for (int j = 0; j < NI; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[cur][j], fa[cur][i], acc[i][j], 0, 0, 0);
-        if (ks + 1 < BK / 16) {
-          // interleave the next sub-step's LDS reads with this sub-step's MFMAs
-          constexpr int kPairs = MI * NI < MI + NI ? MI * NI : MI + NI;
+        if (ks + 1 < kSteps || more) {
+          // interleave the fragment reads in flight with this sub-step's MFMAs
 #pragma unroll
           for (int q = 0; q < kPairs; ++q) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
@@ -338,9 +350,6 @@ struct Bf16Loop {
           if (MI + NI > kPairs) __builtin_amdgcn_sched_group_barrier(0x100, MI + NI - kPairs, 0);
         }
       }
-      wait_dma_all();   // the next stage has landed in LDS
-      __syncthreads();  // and every wave is done with this stage
-      if (t + 1 < nk) load_frags(0, buf ^ 1, 0);
     }
   }
 };
