@@ -42,7 +42,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=2, help="workload id (1..5)")
+    ap.add_argument("--config", type=int, default=2, help="workload id (1..7; 6 = GEMM + all-reduce, 7 = ring attention)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target length of the CPU baseline sample")
     ap.add_argument("--lanes", type=int, default=0, help="SDMA copy lanes (0 = library default)")
