@@ -24,8 +24,10 @@
  *     weights are E x N x K. dtype CSG_BF16 elements are raw bfloat16 bit
  *     patterns (uint16), CSG_F32 are IEEE binary32.
  *   - Objects (schedules, plans) are not thread-safe; distinct objects are
- *     independent. Successive calls on one plan must pass the same compute stream:
- *     the plan's per-call state is reset in that stream's order.
+ *     independent. The kernels of one plan run in call order: the plan's per-call
+ *     state is reset, and its copies wait for earlier readers, in that order. Pass
+ *     the same compute stream to successive calls; a call on another stream first
+ *     makes that stream wait for the previous call's kernel.
  */
 #ifndef CSG_H_
 #define CSG_H_

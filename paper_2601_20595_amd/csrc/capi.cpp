@@ -135,6 +135,8 @@ struct csg_plan {
                                        // flags; consumers: the call whose kernel has finished reading
                                        // the chunk's rows
   uint32_t last_kernel_epoch = 0;      // call number of the latest kernel launched (0: none)
+  hipStream_t last_compute = nullptr;  // compute stream of the latest call (valid if has_last_compute)
+  bool has_last_compute = false;
   // Consumer landing buffers recently read by this plan's kernels: the latest reader's
   // call number per distinct range (newest last), and the newest reader among ranges
   // dropped from the list. Copies into a range wait only for kernels that read it.
@@ -557,6 +559,13 @@ csg_status begin_call(csg_plan* p, csg_mode mode, CallState* cs) {
 // previous call launched none (copy-only, an error) or the copies are the kernel's own
 // (their ready words depend on this call's mode): then the prologue kernel does.
 csg_status launch_prologue_call(csg_plan* p, csg_mode mode, hipStream_t compute) {
+  // The per-call state sets and the copies' write-after-read waits rely on the plan's
+  // kernels running in call order. A call on another compute stream than the previous
+  // one therefore first waits, on the device, for the previous call's kernel.
+  if (p->has_last_compute && p->last_compute != compute && p->last_kernel_epoch)
+    CSG_HIP(hipStreamWaitEvent(compute, p->ev_kernel_done[p->last_kernel_epoch & 1], 0));
+  p->last_compute = compute;
+  p->has_last_compute = true;
   const int set = p->epoch & 1;
   if (mode != CSG_MODE_COPY_ONLY && !p->kernel_copies() && p->reset_for_epoch == p->epoch) return CSG_OK;
   csg::PrologueArgs pa{};

@@ -111,3 +111,39 @@ def test_overlapping_landing_buffers_wait_for_every_chunk():
     refs = [oracle.ag_gemm(np.ascontiguousarray(bits[o:o + M]), d.B.device_array, chunks, order) for o in (0, S)]
     for i in range(calls):
         assert_close(out_to_f64(outs[i], "bf16"), refs[i % 2], tol_for("bf16", "bf16"), "call %d" % i)
+
+
+@pytest.mark.parametrize("n_buffers", [1, 2])
+def test_calls_alternating_compute_streams(n_buffers):
+    """Back-to-back calls whose compute stream alternates between two streams: the
+    plan's kernels must still run in call order (each call's state set is cleared by
+    the previous call's kernel, and copies wait for the last reader of their rows), so
+    every output matches its own inputs."""
+    _say("alternating compute streams: %d landing buffers" % n_buffers)
+    chunks, order, sets = _inputs(3)
+    M = W * S
+    sts = [streams(), streams()]
+    b = to_dev(sets[0].B.device_array)
+    stage = [to_dev(d.A.device_array) for d in sets]
+    landings = []
+    for _ in range(n_buffers):
+        l = stage[0].clone()
+        for c in chunks:
+            if not c.is_local:
+                nan_fill_(l[c.row_begin:c.row_end])
+        landings.append(l)
+    calls = 6
+    outs = [empty_out(M, N, "bf16") for _ in range(calls)]
+    for o in outs:
+        nan_fill_(o)
+    s = csg.Schedule.uniform(W, R, S, Q, KIND)
+    plan = csg.Plan("ag", M, N, K, "bf16", "bf16", s, cfg={"timeout_ms": 2000})
+    torch.cuda.synchronize()
+    for i in range(calls):
+        st = sts[i % 2]
+        plan.ag_gemm(landings[i % n_buffers], stage[i % 3], b, outs[i], "overlap", st.compute, st.copy)
+    plan.check()
+    torch.cuda.synchronize()
+    refs = [oracle.ag_gemm(d.A.device_array, sets[0].B.device_array, chunks, order) for d in sets]
+    for i in range(calls):
+        assert_close(out_to_f64(outs[i], "bf16"), refs[i % 3], tol_for("bf16", "bf16"), "call %d" % i)
