@@ -166,6 +166,27 @@ def _ptr(t) -> int:
     return int(t.data_ptr())
 
 
+def _elem_bytes(dtype) -> int:
+    d = DTYPES[dtype] if isinstance(dtype, str) else int(dtype)
+    return 2 if d == CSG_BF16 else 4
+
+
+def _buf(t, need: int, what: str) -> None:
+    """Checks a tensor argument before its pointer reaches the library, which reads and
+    writes dense row-major buffers of the plan's shape: it must be contiguous, hold at
+    least ``need`` bytes and live on a GPU. Raw integer pointers and None pass
+    unchecked (the C calls reject a NULL where one is required)."""
+    if t is None or isinstance(t, int):
+        return
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % what)
+    have = t.numel() * t.element_size()
+    if have < need:
+        raise ValueError("%s holds %d bytes; the plan needs %d" % (what, have, need))
+    if t.device.type != "cuda":
+        raise ValueError("%s must be a GPU tensor" % what)
+
+
 def _stream(s) -> int:
     if s is None:
         return 0
@@ -423,6 +444,14 @@ class Plan:
                  device: int = 0):
         self.op = op
         self.handle = csg_plan_create(op, M, N, K, in_dtype, out_dtype, schedule.handle, group_rows, cfg, device)
+        # buffer sizes the calls check tensor arguments against
+        ib, ob = _elem_bytes(in_dtype), _elem_bytes(out_dtype)
+        groups = len(group_rows) if group_rows is not None else 1
+        self._bytes = {"a": M * K * ib, "b": groups * N * K * ib, "c": M * N * ob}
+        if op == "ar":
+            chunks, _ = schedule.get()
+            own = sum(c[1] - c[0] for c in chunks if c[4])
+            self._bytes["partials"] = (M // own - 1) * own * N * ob
 
     @property
     def info(self) -> csg_plan_info:
@@ -435,17 +464,34 @@ class Plan:
         csg_plan_set_copy_delays(self.handle, delays_us)
 
     def ag_gemm(self, a_landing, a_staging, b_nk, c, mode="overlap", compute_stream=None, copy_stream=None):
+        z = self._bytes
+        for t, n, what in ((a_landing, z.get("a", 0), "a_landing"), (a_staging, z.get("a", 0), "a_staging"), (b_nk, z.get("b", 0), "b_nk"),
+                           (c, z.get("c", 0), "c")):
+            _buf(t, n, what)
         csg_ag_gemm(self.handle, a_landing, a_staging, b_nk, c, mode, compute_stream, copy_stream)
 
     def gemm_rs(self, a, b_nk, c, c_outgoing, mode="overlap", compute_stream=None, copy_stream=None):
+        z = self._bytes
+        for t, n, what in ((a, z.get("a", 0), "a"), (b_nk, z.get("b", 0), "b_nk"), (c, z.get("c", 0), "c"), (c_outgoing, z.get("c", 0), "c_outgoing")):
+            _buf(t, n, what)
         csg_gemm_rs(self.handle, a, b_nk, c, c_outgoing, mode, compute_stream, copy_stream)
 
     def gemm_ar(self, a, b_nk, c, c_outgoing, partials_staging, partials_landing, reduced_staging, mode="overlap",
                 compute_stream=None, copy_stream=None):
+        z = self._bytes
+        for t, n, what in ((a, z.get("a", 0), "a"), (b_nk, z.get("b", 0), "b_nk"), (c, z.get("c", 0), "c"), (c_outgoing, z.get("c", 0), "c_outgoing"),
+                           (partials_staging, z.get("partials", 0), "partials_staging"),
+                           (partials_landing, z.get("partials", 0), "partials_landing"),
+                           (reduced_staging, z.get("c", 0), "reduced_staging")):
+            _buf(t, n, what)
         csg_gemm_ar(self.handle, a, b_nk, c, c_outgoing, partials_staging, partials_landing, reduced_staging, mode,
                     compute_stream, copy_stream)
 
     def grouped_gemm(self, x_landing, x_staging, b_enk, c, mode="overlap", compute_stream=None, copy_stream=None):
+        z = self._bytes
+        for t, n, what in ((x_landing, z.get("a", 0), "x_landing"), (x_staging, z.get("a", 0), "x_staging"), (b_enk, z.get("b", 0), "b_enk"),
+                           (c, z.get("c", 0), "c")):
+            _buf(t, n, what)
         csg_grouped_gemm(self.handle, x_landing, x_staging, b_enk, c, mode, compute_stream, copy_stream)
 
     def check(self) -> csg_diag:
@@ -475,8 +521,17 @@ class AttnPlan(Plan):
     def __init__(self, n_heads, n_kv_heads, head_dim, q_rows, schedule: Schedule, cfg=None, device: int = 0):
         self.op = "attn"
         self.handle = csg_attn_plan_create(n_heads, n_kv_heads, head_dim, q_rows, schedule.handle, cfg, device)
+        chunks, _ = schedule.get()
+        keys = chunks[-1][1] if chunks else 0
+        self._bytes = {"q": q_rows * n_heads * head_dim * 2, "kv": keys * n_kv_heads * head_dim * 2,
+                       "lse": n_heads * q_rows * 4}
 
     def ring_attn(self, q, k_landing, v_landing, k_staging, v_staging, o, lse, mode="overlap", compute_stream=None,
                   copy_stream=None):
+        z = self._bytes
+        for t, n, what in ((q, z.get("q", 0), "q"), (k_landing, z.get("kv", 0), "k_landing"), (v_landing, z.get("kv", 0), "v_landing"),
+                           (k_staging, z.get("kv", 0), "k_staging"), (v_staging, z.get("kv", 0), "v_staging"), (o, z.get("q", 0), "o"),
+                           (lse, z.get("lse", 0), "lse")):
+            _buf(t, n, what)
         csg_ring_attn(self.handle, q, k_landing, v_landing, k_staging, v_staging, o, lse, mode, compute_stream,
                       copy_stream)

@@ -227,3 +227,19 @@ def test_attention_plans_validate():
     assert _status(csg.AttnPlan, 8, 2, 128, 300, odd, device=-1) == csg.CSG_ERR_UNSUPPORTED
     gemm = csg.Plan("ag", 1024, 64, 64, "bf16", "bf16", s, device=-1)
     assert _status(csg.csg_ring_attn, gemm.handle, 16, 16, 16, 16, 16, 16, 16) == csg.CSG_ERR_INVALID
+
+
+def test_binding_checks_tensor_arguments():
+    """The binding checks a tensor before passing its pointer: contiguous, large enough
+    for the plan's shape, on a GPU (raw pointers and None pass unchecked)."""
+    torch = pytest.importorskip("torch")
+    from paper_2601_20595_amd import _buf
+    big = torch.zeros(64, 64, dtype=torch.int16)
+    with pytest.raises(ValueError, match="contiguous"):
+        _buf(big.t(), 64 * 64 * 2, "a")
+    with pytest.raises(ValueError, match="holds 8192 bytes"):
+        _buf(big, 64 * 64 * 2 + 1, "a")
+    with pytest.raises(ValueError, match="GPU tensor"):
+        _buf(big, 64 * 64 * 2, "a")
+    _buf(None, 1 << 20, "a")
+    _buf(12345, 1 << 20, "a")
