@@ -161,3 +161,36 @@ def test_ar_full_size_sampled():
     assert np.array_equal(c.cpu().numpy().view(np.uint16)[other], d.reduced.device_array[other])
     assert_close(O[[idx[i] for i in other]], Rout[other], 2e-2, "sent partial rows")
     assert np.array_equal(O[[idx[i] for i in own]], G[[idx[i] for i in own]])
+
+
+def _sweep_case(i):
+    g = np.random.default_rng([137, i])
+    dtype, out_dtype = [("bf16", "bf16"), ("bf16", "bf16"), ("bf16", "f32"), ("f32", "f32")][int(g.integers(0, 4))]
+    bm = 256 if dtype == "bf16" else 64          # the own shard starts and ends on tile rows
+    W = int(g.integers(2, 9))
+    r = int(g.integers(0, W))
+    S = bm * int(g.integers(1, 4 if dtype == "bf16" else 9))
+    Q = [q for q in (1, 2, 4, 8) if S % q == 0][int(g.integers(0, 4))]
+    step = 64 if dtype == "bf16" else 16
+    K = step * int(g.integers(1, 9))
+    N = 4 * int(g.integers(1, 150))
+    mode = "compute_only" if g.random() < 0.25 else "overlap"
+    dist = "int" if g.random() < 0.25 else "normal"
+    return W, r, S, Q, N, K, dtype, out_dtype, mode, dist
+
+
+AR_SWEEP = list(range(12))
+
+
+@pytest.mark.parametrize("i", AR_SWEEP, ids=lambda i: "%d-W%d-r%d-S%d-Q%d-N%d-K%d-%s-%s-%s-%s" % ((i,) + _sweep_case(i)))
+def test_ar_sweep_parity(i):
+    """Seeded sweep: ranks, own-shard rows (multiples of the tile height), chunks per
+    shard, N, K, dtypes, mode and input distribution drawn per case; integer inputs are
+    compared bit for bit."""
+    W, r, S, Q, N, K, dtype, out_dtype, mode, dist = _sweep_case(i)
+    _say("ar sweep %d %s" % (i, (W, r, S, Q, N, K, dtype, out_dtype, mode, dist)))
+    w, d, chunks, order = _inputs(W, r, S, Q, N, K, dtype, out_dtype, dist=dist, cfg_id=1370 + i)
+    s = csg.Schedule.uniform(W, r, S, Q, "rs_ring")
+    plan = csg.Plan("ar", W * S, N, K, dtype, out_dtype, s, cfg={"timeout_ms": 1000})
+    c, out = run_ar(plan, d, out_dtype, mode=mode)
+    _check(c, out, d, chunks, order, out_dtype, dtype, mode, exact=(dist == "int" and out_dtype == "f32"))

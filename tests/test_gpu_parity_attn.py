@@ -147,3 +147,22 @@ def test_ring_attention_full_size_sampled():
     o, lse = run_attn(plan, d, chunks)
     rows = sorted(set([0, 1, 127, 128, w.M - 1] + list(np.random.default_rng(7).integers(0, w.M, 27))))
     _check(o, lse, d, rows=rows)
+
+
+def test_ring_attention_withheld_chunk_times_out_and_plan_recovers():
+    """The host releases the last remote key/value chunk long after the kernel's (tiny)
+    wait bound: the kernel must give up with a timeout that names that chunk and exit
+    normally, and the plan must then run correctly without the delay."""
+    _say("ring attention withheld chunk")
+    W, r, Sh, Qc, kind, Sq, H, Hkv = 2, 0, 256, 2, "ring", 128, 4, 2
+    w, d, chunks, order, s = _case(W, r, Sh, Qc, kind, Sq, H, Hkv, cfg_id=144)
+    plan = csg.AttnPlan(H, Hkv, 128, Sq, s, cfg={"timeout_ms": 20})
+    plan.set_copy_delays([0.0, 300000.0])            # second remote chunk 300 ms late
+    with pytest.raises(csg.CsgError) as ei:
+        run_attn(plan, d, chunks)
+    assert ei.value.status == csg.CSG_ERR_TIMEOUT
+    assert ei.value.diag.chunk == order[-1]
+    torch.cuda.synchronize()
+    plan.set_copy_delays(None)
+    o, lse = run_attn(plan, d, chunks)
+    _check(o, lse, d)
