@@ -216,6 +216,11 @@ namespace {
 void free_plan_device(csg_plan* p) {
   if (p->device < 0) return;
   DeviceGuard g(p->device);
+  // The plan's kernels poll its signals' values and read its device tables: wait for
+  // them first (their waits are bounded, so they end), then for copies still in flight,
+  // and only then destroy the signals and free the memory.
+  for (hipEvent_t e : {p->ev_prologue, p->ev_kernel_done[0], p->ev_kernel_done[1]})
+    if (e) (void)hipEventSynchronize(e);
   for (auto* sets : {p->sig_ready, p->sig_send, p->sig_part})
     for (int k = 0; k < 2; ++k)
       for (hsa_signal_t sgn : sets[k])
@@ -225,8 +230,6 @@ void free_plan_device(csg_plan* p) {
       for (hsa_signal_t sgn : sets[k])
         if (sgn.handle) hsa_signal_destroy(sgn);
   p->sdma.close();
-  for (hipEvent_t e : p->ev_kernel_done)
-    if (e) (void)hipEventSynchronize(e);
   for (void* ptr : {static_cast<void*>(p->d_tiles), static_cast<void*>(p->d_list_ptr),
                     static_cast<void*>(p->d_list_ids), static_cast<void*>(p->d_raster), static_cast<void*>(p->d_need),
                     static_cast<void*>(p->d_list_begin), static_cast<void*>(p->d_ws),

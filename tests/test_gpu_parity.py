@@ -498,3 +498,52 @@ def test_full_size_workload_sampled(cfg_id):
     else:
         R = oracle.ag_gemm(d.A.device_array, d.B.device_array, chunks, order, row_subset=rows)
     assert_close(out_to_f64(c[rows], w.out_dtype), R[rows], tol, w.name)
+
+
+@pytest.mark.parametrize("op", ["ag", "rs"])
+def test_plan_destroyed_right_after_a_call_waits_for_its_work(op):
+    """A plan destroyed straight after an overlap call (no check, no synchronisation)
+    must first wait for its kernel and copies, which still read the plan's signals and
+    tables; the caller's outputs are then complete."""
+    W, r, S, Q, N, K = 4, 1, 256, 2, 512, 512
+    _say("destroy right after a call: %s" % op)
+    st = streams()
+    if op == "ag":
+        w, d, perm, chunks, order = _small_ag(W, r, S, Q, "ring", N, K, "bf16", "bf16")
+        s = csg.Schedule.uniform(W, r, S, Q, "ring")
+        plan = csg.Plan("ag", W * S, N, K, "bf16", "bf16", s, cfg={"timeout_ms": 1000})
+        a = to_dev(d.A.device_array)
+        landing = a.clone()
+        for ch in chunks:
+            if not ch.is_local:
+                landing[ch.row_begin:ch.row_end].zero_()
+        b = to_dev(d.B.device_array)
+        c = empty_out(W * S, N, "bf16")
+        torch.cuda.synchronize()
+        plan.ag_gemm(landing, a, b, c, "overlap", st.compute, st.copy)
+        plan.close()
+        torch.cuda.synchronize()
+        R = oracle.ag_gemm(d.A.device_array, d.B.device_array, chunks, order)
+        assert_close(out_to_f64(c, "bf16"), R, 2e-2, "ag after destroy")
+        assert torch.equal(landing, a)
+    else:
+        w = si.Workload(103, "rs", "rs", M=W * S, N=N, K=K, dtype="bf16", out_dtype="bf16", dist="normal", world=W,
+                        rank=r, shard_rows=S, chunks_per_shard=Q, order="rs_ring")
+        d = si.draw(w)
+        chunks, order = oracle.uniform_schedule(W, r, S, Q, "rs_ring")
+        s = csg.Schedule.uniform(W, r, S, Q, "rs_ring")
+        plan = csg.Plan("rs", W * S, N, K, "bf16", "bf16", s, cfg={"timeout_ms": 1000})
+        a, b = to_dev(d.A.device_array), to_dev(d.B.device_array)
+        c, out = empty_out(W * S, N, "bf16"), empty_out(W * S, N, "bf16")
+        out.zero_()
+        torch.cuda.synchronize()
+        plan.gemm_rs(a, b, c, out, "overlap", st.compute, st.copy)
+        plan.close()
+        torch.cuda.synchronize()
+        R, _, _ = oracle.gemm_rs(d.A.device_array, d.B.device_array, chunks, order)
+        G, O = out_to_f64(c, "bf16"), out_to_f64(out, "bf16")
+        assert_close(G, R, 2e-2, "rs after destroy")
+        for ch in chunks:
+            if not ch.is_local:
+                assert np.array_equal(O[ch.row_begin:ch.row_end], G[ch.row_begin:ch.row_end])
+    s.close()
