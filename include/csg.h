@@ -8,13 +8,18 @@
  * complete. On one GPU the "remote" side of a rank is simulated: remote shards
  * are staged in HBM and moved by SDMA copy-engine copies (Section 2.3, copy
  * engine backend; Section 5.2, realization (1): copy engine + global-memory
- * signals). Copies are issued by the calling thread straight to the SDMA engines;
- * a call that moves chunks returns once its copies have completed, while its
- * kernel may still be running on the compute stream.
+ * signals). Copies are issued by the calling thread straight to the SDMA engines.
+ * An overlap call returns once its copies are issued (its kernel waits for each
+ * chunk's copy, csg_plan_check for all of them); a copy-only call returns once they
+ * have completed. Either way the kernel may still be running on the compute stream.
  *
  * Conventions for every entry point
  *   - Every call returns csg_status; nothing throws or aborts across the ABI.
  *     A failing call leaves a thread-local message readable by csg_last_error().
+ *   - Ordering against the caller's streams: a call's kernels follow the work already
+ *     queued on its compute stream, and its copies the work already queued on its
+ *     copy stream. Inputs written on any other stream (the default one included) must
+ *     be complete before the call.
  *   - Pointers named *_host are host memory; every other data pointer is device
  *     memory of the plan's device, owned by the caller. Streams are hipStream_t
  *     values passed as void*; they are owned by the caller and must belong to
