@@ -9,9 +9,10 @@
  * are staged in HBM and moved by SDMA copy-engine copies (Section 2.3, copy
  * engine backend; Section 5.2, realization (1): copy engine + global-memory
  * signals). Copies are issued by the calling thread straight to the SDMA engines.
- * An overlap call returns once its copies are issued (its kernel waits for each
- * chunk's copy, csg_plan_check for all of them); a copy-only call returns once they
- * have completed. Either way the kernel may still be running on the compute stream.
+ * An overlap GEMM call returns once its copies are issued (its kernel waits for each
+ * chunk's copy, csg_plan_check for all of them); ring attention and copy-only calls
+ * return once their copies have completed. Either way the kernel may still be running
+ * on the compute stream.
  *
  * Conventions for every entry point
  *   - Every call returns csg_status; nothing throws or aborts across the ABI.
