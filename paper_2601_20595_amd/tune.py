@@ -76,14 +76,18 @@ def _cfg(**kw) -> Tuple[Tuple[str, int], ...]:
 def search_space(op: str, chunk_splits: Sequence[Optional[int]] = (None,), dispatch: Sequence[int] = (1, 2),
                  split_k: Sequence[int] = (1, 2), tail: Sequence[Tuple[int, int]] = ((0, 0), (2, 8)),
                  copy_workgroups: Sequence[int] = (32, 64, 128), sdma: bool = True,
-                 kernel_copies: bool = True, tiles: Sequence[Optional[Tuple[int, int]]] = (None,)) -> List[Candidate]:
+                 kernel_copies: bool = True, tiles: Sequence[Optional[Tuple[int, int]]] = (None,),
+                 grids: Sequence[int] = (0,)) -> List[Candidate]:
     """Candidates in a fixed order (the first one is the library's default plan).
 
     op: "ag", "rs" or "grouped". GEMM-RS has no copy workgroups (its kernel
     realization sends from the epilogue), so one kernel candidate replaces the
     copy-workgroup sweep. Split-K combined with a tail split is left out (the tail
     split already covers the critical tiles). tiles: (bm, bn) shapes to try, None for
-    the library's default tile."""
+    the library's default tile. grids: persistent grid sizes to try, 0 for one
+    workgroup per co-resident slot (the default); a grid that divides the tile count
+    into whole waves (224 for 896 tiles on 256 CUs) keeps the waves in step and the
+    workgroups sharing a die's L2 at the same K steps."""
     if op not in ("ag", "rs", "grouped"):
         raise ValueError("unknown op %r" % op)
     backends: List[Tuple[int, Optional[int]]] = []
@@ -96,14 +100,14 @@ def search_space(op: str, chunk_splits: Sequence[Optional[int]] = (None,), dispa
             backends += [(1, cw) for cw in copy_workgroups]
     out: List[Candidate] = []
     seen = set()
-    for q, (be, cw), disp, sk, (ts, tc), tile in itertools.product(chunk_splits, backends, dispatch, split_k, tail,
-                                                                    tiles):
+    for q, (be, cw), disp, sk, (ts, tc), tile, grid in itertools.product(chunk_splits, backends, dispatch, split_k,
+                                                                          tail, tiles, grids):
         if sk > 1 and ts > 1:
             continue
         bm, bn = tile if tile is not None else (None, None)
         c = Candidate(q, _cfg(copy_backend=be or None, copy_workgroups=cw, tile_dispatch=disp if disp != 1 else None,
                               split_k=sk if sk > 1 else None, tail_split=ts or None, tail_chunks=tc or None,
-                              bm=bm, bn=bn, bk=64 if tile is not None else None))
+                              bm=bm, bn=bn, bk=64 if tile is not None else None, num_workgroups=grid or None))
         if c not in seen:
             seen.add(c)
             out.append(c)

@@ -102,3 +102,13 @@ def test_uniform_plan_factory_builds_host_plans_and_rejects_unaligned_epilogue_s
     p = perm_make(tune.Candidate(4, ()))
     assert p.info.n_chunks == 16
     p.close()
+
+
+def test_search_space_grid_dimension():
+    """Grid sizes are a search dimension; 0 keeps the library's default grid, which
+    stays the first candidate."""
+    base = tune.search_space("ag", kernel_copies=False)
+    grids = tune.search_space("ag", kernel_copies=False, grids=(0, 224))
+    assert grids[0] == base[0]
+    assert len(grids) == 2 * len(base)
+    assert sum(1 for c in grids if ("num_workgroups", 224) in c.cfg) == len(base)
