@@ -33,7 +33,7 @@
  *     independent. The kernels of one plan run in call order: the plan's per-call
  *     state is reset, and its copies wait for earlier readers, in that order. Pass
  *     the same compute stream to successive calls; a call on another stream first
- *     makes that stream wait for the previous call's kernel.
+ *     makes that stream wait for the previous call's kernel and prologue.
  */
 #ifndef CSG_H_
 #define CSG_H_

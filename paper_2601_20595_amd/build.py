@@ -28,15 +28,20 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.cpp")) + glob.glob(os.path.join(CSRC, "*.hip")))
 
 
+def compile_flags() -> list:
+    """hipcc flags of every library source (device code for gfx950 only)."""
+    return ["-O3", "-std=c++17", "-fPIC", "-I", os.path.join(ROOT, "include"), "-I", CSRC,
+            "--offload-arch=" + ARCH,
+            # packed fp32 ALU ops are kept out of every kernel
+            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+            "-Wno-unused-command-line-argument"]
+
+
 def build(verbose: bool = False) -> str:
     """Compile every source into LIB (always rebuilds)."""
     objdir = os.path.join(HERE, "_build")
     os.makedirs(objdir, exist_ok=True)
-    common = ["-O3", "-std=c++17", "-fPIC", "-I", os.path.join(ROOT, "include"), "-I", CSRC,
-              "--offload-arch=" + ARCH,
-              # packed fp32 ALU ops are kept out of every kernel
-              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-              "-Wno-unused-command-line-argument"]
+    common = compile_flags()
     objs = []
     procs = []
     for src in sources():

@@ -15,12 +15,15 @@
 // behind it could not progress until the kernel that waits for its flag ends.
 //
 // The ordering the copies need is enforced by the calling thread before it issues
-// them (the caller's copy stream has reached the call; the previous call's kernel
-// no longer reads the buffer being rewritten), and a call returns once its copies
-// have completed, so work queued afterwards on any stream sees them. This matches
-// the paper's copy-engine backend, whose transfers are launched from the host
-// (Section 2.3). Reduce-scatter output chunks are copied out by the calling thread
-// as their completion flags (coherent host memory) rise.
+// them (the caller's copy stream has reached the call; the earlier kernel that read
+// the rows being rewritten has finished reading them). An overlap GEMM call returns
+// once its copies are issued: its kernel waits for each chunk's copy, and
+// csg_plan_check for all of them. Ring-attention and copy-only calls return once
+// their copies have completed. This matches the paper's copy-engine backend, whose
+// transfers are launched from the host (Section 2.3). Reduce-scatter output chunks
+// are copied out by the calling thread as their completion flags (coherent host
+// memory) rise; those copies complete after the call returns, and the next call's
+// kernel waits for each before rewriting its rows.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -171,7 +174,8 @@ struct csg_plan {
                                        // error paths only; producer: every call)
   int copies_set = 0;                  // signal set of those copies
   hipEvent_t ev_copy_in = nullptr;     // the caller's copy stream reached the call
-  hipEvent_t ev_prologue = nullptr;    // the prologue finished (waited for on an epoch wrap)
+  hipEvent_t ev_prologue = nullptr;    // the latest prologue finished
+  bool prologue_queued = false;        // ev_prologue has been recorded
   hipEvent_t ev_kernel_done[2] = {nullptr, nullptr};  // by epoch parity
   hipEvent_t ev_k0[kTimingRing] = {};  // timing events around each kernel launch (ring)
   hipEvent_t ev_k1[kTimingRing] = {};
@@ -563,10 +567,14 @@ csg_status begin_call(csg_plan* p, csg_mode mode, CallState* cs) {
 // (their ready words depend on this call's mode): then the prologue kernel does.
 csg_status launch_prologue_call(csg_plan* p, csg_mode mode, hipStream_t compute) {
   // The per-call state sets and the copies' write-after-read waits rely on the plan's
-  // kernels running in call order. A call on another compute stream than the previous
-  // one therefore first waits, on the device, for the previous call's kernel.
-  if (p->has_last_compute && p->last_compute != compute && p->last_kernel_epoch)
-    CSG_HIP(hipStreamWaitEvent(compute, p->ev_kernel_done[p->last_kernel_epoch & 1], 0));
+  // kernels and prologues running in call order. A call on another compute stream than
+  // the previous one therefore first waits, on the device, for the latest kernel and the
+  // latest prologue queued on the earlier streams (a copy-only call queues a prologue
+  // that clears a state set, and no kernel).
+  if (p->has_last_compute && p->last_compute != compute) {
+    if (p->last_kernel_epoch) CSG_HIP(hipStreamWaitEvent(compute, p->ev_kernel_done[p->last_kernel_epoch & 1], 0));
+    if (p->prologue_queued) CSG_HIP(hipStreamWaitEvent(compute, p->ev_prologue, 0));
+  }
   p->last_compute = compute;
   p->has_last_compute = true;
   const int set = p->epoch & 1;
@@ -590,6 +598,7 @@ csg_status launch_prologue_call(csg_plan* p, csg_mode mode, hipStream_t compute)
   }
   CSG_HIP(csg::launch_prologue(pa, compute));
   CSG_HIP(hipEventRecord(p->ev_prologue, compute));
+  p->prologue_queued = true;
   return CSG_OK;
 }
 
@@ -1247,6 +1256,12 @@ csg_status csg_plan_create(csg_op op, int64_t M, int64_t N, int64_t K, csg_dtype
                     static_cast<long long>(ch.row_begin));
       }
 
+  // every kernel variant keeps a per-workgroup bitmap of the chunks it has seen ready
+  // (consumers: landed; producers: the previous call's copy out of the chunk done)
+  if (p->n_chunks() > csg::kernel_max_chunks()) {
+    delete p;
+    return fail(CSG_ERR_UNSUPPORTED, "at most %d chunks", csg::kernel_max_chunks());
+  }
   if (device >= 0) {
     p->key = csg::KernelKey{bf16 ? csg::InType::BF16 : csg::InType::F32, out_dtype == CSG_BF16, !p->consumer(),
                             c.bm, c.bn, c.bk, p->allreduce()};
@@ -1266,10 +1281,6 @@ csg_status csg_plan_create(csg_op op, int64_t M, int64_t N, int64_t K, csg_dtype
       delete p;
       return fail(CSG_ERR_UNSUPPORTED, "a %d-row tile of A/B (K = %lld) or of C (N = %lld) exceeds the 32-bit offset range",
                   std::max(c.bm, c.bn), static_cast<long long>(K), static_cast<long long>(N));
-    }
-    if (p->consumer() && p->n_chunks() > csg::kernel_max_chunks()) {
-      delete p;
-      return fail(CSG_ERR_UNSUPPORTED, "at most %d chunks", csg::kernel_max_chunks());
     }
     char arch[64];
     csg_status st = csg_device_check(device, arch, sizeof arch);

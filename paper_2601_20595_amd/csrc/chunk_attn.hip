@@ -390,7 +390,7 @@ __global__ __launch_bounds__(kThreads, 2) void ring_attn(AttnArgs a) {
       __syncthreads();
       if (tid == 0) s_state = wait_chunk(a, c, u, ready_bits);
       __syncthreads();
-      if (s_state < 0) {
+      if (__builtin_amdgcn_readfirstlane(s_state) < 0) {
         aborted = true;
         break;
       }

@@ -706,11 +706,12 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
     __syncthreads();
     // uniform across the workgroup; readfirstlane lets everything derived from it live in SGPRs
     const int pos = __builtin_amdgcn_readfirstlane(s_pos);
-    if (pos >= a.n_tiles || s_state < 0) break;
+    const int state = __builtin_amdgcn_readfirstlane(s_state);
+    if (pos >= a.n_tiles || state < 0) break;
     ++units;
     // a chunk seen ready for the first time: every wave drops possibly stale cache
     // lines, unless chunks are line-aligned (then no stale line of a chunk can exist)
-    if (!kProducer && s_state > 0 && a.acquire_fresh) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
+    if (!kProducer && state > 0 && a.acquire_fresh) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
 
     const TileDesc td = a.tiles[pos];
     const int64_t col0 = static_cast<int64_t>(td.n_tile) * BN;
@@ -727,7 +728,7 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
     g.abytes = (static_cast<int64_t>(g.arows) * a.K - k0) * in_bytes;
     g.bbytes = (static_cast<int64_t>(g.brows) * a.K - k0) * in_bytes;
 
-    if (!kProducer && s_state > 0 && a.n_tiles_n > 0) {
+    if (!kProducer && state > 0 && a.n_tiles_n > 0) {
       // this workgroup saw one of the tile's chunks land just now: warm its share of
       // the tile's A rows (all K columns), shared with the other column tiles and
       // K-slices
@@ -805,13 +806,17 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
       __syncthreads();
       if (tid == 0) s_state = wait_chunks(a, pos, ready_bits);
       __syncthreads();
-      return s_state >= 0;
+      return __builtin_amdgcn_readfirstlane(s_state) >= 0;
     };
     auto acc_run = [&](int r) -> f32x4 {
       const int i = r / (NI * 4), j = (r / 4) % NI, q = r % 4;
       return f32x4{acc[i][j][4 * q + 0], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
     };
 
+    // A wait of this unit gave up (timeout, or another workgroup's abort): the unit is
+    // left unfinished. Every such wait has raised the kernel's abort flag, so each
+    // workgroup stops when it takes its next unit; the loop's only exit stays at its top.
+    bool skip = false;
     if constexpr (kReduce) {
       // GEMM + all-reduce: a tile of the own shard adds the other ranks' partial sums of
       // its rows (in ascending rank order, in fp32) before its output is stored, so the
@@ -821,9 +826,9 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
         __syncthreads();
         if (tid == 0) s_state = wait_partials(a, td, pos);
         __syncthreads();
-        if (s_state < 0) break;
+        skip = __builtin_amdgcn_readfirstlane(s_state) < 0;
         const int64_t prow = td.row_begin - a.own_row0;
-        for (int j = 0; j < a.n_peers; ++j) {
+        for (int j = 0; j < (skip ? 0 : a.n_peers); ++j) {
           const __amdgpu_buffer_rsrc_t rsP =
               make_rsrc(a.partials + ((static_cast<int64_t>(j) * a.own_rows + prow) * a.N + col0) * kOutBytes,
                         static_cast<int64_t>(g.arows) * a.N * kOutBytes);
@@ -855,7 +860,11 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
     }
 
     const int nslices = td.slice >> 16;
-    if (nslices == 2) {
+    // false when this unit only left partial sums for another slice of its tile
+    bool wrote = true;
+    if (skip) {
+      wrote = false;
+    } else if (nslices == 2) {
       // Split in two along K. The slice that gets here second (low half of the tile's
       // slot word) keeps its partial sums in registers, waits until the other slice has
       // stored its own (high half) and writes the output from the sum of the two
@@ -870,7 +879,7 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
       if (tid == 0)
         s_state = (__hip_atomic_fetch_add(word, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & 0xffffu) == 1u;
       __syncthreads();
-      if (!s_state) {
+      if (!__builtin_amdgcn_readfirstlane(s_state)) {
 #pragma unroll
         for (int r = 0; r < kRuns; ++r)
           __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc_run(r)), rsW, toff,
@@ -880,25 +889,28 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
         else wait_dma_all();
         __syncthreads();
         if (tid == 0) __hip_atomic_fetch_add(word, 1u << 16, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (a.trace && tid == 0) {
-          a.trace[kTraceWords * pos + 2] = wall_clock64();
-          a.trace[kTraceWords * pos + 5] = clock64();
+        wrote = false;
+      } else {
+        // the other slice has arrived, so it is only storing: a short, bounded wait
+        if (tid == 0) s_state = wait_slices_stored(a, word, 1, pos);
+        __syncthreads();
+        skip = __builtin_amdgcn_readfirstlane(s_state) < 0;
+        if (!skip) {
+          if (a.steal) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+          else asm volatile("buffer_inv sc0" ::: "memory");  // drop this CU's L1 copy, if any
+          skip = !wait_previous_copy_out();
         }
-        continue;
+        if (!skip) {
+          const int other = (1 - me) * kSliceBytes;
+          add_stored_pair<kRuns>(
+              [&](int r) -> f32x4 {
+                return __builtin_bit_cast(
+                    f32x4, __builtin_amdgcn_raw_buffer_load_b128(rsW, toff, other + r * kThreads * 16, 0));
+              },
+              acc_run, store_run);
+        }
+        wrote = !skip;
       }
-      // the other slice has arrived, so it is only storing: a short, bounded wait
-      if (tid == 0) s_state = wait_slices_stored(a, word, 1, pos);
-      __syncthreads();
-      if (s_state < 0) break;
-      if (a.steal) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-      else asm volatile("buffer_inv sc0" ::: "memory");  // drop this CU's L1 copy, if any
-      if (!wait_previous_copy_out()) break;
-      const int other = (1 - me) * kSliceBytes;
-      add_stored_pair<kRuns>(
-          [&](int r) -> f32x4 {
-            return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rsW, toff, other + r * kThreads * 16, 0));
-          },
-          acc_run, store_run);
     } else if (nslices > 2) {
       // Split along K in more than two: store this slice's partial sums; the slice that
       // finishes its tile last adds all of them in slice order (so the result does not
@@ -925,31 +937,34 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
         s_state = (__hip_atomic_fetch_add(a.slot_count + a.raster[pos], 1u, __ATOMIC_RELAXED,
                                           __HIP_MEMORY_SCOPE_AGENT) == static_cast<uint32_t>(nslices - 1));
       __syncthreads();
-      if (!s_state) {
-        if (a.trace && tid == 0) {
-          a.trace[kTraceWords * pos + 2] = wall_clock64();
-          a.trace[kTraceWords * pos + 5] = clock64();
+      if (!__builtin_amdgcn_readfirstlane(s_state)) {
+        wrote = false;
+      } else {
+        if (a.steal) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        else asm volatile("buffer_inv sc0" ::: "memory");
+        skip = !wait_previous_copy_out();
+        if (!skip) {
+          auto load_part = [&](int sl, int r) -> f32x4 {
+            return __builtin_bit_cast(
+                f32x4, __builtin_amdgcn_raw_buffer_load_b128(rsW, toff, sl * kSliceBytes + r * kThreads * 16, 0));
+          };
+          reduce_slices<kRuns>(nslices, load_part, store_run);
         }
-        continue;
+        wrote = !skip;
       }
-      if (a.steal) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-      else asm volatile("buffer_inv sc0" ::: "memory");
-      if (!wait_previous_copy_out()) break;
-      auto load_part = [&](int sl, int r) -> f32x4 {
-        return __builtin_bit_cast(f32x4,
-                                  __builtin_amdgcn_raw_buffer_load_b128(rsW, toff, sl * kSliceBytes + r * kThreads * 16, 0));
-      };
-      reduce_slices<kRuns>(nslices, load_part, store_run);
     } else {
-      if (!wait_previous_copy_out()) break;
+      skip = !wait_previous_copy_out();
+      if (!skip) {
 #pragma unroll
-      for (int r = 0; r < kRuns; ++r) {
-        store_run(r, acc_run(r));
-        __builtin_amdgcn_sched_barrier(0);  // convert-and-store one run at a time
+        for (int r = 0; r < kRuns; ++r) {
+          store_run(r, acc_run(r));
+          __builtin_amdgcn_sched_barrier(0);  // convert-and-store one run at a time
+        }
       }
+      wrote = !skip;
     }
 
-    if constexpr (kProducer) {
+    if (kProducer && wrote) {
       // This wave's C stores (system-coherent, written through to memory) have
       // completed before the workgroup counts the tile. The counter and flag updates
       // are relaxed system-scope atomics, performed at the memory side; they are

@@ -156,6 +156,24 @@ def test_validation_errors():
                    device=-1) == csg.CSG_OK
 
 
+def test_every_op_rejects_more_chunks_than_the_kernels_track():
+    """The kernels keep one bit per chunk of the chunks a workgroup has seen ready; the
+    producers (GEMM-RS, GEMM-AR) wait on that bitmap too, before rewriting a chunk's rows
+    of C. A plan with more chunks than the bitmap holds is rejected for every op."""
+    W, S, Q = 2, 4096, 4096                      # 8192 one-row chunks
+    s = csg.Schedule.uniform(W, 0, S, Q, "rs_ring")
+    for op in ("ag", "rs", "ar"):
+        try:
+            csg.Plan(op, W * S, 64, 64, "bf16", "bf16", s, device=-1)
+            raise AssertionError("%s plan with %d chunks accepted" % (op, W * Q))
+        except csg.CsgError as e:
+            assert e.status == csg.CSG_ERR_UNSUPPORTED, op
+            assert "at most 4096 chunks" in str(e), (op, str(e))
+    ok = csg.Schedule.uniform(W, 0, 2048, 2048, "rs_ring")   # exactly 4096 chunks
+    for op in ("ag", "rs", "ar"):
+        assert _status(csg.Plan, op, W * 2048, 64, 64, "bf16", "bf16", ok, device=-1) == csg.CSG_OK, op
+
+
 def test_kernel_copy_backend_validation():
     s = csg.Schedule.uniform(2, 0, 64, 2, "ring")
     for bad in ({"copy_backend": 2}, {"copy_backend": -1}, {"copy_workgroups": -1}, {"copy_workgroups": 5000}):

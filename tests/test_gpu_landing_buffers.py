@@ -147,3 +147,41 @@ def test_calls_alternating_compute_streams(n_buffers):
     refs = [oracle.ag_gemm(d.A.device_array, sets[0].B.device_array, chunks, order) for d in sets]
     for i in range(calls):
         assert_close(out_to_f64(outs[i], "bf16"), refs[i % 3], tol_for("bf16", "bf16"), "call %d" % i)
+
+
+def test_copy_only_call_on_a_busy_stream_then_other_streams():
+    """A copy-only call queues a prologue (it clears a per-call state set) and no kernel.
+    Queued on a stream that is still busy with other work, that prologue runs late; the
+    calls that follow on other compute streams must wait for it, or it would clear the
+    state of a kernel already running. Every overlap call's output must match its inputs."""
+    _say("copy-only call on a busy stream, then calls on two other streams")
+    chunks, order, sets = _inputs(3)
+    M = W * S
+    sts = [streams(), streams(), streams()]
+    b = to_dev(sets[0].B.device_array)
+    stage = [to_dev(d.A.device_array) for d in sets]
+    landing = stage[0].clone()
+    modes = ["overlap", "copy_only", "overlap", "overlap", "copy_only", "overlap", "overlap"]
+    outs = [empty_out(M, N, "bf16") for _ in modes]
+    for o in outs:
+        nan_fill_(o)
+    s = csg.Schedule.uniform(W, R, S, Q, KIND)
+    plan = csg.Plan("ag", M, N, K, "bf16", "bf16", s, cfg={"timeout_ms": 2000})
+    x = torch.randn(2048, 2048, device=DEV)
+    torch.cuda.synchronize()
+    for i, mode in enumerate(modes):
+        if mode == "copy_only":
+            st = sts[2]
+            with torch.cuda.stream(st.compute):
+                y = x
+                for _ in range(8):          # a few ms of unrelated work ahead of the prologue
+                    y = torch.mm(y, x)
+        else:
+            st = sts[i % 2]
+        plan.ag_gemm(landing, stage[i % 3], b, outs[i], mode, st.compute, st.copy)
+    plan.check()
+    torch.cuda.synchronize()
+    refs = [oracle.ag_gemm(d.A.device_array, sets[0].B.device_array, chunks, order) for d in sets]
+    for i, mode in enumerate(modes):
+        if mode == "overlap":
+            assert_close(out_to_f64(outs[i], "bf16"), refs[i % 3], tol_for("bf16", "bf16"), "call %d" % i)
