@@ -1,23 +1,32 @@
 #!/usr/bin/env python3
 """Benchmark: chunk-scheduled GEMM TFLOP/s on one MI355X, with compute/copy overlap.
 
-One step = one call of the whole path on one batch of synthetic input: the
-prologue, the SDMA chunk copies whose completion signals are the per-chunk flags,
-and the persistent chunk-ordered GEMM kernel, in overlap mode. Steps run back to
-back, as in a layer loop where each layer gathers into its own activation: the
-all-gather and grouped workloads alternate between two landing buffers
-(--landing-buffers), so a step's copies wait only for the kernel two steps back to
-have read the rows they overwrite (the library tracks that per buffer), and the same
-loop with one landing buffer is reported beside it. The default workload is the
-all-gather GEMM of 8 simulated ranks (A 8192 x 4096 bf16 in 8 shards of 4
-chunks, ring arrival; B 4096 x 1792; fp32 accumulation, bf16 output).
+One step = one call of the whole path on one batch of synthetic input: the SDMA chunk
+copies whose completion signals are the per-chunk flags, and the persistent
+chunk-ordered GEMM kernel, in overlap mode. The default workload is the largest one:
+the all-gather GEMM of 8 simulated ranks with fine chunks (A 16384 x 8192 bf16 in 8
+shards of 16 chunks of 128 rows, seeded arrival order, per-chunk release delays drawn
+from U[0, 20] us; B 8192 x 3584; fp32 accumulation, bf16 output).
 
-Prints ONE JSON line. Besides the contract fields it reports, from separate
-phases after the timed region, isolated-call times of the overlap, compute-only
-and copy-only modes of the same workload and the overlap efficiency
-max(t_compute, t_copy) / t_total; the roofline of the GEMM kernel (its durations
-in the timed region, from timing events the library records around each launch);
-and the CPU oracle timed on a bounded sample.
+The timed region is `--steps` back-to-back overlap calls that all gather into the same
+landing buffer, as consecutive calls of one layer do: a call's copy of a chunk waits
+until the previous call's kernel has read that chunk's rows.
+
+Prints ONE JSON line. Besides the contract fields it reports, from separate phases
+after the timed region:
+- isolated calls, cold: before each one a 512 MiB write evicts the inputs from the
+  last-level cache and the L2s; each call is timed on the device, from an event on the
+  compute stream before the call to an event after csg_plan_join (the end of the
+  call's kernel and of every copy it issued); median, p10 and p90 of overlap,
+  compute-only and copy-only calls, and the per-call overlap efficiency
+  max(t_compute, t_copy) / t_total;
+- the steady state of the same back-to-back loop in compute-only and copy-only mode,
+  and the overlap loop gathering into two landing buffers in turn (the next call's
+  copies then run under this call's kernel);
+- the roofline of the GEMM kernel: its durations in the timed region (timing events
+  the library records around each launch) against the nominal bf16 MFMA peak and the
+  peak the MFMA microbenchmark measures on the device;
+- the CPU oracle timed on a bounded sample.
 """
 from __future__ import annotations
 
@@ -34,7 +43,8 @@ sys.path.insert(0, ROOT)
 
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}  # MI355X dense MFMA peaks
 HBM_PEAK_GBS = 8000.0
-CAL_BYTES = 256 << 20  # bytes read (and written) by the calibration copy
+CAL_BYTES = 256 << 20    # bytes read (and written) by the calibration copy
+FLUSH_BYTES = 512 << 20  # written before each isolated call: more than the last-level cache and every L2
 
 
 def parse():
@@ -42,17 +52,22 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=2, help="workload id (1..7; 6 = GEMM + all-reduce, 7 = ring attention)")
+    ap.add_argument("--config", type=int, default=4,
+                    help="workload id (1..7; 4 = the headline, 6 = GEMM + all-reduce, 7 = ring attention)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target length of the CPU baseline sample")
     ap.add_argument("--lanes", type=int, default=0, help="SDMA copy lanes (0 = library default)")
     ap.add_argument("--no-kernel-copies", action="store_true",
                     help="skip the comparison with chunks moved by the kernel's own workgroups")
-    ap.add_argument("--landing-buffers", type=int, default=2,
-                    help="all-gather and grouped workloads: consecutive steps gather into this many landing "
-                         "buffers in turn (as consecutive layers gather into their own activations); 1 = every "
-                         "step into the same buffer")
+    ap.add_argument("--isolated-reps", type=int, default=0,
+                    help="cold isolated calls per mode (0 = as many as --steps)")
+    ap.add_argument("--plan-cfg", type=str, default="",
+                    help="JSON object of plan configuration fields for the measured plan (e.g. tile order)")
     return ap.parse_args()
+
+
+def pct(a, q):
+    return round(float(np.percentile(np.asarray(a), q)), 4)
 
 
 def main():
@@ -85,7 +100,10 @@ def main():
     else:
         sched = csg.Schedule.uniform(w.world, w.rank, w.shard_rows, w.chunks_per_shard, w.order, d.perm)
         group_rows = None
-    cfg = {"copy_engines": args.lanes} if args.lanes else None
+    cfg = {"copy_engines": args.lanes} if args.lanes else {}
+    if args.plan_cfg:
+        cfg.update(json.loads(args.plan_cfg))
+    cfg = cfg or None
     if w.op == "attn":
         e = w.extras
         plan = csg.AttnPlan(e["heads"], e["kv_heads"], e["head_dim"], w.M, sched, cfg=cfg)
@@ -95,6 +113,11 @@ def main():
         plan.set_copy_delays(d.delays_us)
     chunks, _ = sched.get()
     remote_rows = sum(c[1] - c[0] for c in chunks if not c[4])
+
+    # the MFMA microbenchmark first, on an idle device: a short run and one about as long
+    # as the workload's kernel (the clock falls as a longer run heats the device)
+    peak_short = csg.csg_measure_mfma_peak(0, 800)
+    peak_long = csg.csg_measure_mfma_peak(0, 8000)
 
     a_full = to_dev(d.A.device_array)
     b = to_dev(d.B.device_array)
@@ -131,9 +154,7 @@ def main():
         landing = a_full.clone()
         outgoing = None
         moved_bytes = remote_rows * w.K * in_bytes
-    # landing buffers used in turn by consecutive steps (all-gather and grouped)
-    landings = [landing] + [landing.clone() for _ in range(max(args.landing_buffers, 1) - 1)] if landing is not None \
-        else [None]
+    landings = [landing]   # the timed region: every step gathers into the same buffer
     compute = torch.cuda.Stream(device=dev)
     copy = torch.cuda.Stream(device=dev)
     # plain device-to-device copy of known size, run once before the timed region: the
@@ -142,6 +163,7 @@ def main():
     cal_dst = torch.empty_like(cal_src)
     cal_dst.copy_(cal_src)
     del cal_src, cal_dst
+    flush_buf = torch.empty(FLUSH_BYTES // 4, dtype=torch.int32, device=dev)
     torch.cuda.synchronize()
 
     def call(mode, p=None, step=0):
@@ -177,22 +199,29 @@ def main():
         wall = time.perf_counter() - t0
         return wall, p.kernel_times(steps)
 
-    def bracketed(mode, reps, warmup):
-        """Isolated calls (the GPU idle before each): per call, the wall time from the
-        call to its kernel and every copy having completed (ms)."""
+    def isolated(mode, reps, warmup):
+        """Cold isolated calls: the caches flushed and the device idle before each one;
+        per call, the device time (ms) from an event queued on the compute stream just
+        before the call to one queued after csg_plan_join (the call's kernel and every
+        copy it issued have completed)."""
         for _ in range(warmup):
             call(mode)
         plan.check()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
         tot = []
-        for _ in range(reps):
+        for i in range(reps):
+            with torch.cuda.stream(compute):
+                flush_buf.fill_(i)
             torch.cuda.synchronize()
-            t0 = time.perf_counter()
+            ev0.record(compute)
             call(mode)
+            plan.join(compute)
+            ev1.record(compute)
+            ev1.synchronize()
             plan.check()
-            torch.cuda.synchronize()
-            tot.append((time.perf_counter() - t0) * 1e3)
-        ker = plan.kernel_times(reps) if mode != "copy_only" else np.array([])
-        return np.array(tot), ker
+            tot.append(ev0.elapsed_time(ev1))
+        return np.array(tot)
 
     # ---- the timed region: overlap steps ------------------------------------------
     wall, ker = timed_loop("overlap", args.steps, args.warmup)
@@ -204,30 +233,36 @@ def main():
     wall_x, _ = timed_loop("copy_only", args.steps, args.warmup)
     ms_comp = wall_c * 1e3 / args.steps
     ms_copy = wall_x * 1e3 / args.steps
-    overlap_eff = max(ms_comp, ms_copy) / ms_per_step
-    ms_one_landing = None
-    if len(landings) > 1:
-        # the same overlap loop with every step gathering into one landing buffer: a
-        # step's copy of a chunk then waits for the previous step's kernel to have read it
-        kept = list(landings)
-        landings[:] = kept[:1]
-        wall_1, _ = timed_loop("overlap", args.steps, args.warmup)
-        landings[:] = kept
-        ms_one_landing = wall_1 * 1e3 / args.steps
-    # isolated calls: each mode timed alike (the call until its kernel and copies are
-    # done, GPU idle before)
-    tot, _ = bracketed("overlap", args.steps, args.warmup)
-    tot_c, _ = bracketed("compute_only", args.steps, args.warmup)
-    tot_x, _ = bracketed("copy_only", args.steps, args.warmup)
+    ms_two_landing = None
+    if landing is not None:
+        # the overlap loop gathering into two landing buffers in turn: the next step's
+        # copies may run under this step's kernel (a pipeline a dependent layer chain
+        # cannot build)
+        landings.append(landing.clone())
+        wall_2, _ = timed_loop("overlap", args.steps, args.warmup)
+        del landings[1:]
+        ms_two_landing = wall_2 * 1e3 / args.steps
+    # cold isolated calls, each mode alike
+    reps = args.isolated_reps or max(args.steps, 10)
+    tot = isolated("overlap", reps, args.warmup)
+    tot_c = isolated("compute_only", reps, args.warmup)
+    tot_x = isolated("copy_only", reps, args.warmup)
     t_total = float(np.median(tot))
     t_comp = float(np.median(tot_c))
     t_copy = float(np.median(tot_x))
-    overlap_eff_isolated = max(t_comp, t_copy) / t_total
+    overlap_eff = max(t_comp, t_copy) / t_total
 
     peak = MFMA_PEAK_TFLOPS[w.dtype]
     k_overlap = float(np.mean(ker))
     k_comp = float(np.mean(ker_c))
     kernel_name = "ring_attn" if w.op == "attn" else "chunk_gemm"
+    tf_overlap = w.flops / (k_overlap * 1e-3) / 1e12
+    tf_comp = w.flops / (k_comp * 1e-3) / 1e12
+    measured = {"short": {"tflops": round(peak_short[0], 1), "ms": round(peak_short[1], 4),
+                          "ghz": round(peak_short[2], 3)},
+                "sustained": {"tflops": round(peak_long[0], 1), "ms": round(peak_long[1], 4),
+                              "ghz": round(peak_long[2], 3)}}
+    mpeak = peak_long[0] if w.dtype == "bf16" else None
     rec = {
         "metric": "chunk-scheduled GEMM TFLOP/s @1 GPU; overlap eff = max(comp,copy)/total",
         "value": round(value, 2),
@@ -243,30 +278,40 @@ def main():
         "data": "synthetic (seeded %s values)" % w.dist,
         "config": {"workload": w.name, "op": w.op, "M": w.M, "N": w.N, "K": w.K, "world": w.world,
                    "chunks": len(chunks), "moved_bytes": moved_bytes, "arch": arch,
+                   "copy_delays": "cumulative release times, U[0,20] us each" if d.delays_us is not None else None,
                    "num_workgroups": plan.info.num_workgroups,
                    "tile": [plan.info.bm, plan.info.bn, plan.info.bk],
-                   "landing_buffers": len(landings) if landing is not None else None},
+                   "plan_cfg": cfg or {},
+                   "landing_buffers": 1 if landing is not None else None},
+        # cold isolated calls (device events; caches flushed before each)
+        "overlap_eff": round(overlap_eff, 4),
+        "t_total_ms": {"median": round(t_total, 4), "p10": pct(tot, 10), "p90": pct(tot, 90)},
+        "t_compute_only_ms": {"median": round(t_comp, 4), "p10": pct(tot_c, 10), "p90": pct(tot_c, 90)},
+        "t_copy_only_ms": {"median": round(t_copy, 4), "p10": pct(tot_x, 10), "p90": pct(tot_x, 90)},
+        "isolated": {"reps": reps, "cache_flush_bytes": FLUSH_BYTES,
+                     "timing": "device events: compute stream before the call .. after csg_plan_join"},
+        "e2e_tflops_isolated": round(w.flops / (t_total * 1e-3) / 1e12, 2),
+        "copy_GBps_isolated": round(moved_bytes / (t_copy * 1e-3) / 1e9, 2),
         # steady state: ms per step of back-to-back loops in each mode
         "ms_per_step_compute_only": round(ms_comp, 4),
         "ms_per_step_copy_only": round(ms_copy, 4),
-        "overlap_eff": round(overlap_eff, 4),
-        "ms_per_step_one_landing_buffer": None if ms_one_landing is None else round(ms_one_landing, 4),
+        "overlap_eff_steady": round(max(ms_comp, ms_copy) / ms_per_step, 4),
+        "ms_per_step_two_landing_buffers": None if ms_two_landing is None else round(ms_two_landing, 4),
+        "overlap_eff_steady_two_landing_buffers":
+            None if ms_two_landing is None else round(max(ms_comp, ms_copy) / ms_two_landing, 4),
         "compute_only_tflops": round(w.flops / (ms_comp * 1e-3) / 1e12, 2),
-        "copy_only_GBps": round(moved_bytes / (ms_copy * 1e-3) / 1e9, 2),
-        # one isolated call per mode (median)
-        "t_total_ms_median": round(t_total, 4),
-        "t_compute_only_ms_median": round(t_comp, 4),
-        "t_copy_only_ms_median": round(t_copy, 4),
-        "overlap_eff_isolated": round(overlap_eff_isolated, 4),
-        "roofline": {"bound": "mfma", "achieved": round(w.flops / (k_overlap * 1e-3) / 1e12, 2), "peak": peak,
-                     "unit": "TFLOP/s", "frac": round(w.flops / (k_overlap * 1e-3) / 1e12 / peak, 4),
+        "roofline": {"bound": "mfma", "achieved": round(tf_overlap, 2), "peak": peak,
+                     "unit": "TFLOP/s", "frac": round(tf_overlap / peak, 4),
                      "traffic": kernel_traffic(w.name, kernel_name), "kernel": kernel_name,
                      "phase": "overlap (timed region)",
-                     "kernel_ms_mean": round(k_overlap, 4)},
-        "roofline_compute_only": {"bound": "mfma", "achieved": round(w.flops / (k_comp * 1e-3) / 1e12, 2),
+                     "kernel_ms_mean": round(k_overlap, 4),
+                     "frac_of_measured_peak": round(tf_overlap / mpeak, 4) if mpeak else None},
+        "roofline_compute_only": {"bound": "mfma", "achieved": round(tf_comp, 2),
                                   "peak": peak, "unit": "TFLOP/s",
-                                  "frac": round(w.flops / (k_comp * 1e-3) / 1e12 / peak, 4),
-                                  "kernel_ms_mean": round(k_comp, 4)},
+                                  "frac": round(tf_comp / peak, 4),
+                                  "kernel_ms_mean": round(k_comp, 4),
+                                  "frac_of_measured_peak": round(tf_comp / mpeak, 4) if mpeak else None},
+        "mfma_peak_measured": measured,
     }
     if not args.no_kernel_copies and w.op not in ("ar", "attn"):  # these copy with the engines only
         rec["kernel_copy_backend"] = kernel_copy_sweep(w, sched, group_rows, d, timed_loop, moved_bytes, args)
@@ -336,6 +381,17 @@ def kernel_traffic(workload: str, kernel: str = "chunk_gemm"):
     return entry.get("bytes_per_launch")
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, d, chunks, target_s):
     """The oracle as it stands, timed on a bounded sample of the same workload: whole
     output rows of the chunks in arrival order, grown until about target_s seconds."""
@@ -366,6 +422,7 @@ def cpu_baseline(w, d, chunks, target_s):
         except Exception:
             cores = 1
         return {"value": round(flops / t / 1e12, 6), "unit": "TFLOP/s", "cores": cores,
+                "affinity_cores": len(os.sched_getaffinity(0)), "cpu_model": cpu_model(),
                 "kind": "oracle", "seconds": round(t, 3),
                 "sample": "%d of %d query rows, all %d heads, all %d keys, fp64 numpy attention"
                           % (n, w.M, e["heads"], K.shape[0])}
@@ -392,6 +449,7 @@ def cpu_baseline(w, d, chunks, target_s):
     t = run(rows_all[:n])
     flops = 2.0 * n * w.N * w.K
     return {"value": round(flops / t / 1e12, 6), "unit": "TFLOP/s", "cores": oracle.num_threads(),
+            "affinity_cores": len(os.sched_getaffinity(0)), "cpu_model": cpu_model(),
             "kind": "oracle", "seconds": round(t, 3),
             "sample": "%d of %d output rows (first rows in chunk row order), all %d columns, K=%d, fp64 plain loops"
                       % (n, w.M, w.N, w.K)}

@@ -9,10 +9,11 @@
  * are staged in HBM and moved by SDMA copy-engine copies (Section 2.3, copy
  * engine backend; Section 5.2, realization (1): copy engine + global-memory
  * signals). Copies are issued by the calling thread straight to the SDMA engines.
- * An overlap GEMM call returns once its copies are issued (its kernel waits for each
- * chunk's copy, csg_plan_check for all of them); ring attention and copy-only calls
- * return once their copies have completed. Either way the kernel may still be running
- * on the compute stream.
+ * Overlap GEMM calls and every copy-only call return once their copies are issued (an
+ * overlap kernel waits for each chunk's copy; csg_plan_check waits for all of them,
+ * and csg_plan_join makes a stream wait for them on the device); ring-attention
+ * overlap calls return once their copies have completed. Either way the kernel may
+ * still be running on the compute stream.
  *
  * Conventions for every entry point
  *   - Every call returns csg_status; nothing throws or aborts across the ABI.
@@ -286,7 +287,8 @@ csg_status csg_plan_set_copy_delays(csg_plan* p, const float* delay_us_host, int
  * read every chunk; a buffer no earlier call of the plan overlaps (say, the other
  * of two activations used in turn) needs no wait. In overlap mode the call returns
  * once every copy is issued (the kernel waits for each, and csg_plan_check for
- * all); in copy-only mode it returns when the copies have completed. The kernel runs
+ * all); so does copy-only mode (csg_plan_check or csg_plan_join wait for the
+ * copies). The kernel runs
  * tiles in chunk order, each waiting for its chunks. Work queued on `compute`
  * afterwards is ordered after the kernel. Asynchronous failures (a flag wait that
  * timed out) surface through csg_plan_check. CSG_ERR_TIMEOUT if a host wait
@@ -373,7 +375,8 @@ csg_status csg_attn_plan_create(int32_t n_heads, int32_t n_kv_heads, int32_t hea
  * over all S keys (no mask). As for csg_ag_gemm: the kernel is queued on `compute`,
  * the calling thread copies each remote chunk's keys and values by SDMA (two copies,
  * one completion signal as the chunk's ready flag) once the previous call's kernel
- * has finished reading those rows, and returns when the copies have completed. Each
+ * has finished reading those rows, and returns when the copies have completed
+ * (copy-only mode: once they are issued, as for csg_ag_gemm). Each
  * work unit (one head, 128 query rows) consumes the chunks in arrival order, waiting
  * for each once. Compute-only: the landing buffers must already hold every row. */
 csg_status csg_ring_attn(csg_plan* p, const void* q, void* k_landing, void* v_landing,
@@ -386,6 +389,28 @@ csg_status csg_ring_attn(csg_plan* p, const void* q, void* k_landing, void* v_la
  * finished without running every work unit (which only a grid that leaves a die
  * without workgroups can cause); CSG_OK otherwise. */
 csg_status csg_plan_check(csg_plan* p, csg_diag* out);
+
+/* Makes `stream` (a hipStream_t of the plan's device) wait, on the device, until every
+ * copy the plan's last call issued has completed: a one-thread kernel is queued on it
+ * that polls the copies' completion signals, at most the plan's timeout_ms per copy
+ * (a copy still running then is reported by csg_plan_check, not here). Work queued on
+ * `stream` afterwards follows the copies without a host wait, e.g. a consumer of
+ * GEMM-RS's outgoing buffer, or an event that timestamps the end of the call's copies.
+ * Queued on the call's compute stream it also follows the call's kernel. Enqueues
+ * nothing for plans whose kernel moves the chunks itself (CSG_COPY_KERNEL: the kernel
+ * covers its copies) or that never ran. CSG_ERR_STATE on a host-only plan. */
+csg_status csg_plan_join(csg_plan* p, void* stream);
+
+/* MFMA microbenchmark (a measurement aid, not part of any call above): one workgroup
+ * of four waves per CU of `device`, each wave issuing `iters` rounds of 8 independent
+ * bf16 32x32x16 MFMAs on register operands. *tflops receives the dense bf16 rate the
+ * device sustained (2 * 32 * 32 * 16 flops per MFMA over the dispatch's own start and
+ * end timestamps), *ms (may be NULL) the kernel's duration and *ghz (may be NULL) the
+ * shader clock of workgroup 0 over its loop. The rate falls with the clock as a longer
+ * run heats the device, so the measured peak depends on iters (about 1 ms per 7800
+ * iterations at 2 GHz). Allocates and frees its own small buffers; synchronous.
+ * CSG_ERR_UNSUPPORTED unless the device is gfx950. */
+csg_status csg_measure_mfma_peak(int device, int32_t iters, double* tflops, double* ms, double* ghz);
 
 /* Durations of the plan's most recent GEMM kernel launches, oldest first: the time
  * between two timing events the library records on the compute stream right

@@ -48,7 +48,8 @@ ABI_FUNCTIONS = (
     "csg_schedule_get", "csg_schedule_destroy",
     "csg_plan_create", "csg_plan_info_get", "csg_plan_get_map", "csg_plan_set_copy_delays",
     "csg_ag_gemm", "csg_gemm_rs", "csg_gemm_ar", "csg_grouped_gemm", "csg_plan_check", "csg_plan_kernel_times",
-    "csg_plan_trace", "csg_plan_destroy", "csg_attn_plan_create", "csg_ring_attn",
+    "csg_plan_trace", "csg_plan_destroy", "csg_attn_plan_create", "csg_ring_attn", "csg_plan_join",
+    "csg_measure_mfma_peak",
 )
 
 
@@ -132,6 +133,9 @@ def _lib():
         "csg_plan_kernel_times": ([vp, P(ctypes.c_float), i32, P(i32)], st),
         "csg_plan_trace": ([vp, P(csg_trace_unit), i32, P(i32)], st),
         "csg_plan_destroy": ([vp], None),
+        "csg_plan_join": ([vp, vp], st),
+        "csg_measure_mfma_peak": ([ctypes.c_int, i32, P(ctypes.c_double), P(ctypes.c_double), P(ctypes.c_double)],
+                                  st),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -375,6 +379,19 @@ def csg_plan_check(plan: int) -> csg_diag:
     return d
 
 
+def csg_plan_join(plan: int, stream) -> None:
+    """Queues on `stream` a wait, on the device, for every copy of the plan's last call."""
+    _check(_lib().csg_plan_join(plan, _stream(stream)), "csg_plan_join")
+
+
+def csg_measure_mfma_peak(device: int = 0, iters: int = 4096):
+    """(TFLOP/s, ms, GHz) of the MFMA microbenchmark: dense bf16 rate on every SIMD."""
+    tf, ms, ghz = ctypes.c_double(0), ctypes.c_double(0), ctypes.c_double(0)
+    _check(_lib().csg_measure_mfma_peak(device, iters, ctypes.byref(tf), ctypes.byref(ms), ctypes.byref(ghz)),
+           "csg_measure_mfma_peak")
+    return tf.value, ms.value, ghz.value
+
+
 def csg_plan_kernel_times(plan: int, n: int = 256) -> np.ndarray:
     """Durations (ms) of the plan's last n kernel launches, oldest first."""
     buf = np.zeros(max(n, 1), dtype=np.float32)
@@ -499,6 +516,9 @@ class Plan:
 
     def kernel_times(self, n: int = 256) -> np.ndarray:
         return csg_plan_kernel_times(self.handle, n)
+
+    def join(self, stream) -> None:
+        csg_plan_join(self.handle, stream)
 
     def trace(self) -> np.ndarray:
         return csg_plan_trace(self.handle, self.info.n_units)

@@ -152,6 +152,11 @@ struct csg_plan {
   uint32_t landing_dropped = 0;
   uint32_t* h_out_flags_dev = nullptr; // its device address
   uint32_t* d_scratch = nullptr;       // target of the engines' warm-up copies
+  // csg_plan_join: per signal set, the value pointers of every copy signal of the set
+  // (copies in, copies out, sends, partials), and the join kernel's timeout word
+  const int64_t** d_join[2] = {nullptr, nullptr};
+  int32_t n_join[2] = {0, 0};
+  uint32_t* d_join_flag = nullptr;
   csg::SdmaEngines sdma;
   // Completion signals of the chunk copies, per set (calls alternate sets), per remote
   // chunk position: consumers' copies in, the producer's copies out.
@@ -247,7 +252,9 @@ void free_plan_device(csg_plan* p) {
                     static_cast<void*>(p->d_copy_done), static_cast<void*>(p->d_kready),
                     static_cast<void*>(p->d_ready_k), static_cast<void*>(p->d_chunk_sent),
                     static_cast<void*>(p->d_copy_state), static_cast<void*>(p->d_release_ticks),
-                    static_cast<void*>(p->d_arrival), static_cast<void*>(p->d_chunk_rows)})
+                    static_cast<void*>(p->d_arrival), static_cast<void*>(p->d_chunk_rows),
+                    static_cast<void*>(p->d_join[0]), static_cast<void*>(p->d_join[1]),
+                    static_cast<void*>(p->d_join_flag)})
     if (ptr) (void)hipFree(ptr);
   if (p->h_out_flags) (void)hipHostFree(p->h_out_flags);
   for (hipEvent_t e : {p->ev_copy_in, p->ev_prologue, p->ev_kernel_done[0], p->ev_kernel_done[1]})
@@ -269,6 +276,27 @@ csg_status upload(T** dst, const std::vector<T>& src) {
 
 int64_t in_bytes(const csg_plan* p) { return p->in_dtype == CSG_BF16 ? 2 : 4; }
 int64_t out_bytes(const csg_plan* p) { return p->out_dtype == CSG_BF16 ? 2 : 4; }
+
+// The join tables of csg_plan_join: per signal set, the completion values of every copy
+// signal the set holds.
+csg_status setup_join(csg_plan* p) {
+  for (int set = 0; set < 2; ++set) {
+    std::vector<const int64_t*> ptrs;
+    for (auto* sets : {p->sig_ready, p->sig_send, p->sig_part})
+      for (hsa_signal_t sgn : sets[set]) {
+        const int64_t* vp = nullptr;
+        const hsa_status_t hs = p->sdma.signal_value_ptr(sgn, &vp);
+        if (hs != HSA_STATUS_SUCCESS) return fail(CSG_ERR_HIP, "copy signal: %s", csg::hsa_error(hs).c_str());
+        ptrs.push_back(vp);
+      }
+    p->n_join[set] = static_cast<int32_t>(ptrs.size());
+    const csg_status st = upload(&p->d_join[set], ptrs);
+    if (st != CSG_OK) return st;
+  }
+  CSG_HIP(hipMalloc(&p->d_join_flag, 4));
+  CSG_HIP(hipMemset(p->d_join_flag, 0, 4));
+  return CSG_OK;
+}
 
 csg_status setup_device(csg_plan* p) {
   DeviceGuard g(p->device);
@@ -460,6 +488,7 @@ csg_status setup_device(csg_plan* p) {
     CSG_HIP(hipEventCreate(&p->ev_k1[i]));
   }
   CSG_HIP(hipStreamCreateWithFlags(&p->aux, hipStreamNonBlocking));
+  if ((st = setup_join(p)) != CSG_OK) return st;
   CSG_HIP(hipDeviceSynchronize());
   return CSG_OK;
 }
@@ -938,6 +967,7 @@ csg_status setup_attn_device(csg_plan* p) {
     CSG_HIP(hipEventCreate(&p->ev_k1[i]));
   }
   CSG_HIP(hipStreamCreateWithFlags(&p->aux, hipStreamNonBlocking));
+  if ((st = setup_join(p)) != CSG_OK) return st;
   CSG_HIP(hipDeviceSynchronize());
   return CSG_OK;
 }
@@ -1049,7 +1079,10 @@ csg_status consumer_call(csg_plan* p, void* landing, const void* staging, const 
     p->copies_in_flight = false;
     return CSG_OK;
   }
-  return finish_copies(p, p->remote_order.size());
+  // Copy-only: the copies complete on their own. The next call waits for them before it
+  // arms a signal again, csg_plan_check waits for them, and csg_plan_join makes a
+  // stream wait for them on the device.
+  return CSG_OK;
 }
 
 }  // namespace
@@ -1547,6 +1580,7 @@ csg_status csg_ring_attn(csg_plan* p, const void* q, void* k_landing, void* v_la
     return st;
   if (!copies) return CSG_OK;
   if ((st = issuer.run(true)) != CSG_OK) return st;
+  if (mode == CSG_MODE_COPY_ONLY) return CSG_OK;  // as for the GEMMs: the copies complete on their own
   return finish_copies(p, p->remote_order.size());
 }
 
@@ -1672,6 +1706,56 @@ csg_status csg_plan_check(csg_plan* p, csg_diag* out) {
   if (d.timed_out)
     return fail(CSG_ERR_TIMEOUT, "chunk %d (tile %d) never became ready (value %u, call %u)", d.chunk, d.tile,
                 d.observed, d.epoch);
+  return CSG_OK;
+}
+
+csg_status csg_plan_join(csg_plan* p, void* stream) {
+  if (!p) return fail(CSG_ERR_INVALID, "plan is NULL");
+  if (p->device < 0) return fail(CSG_ERR_STATE, "host-only plan (created with device < 0) has no copies");
+  if (p->kernel_copies() || p->epoch == 0) return CSG_OK;  // no copy outside the plan's kernels
+  DeviceGuard g(p->device);
+  if (g.err != hipSuccess) return hip_fail(g.err, "hipSetDevice");
+  const int set = p->epoch & 1;
+  if (p->n_join[set] == 0) return CSG_OK;
+  const uint64_t ticks = static_cast<uint64_t>(p->cfg.timeout_ms) * 100000ull;  // 100 MHz wall clock
+  CSG_HIP(csg::launch_join(p->d_join[set], p->n_join[set], ticks, p->d_join_flag,
+                           static_cast<hipStream_t>(stream)));
+  return CSG_OK;
+}
+
+csg_status csg_measure_mfma_peak(int device, int32_t iters, double* tflops, double* ms, double* ghz) {
+  if (!tflops || iters < 1) return fail(CSG_ERR_INVALID, "NULL output or iters < 1");
+  char arch[64];
+  csg_status st = csg_device_check(device, arch, sizeof arch);
+  if (st != CSG_OK) return st;
+  DeviceGuard g(device);
+  if (g.err != hipSuccess) return hip_fail(g.err, "hipSetDevice");
+  int cus = 0;
+  CSG_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device));
+  float* sink = nullptr;
+  uint64_t* clocks = nullptr;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  hipStream_t s = nullptr;
+  hipError_t e = hipMalloc(&sink, static_cast<size_t>(cus) * 256 * sizeof(float));
+  if (e == hipSuccess) e = hipMalloc(&clocks, 2 * sizeof(uint64_t));
+  if (e == hipSuccess) e = hipEventCreate(&e0);
+  if (e == hipSuccess) e = hipEventCreate(&e1);
+  if (e == hipSuccess) e = hipStreamCreateWithFlags(&s, hipStreamNonBlocking);
+  uint64_t c[2] = {0, 0};
+  float t_ms = 0.0f;
+  if (e == hipSuccess) e = csg::launch_mfma_peak(cus, iters, sink, clocks, s, e0, e1);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e == hipSuccess) e = hipEventElapsedTime(&t_ms, e0, e1);
+  if (e == hipSuccess) e = hipMemcpy(c, clocks, sizeof c, hipMemcpyDeviceToHost);
+  for (hipEvent_t ev : {e0, e1})
+    if (ev) (void)hipEventDestroy(ev);
+  if (s) (void)hipStreamDestroy(s);
+  if (sink) (void)hipFree(sink);
+  if (clocks) (void)hipFree(clocks);
+  if (e != hipSuccess) return hip_fail(e, "MFMA microbenchmark");
+  *tflops = t_ms > 0.0f ? csg::mfma_peak_flops(cus, iters) / (t_ms * 1e-3) / 1e12 : 0.0;
+  if (ms) *ms = t_ms;
+  if (ghz) *ghz = c[1] ? static_cast<double>(c[0]) / (static_cast<double>(c[1]) * 10.0) : 0.0;  // cycles / ns
   return CSG_OK;
 }
 

@@ -174,6 +174,18 @@ hipError_t kernel_grid(const KernelKey& key, int device, int32_t* grid);
 hipError_t launch_chunk_gemm(const KernelKey& key, const GemmArgs& args, int32_t grid, hipStream_t stream,
                              hipEvent_t start, hipEvent_t stop);
 
+// One thread waits until each of the n values reads 0 (the completion values of
+// copies), at most timeout_ticks (100 MHz) per value; *timed_out is set to 1 if one did
+// not. Work queued behind it on `stream` then follows those copies.
+hipError_t launch_join(const int64_t* const* values, int32_t n, uint64_t timeout_ticks, uint32_t* timed_out,
+                       hipStream_t stream);
+// MFMA microbenchmark: `grid` workgroups of 4 waves, each wave `iters` rounds of 8
+// independent bf16 32x32x16 MFMAs. clocks[0] = shader cycles, clocks[1] = 100 MHz
+// ticks of workgroup 0's loop. start/stop receive the dispatch's timestamps.
+hipError_t launch_mfma_peak(int32_t grid, int32_t iters, float* sink, uint64_t* clocks, hipStream_t stream,
+                            hipEvent_t start, hipEvent_t stop);
+double mfma_peak_flops(int32_t grid, int32_t iters);
+
 // Per-call set-up on the compute stream: clears the per-chunk counters, the
 // tickets, the split-K slot counts, the diagnostics and the copy workgroups' state,
 // and sets the ready words of kernel-moved chunks.
