@@ -299,6 +299,37 @@ csg_status csg_plan_set_copy_delays(csg_plan* p, const float* delay_us_host, int
 csg_status csg_ag_gemm(csg_plan* p, void* a_landing, const void* a_staging, const void* b_nk,
                        void* c, csg_mode mode, void* compute_stream, void* copy_stream);
 
+/* For callers that cannot allocate device memory: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc. The all-gather GEMM of csg_ag_gemm with
+ * the chunks moved by the kernel's own copy workgroups (as with
+ * csg_plan_cfg.copy_backend = CSG_COPY_KERNEL; no copy engine, no signal), without a
+ * plan: every table it needs (work units, chunk lists, copy slabs) and every per-call
+ * word (tickets, counters, ready words, diagnostics) lives in a static device array of
+ * the library, 2 MiB per device, which each device the library runs on holds from the
+ * library's load until the process ends. The call allocates nothing (no hipMalloc,
+ * hipFree or allocating library routine); it queues a table upload when the schedule,
+ * shape or dtypes differ from the previous call's on the device, then a prologue and
+ * the kernel, all on `stream` (a hipStream_t of `device`), and returns.
+ * Arguments as for csg_plan_create + csg_ag_gemm: `s` (host; not kept after the call)
+ * covers exactly M rows; a_landing (M x K, local rows in place), a_staging (same
+ * layout, the remote rows), b_nk (N x K), c (M x N) are device buffers of `device`,
+ * 16-byte aligned; tiles are 256 x 256 x 64 (bf16 input) or 64 x 64 x 16 (f32), dispatched
+ * per die with stealing, not split. copy_workgroups: workgroups that move the chunks
+ * (0 = 16). Modes as for csg_ag_gemm (compute-only: a_landing already holds every row;
+ * copy-only: the copy workgroups alone run).
+ * Limits: at most 4096 chunks, 16384 tiles, 32768 (tile, remote chunk) pairs and 16384
+ * copy slabs of 256 KiB (4 GiB of remote rows); beyond them CSG_ERR_UNSUPPORTED, before
+ * anything is queued. Every other check of csg_plan_create and csg_ag_gemm applies
+ * (CSG_ERR_INVALID / CSG_ERR_UNSUPPORTED).
+ * All calls on one device share its array, which keeps the last call's tables: calls
+ * that may overlap on one device (on different streams, or from several threads without
+ * an order between their streams) race and give wrong results; calls queued on one
+ * stream are ordered. A flag wait that times out (2 s; the kernel's own copy workgroups
+ * move every chunk, so only a stalled device gets there) is not reported. */
+csg_status csg_ag_gemm_noalloc(const csg_schedule* s, int64_t M, int64_t N, int64_t K, csg_dtype in_dtype,
+                               csg_dtype out_dtype, void* a_landing, const void* a_staging, const void* b_nk,
+                               void* c, csg_mode mode, int32_t copy_workgroups, int device, void* stream);
+
 /* GEMM + ReduceScatter on one rank: the kernel computes C tiles in emission
  * order; the last tile of an output chunk releases the chunk's flag, and the
  * calling thread then copies the chunk by SDMA from c to c_outgoing (non-local

@@ -49,7 +49,7 @@ ABI_FUNCTIONS = (
     "csg_plan_create", "csg_plan_info_get", "csg_plan_get_map", "csg_plan_set_copy_delays",
     "csg_ag_gemm", "csg_gemm_rs", "csg_gemm_ar", "csg_grouped_gemm", "csg_plan_check", "csg_plan_kernel_times",
     "csg_plan_trace", "csg_plan_destroy", "csg_attn_plan_create", "csg_ring_attn", "csg_plan_join",
-    "csg_measure_mfma_peak",
+    "csg_measure_mfma_peak", "csg_ag_gemm_noalloc",
 )
 
 
@@ -134,6 +134,7 @@ def _lib():
         "csg_plan_trace": ([vp, P(csg_trace_unit), i32, P(i32)], st),
         "csg_plan_destroy": ([vp], None),
         "csg_plan_join": ([vp, vp], st),
+        "csg_ag_gemm_noalloc": ([vp, i64, i64, i64, st, st, vp, vp, vp, vp, st, i32, ctypes.c_int, vp], st),
         "csg_measure_mfma_peak": ([ctypes.c_int, i32, P(ctypes.c_double), P(ctypes.c_double), P(ctypes.c_double)],
                                   st),
     }
@@ -377,6 +378,21 @@ def csg_plan_check(plan: int) -> csg_diag:
         raise err
     _check(st, "csg_plan_check")
     return d
+
+
+def csg_ag_gemm_noalloc(schedule, M, N, K, in_dtype, out_dtype, a_landing, a_staging, b_nk, c, mode="overlap",
+                        copy_workgroups=0, device=0, stream=None) -> None:
+    """The all-gather GEMM without a plan, on the library's static device scratch
+    (allocates nothing). `schedule` is a Schedule or a csg_schedule handle."""
+    h = schedule.handle if isinstance(schedule, Schedule) else schedule
+    ib = _elem_bytes(in_dtype)
+    for t, n, what in ((a_landing, M * K * ib, "a_landing"), (a_staging, M * K * ib, "a_staging"),
+                       (b_nk, N * K * ib, "b_nk"), (c, M * N * _elem_bytes(out_dtype), "c")):
+        _buf(t, n, what)
+    _check(_lib().csg_ag_gemm_noalloc(h, M, N, K, DTYPES[in_dtype] if isinstance(in_dtype, str) else in_dtype,
+                                      DTYPES[out_dtype] if isinstance(out_dtype, str) else out_dtype,
+                                      _ptr(a_landing), _ptr(a_staging), _ptr(b_nk), _ptr(c), _mode(mode),
+                                      copy_workgroups, device, _stream(stream)), "csg_ag_gemm_noalloc")
 
 
 def csg_plan_join(plan: int, stream) -> None:

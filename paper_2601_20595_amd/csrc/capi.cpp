@@ -33,6 +33,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <thread>
@@ -40,6 +41,8 @@
 
 #include "../../include/csg.h"
 #include "attn.hpp"
+#include "exec_tables.hpp"
+#include "noalloc.hpp"
 #include "kernels.hpp"
 #include "planner.hpp"
 #include "sdma.hpp"
@@ -303,88 +306,30 @@ csg_status setup_device(csg_plan* p) {
   if (g.err != hipSuccess) return hip_fail(g.err, "hipSetDevice");
   const csg::TileMap& m = p->map;
   const int32_t n_tiles = m.n_tiles();
-  const int32_t nN = m.n_tiles_n;
-  // execution list: the chunk-ordered tile list split into one sub-list per die, a
-  // tile going to die (row-tile index mod dies) so that tiles sharing A rows share
-  // an L2; each sub-list keeps the chunk order (static dispatch uses the plain list)
-  std::vector<int32_t> exec_order;
-  std::vector<int32_t> list_begin(csg::kXcdLists + 1, 0);
-  if (p->cfg.tile_dispatch == 2) {
-    exec_order = m.order;
-    list_begin.assign(csg::kXcdLists + 1, n_tiles);
-    list_begin[0] = 0;
-  } else {
-    for (int x = 0; x < csg::kXcdLists; ++x) {
-      list_begin[x] = static_cast<int32_t>(exec_order.size());
-      for (int32_t t : m.order)
-        if ((t / nN) % csg::kXcdLists == x) exec_order.push_back(t);
-    }
-    list_begin[csg::kXcdLists] = static_cast<int32_t>(exec_order.size());
-  }
-  // K-slices per tile: split_k for every tile; tail_split for the tiles on the
-  // critical path of the overlap, i.e. those reading one of the tail_chunks
-  // last-arriving chunks (consumers), or writing one of the tail_chunks first-emitted
-  // chunks (producer)
-  const int32_t KT = static_cast<int32_t>(p->K / p->cfg.bk);
-  std::vector<int32_t> tile_split(n_tiles, std::max(1, p->cfg.split_k));
-  if (p->cfg.tail_split > 1 && p->cfg.tail_chunks > 0) {
-    std::vector<int32_t> pos(p->n_chunks());
-    for (int32_t i = 0; i < p->n_chunks(); ++i) pos[p->sched.order[i]] = i;
-    for (int32_t t = 0; t < n_tiles; ++t) {
-      int32_t lo = p->n_chunks(), hi = -1;
-      for (int32_t q = m.tile_ptr[t]; q < m.tile_ptr[t + 1]; ++q) {
-        lo = std::min(lo, pos[m.tile_chunks[q]]);
-        hi = std::max(hi, pos[m.tile_chunks[q]]);
-      }
-      const bool critical = p->consumer() ? hi >= p->n_chunks() - p->cfg.tail_chunks : lo < p->cfg.tail_chunks;
-      if (critical) tile_split[t] = std::max(tile_split[t], p->cfg.tail_split);
-    }
-  }
-  for (int32_t& sp : tile_split) sp = std::min(sp, KT);
-  // work units: every tile, as tile_split[t] consecutive K-slices; the slices of a
-  // split tile own consecutive partial-sum buffers of the workspace
-  std::vector<csg::TileDesc> tiles;
-  std::vector<int32_t> lptr(1, 0), lids, raster;
-  std::vector<int32_t> unit_begin(csg::kXcdLists + 1, 0);
-  int32_t ws_slices = 0;
-  for (int32_t i = 0, x = 0; i < n_tiles; ++i) {
-    while (x <= csg::kXcdLists && list_begin[x] == i) unit_begin[x++] = static_cast<int32_t>(tiles.size());
-    const int32_t t = exec_order[i];
-    const csg::RowTile& rt = m.row_tiles[t / nN];
-    const int32_t split = tile_split[t];
-    for (int32_t sl = 0; sl < split; ++sl) {
-      const int32_t k0 = static_cast<int32_t>(static_cast<int64_t>(KT) * sl / split);
-      const int32_t k1 = static_cast<int32_t>(static_cast<int64_t>(KT) * (sl + 1) / split);
-      tiles.push_back({static_cast<int32_t>(rt.row_begin), static_cast<int32_t>(rt.row_end), t % nN, rt.group, k0, k1,
-                       split > 1 ? ws_slices : -1, sl | (split << 16)});
-      raster.push_back(t);
-      for (int32_t q = m.tile_ptr[t]; q < m.tile_ptr[t + 1]; ++q) {
-        const int32_t c = m.tile_chunks[q];
-        // consumers wait only for chunks that have to arrive; producers signal every chunk
-        if (!p->consumer() || !p->sched.chunks[c].is_local) lids.push_back(c);
-      }
-      lptr.push_back(static_cast<int32_t>(lids.size()));
-    }
-    if (split > 1) ws_slices += split;
-  }
-  for (int x = 0; x <= csg::kXcdLists; ++x)
-    if (list_begin[x] == n_tiles) unit_begin[x] = static_cast<int32_t>(tiles.size());
+  csg::ExecOptions eo;
+  eo.consumer = p->consumer();
+  eo.K = p->K;
+  eo.in_bytes = in_bytes(p);
+  eo.bk = p->cfg.bk;
+  eo.split_k = p->cfg.split_k;
+  eo.tail_split = p->cfg.tail_split;
+  eo.tail_chunks = p->cfg.tail_chunks;
+  eo.tile_dispatch = p->cfg.tile_dispatch;
+  csg::ExecTables et;
+  csg::build_exec_tables(p->sched, m, eo, &et);
+  const std::vector<csg::TileDesc>& tiles = et.units;
+  const std::vector<int32_t>& lptr = et.list_ptr;
+  const std::vector<int32_t>& lids = et.list_ids;
+  const std::vector<int32_t>& raster = et.raster;
+  const std::vector<int32_t>& need = et.need;
+  const std::vector<int32_t>& list_begin = et.list_begin;
+  const int32_t ws_slices = et.ws_slices;
   const int32_t n_units = static_cast<int32_t>(tiles.size());
   p->ws_slices = ws_slices;
   p->units = tiles;
   p->unit_raster = raster;
-  list_begin = unit_begin;
   p->n_units = n_units;
-  p->lines_aligned = true;
-  for (const csg::ChunkDesc& c : p->sched.chunks)
-    if ((c.row_begin * p->K * in_bytes(p)) % 128 != 0) p->lines_aligned = false;
-  // per chunk: tiles that write it (producer), or work units that read it (consumers:
-  // the units of split tiles each read the chunk's rows for their K range)
-  std::vector<int32_t> need(p->n_chunks(), 0);
-  if (p->consumer())
-    for (int32_t c : lids) ++need[c];
-  else
-    for (int32_t c = 0; c < p->n_chunks(); ++c) need[c] = m.chunk_ptr[c + 1] - m.chunk_ptr[c];
+  p->lines_aligned = et.lines_aligned;
   csg_status st;
   if ((st = upload(&p->d_tiles, tiles)) != CSG_OK) return st;
   if ((st = upload(&p->d_list_ptr, lptr)) != CSG_OK) return st;
@@ -428,14 +373,8 @@ csg_status setup_device(csg_plan* p) {
     // (coherent) device memory
     CSG_HIP(hipExtMallocWithFlags(reinterpret_cast<void**>(&p->d_kready), nflag * 8, hipDeviceMallocFinegrained));
     CSG_HIP(hipMemset(p->d_kready, 0, nflag * 8));
-    for (size_t i = 0; i < p->remote_order.size(); ++i) {
-      const int32_t cid = p->remote_order[i];
-      const csg::ChunkDesc& ch = p->sched.chunks[cid];
-      const int64_t off = ch.row_begin * row_bytes, bytes = (ch.row_end - ch.row_begin) * row_bytes;
-      int32_t n = 0;
-      for (int64_t b = 0; b < bytes; b += kCopySlab, ++n)
-        items.push_back({off + b, static_cast<int32_t>(std::min<int64_t>(kCopySlab, bytes - b)), static_cast<int32_t>(i)});
-      parts.push_back(n);
+    csg::build_copy_items(p->sched, p->remote_order, row_bytes, kCopySlab, &items, &parts);
+    for (const int32_t cid : p->remote_order) {
       sent[cid] = 1;
       words[cid] = p->d_kready + cid;
     }
@@ -1085,6 +1024,87 @@ csg_status consumer_call(csg_plan* p, void* landing, const void* staging, const 
   return CSG_OK;
 }
 
+// ---- the allocation-free all-gather GEMM (csg_ag_gemm_noalloc) ----------------------
+// Its tables and per-call words live in the library's static device scratch, at the
+// fixed offsets below; nothing is allocated per call or per schedule.
+constexpr int32_t kNaMaxChunks = 4096;   // also the kernels' ready-bitmap bound
+constexpr int32_t kNaMaxUnits = 16384;   // tiles
+constexpr int32_t kNaMaxNnz = 32768;     // (tile, remote chunk) pairs
+constexpr int32_t kNaMaxItems = 16384;   // 256 KiB copy slabs: 4 GiB of remote rows
+
+struct NaLayout {
+  // per-call words, reset by the prologue of every call
+  size_t diag, ticket, copy_state, counters, out_flags, kready, copy_done;
+  // tables, written when a call's schedule or shape differs from the previous call's
+  size_t tables, zero, tiles, list_ptr, list_ids, raster, list_begin, need, ready, items, copy_chunk, copy_parts;
+  size_t end;
+};
+
+NaLayout na_layout() {
+  NaLayout L{};
+  size_t o = 0;
+  auto take = [&o](size_t bytes) {
+    const size_t at = o;
+    o = (o + bytes + 255) & ~size_t{255};
+    return at;
+  };
+  L.diag = take(sizeof(csg::DeviceDiag));
+  L.ticket = take(csg::kXcdLists * 4);
+  L.copy_state = take(sizeof(csg::CopyState));
+  L.counters = take(kNaMaxChunks * 4);
+  L.out_flags = take(kNaMaxChunks * 4);
+  L.kready = take(kNaMaxChunks * 8);
+  L.copy_done = take(kNaMaxChunks * 4);
+  L.tables = o;
+  L.zero = take(64);
+  L.tiles = take(kNaMaxUnits * sizeof(csg::TileDesc));
+  L.list_ptr = take((kNaMaxUnits + 1) * 4);
+  L.list_ids = take(kNaMaxNnz * 4);
+  L.raster = take(kNaMaxUnits * 4);
+  L.list_begin = take((csg::kXcdLists + 1) * 4);
+  L.need = take(kNaMaxChunks * 4);
+  L.ready = take(kNaMaxChunks * 8);
+  L.items = take(kNaMaxItems * sizeof(csg::CopyItem));
+  L.copy_chunk = take(kNaMaxChunks * 4);
+  L.copy_parts = take(kNaMaxChunks * 4);
+  L.end = o;
+  return L;
+}
+
+// What a device's scratch currently holds, and the host image of its tables.
+struct NaDevice {
+  bool checked = false;          // csg_device_check passed
+  int32_t grid[4] = {0, 0, 0, 0};  // persistent grid per (input, output) dtype pair
+  uint64_t sig = 0;              // signature of the tables in the scratch (0: none)
+  std::vector<unsigned char> image;
+  int32_t n_units = 0, n_remote = 0, n_items = 0, n_tiles_n = 0;
+  bool lines_aligned = true;
+  uint32_t calls = 0;
+};
+std::mutex g_na_mu;
+NaDevice g_na[64];
+
+uint64_t na_signature(const csg::Schedule& s, int64_t M, int64_t N, int64_t K, csg_dtype in, csg_dtype out) {
+  uint64_t h = 1469598103934665603ull;
+  auto mix = [&h](uint64_t v) {
+    for (int i = 0; i < 8; ++i) {
+      h ^= (v >> (8 * i)) & 0xffu;
+      h *= 1099511628211ull;
+    }
+  };
+  mix(static_cast<uint64_t>(M));
+  mix(static_cast<uint64_t>(N));
+  mix(static_cast<uint64_t>(K));
+  mix(static_cast<uint64_t>(in) * 16 + static_cast<uint64_t>(out));
+  for (const csg::ChunkDesc& c : s.chunks) {
+    mix(static_cast<uint64_t>(c.row_begin));
+    mix(static_cast<uint64_t>(c.row_end));
+    mix(static_cast<uint64_t>(c.is_local));
+  }
+  for (int32_t o : s.order) mix(static_cast<uint64_t>(o));
+  return h | 1u;  // never 0
+}
+
 }  // namespace
 
 // =====================================================================================
@@ -1410,6 +1430,182 @@ csg_status csg_ag_gemm(csg_plan* p, void* a_landing, const void* a_staging, cons
   if (!p) return fail(CSG_ERR_INVALID, "plan is NULL");
   if (p->op != CSG_AG_GEMM || p->attention()) return fail(CSG_ERR_INVALID, "plan is not an all-gather GEMM plan");
   return consumer_call(p, a_landing, a_staging, b_nk, c, mode, compute_stream, copy_stream);
+}
+
+csg_status csg_ag_gemm_noalloc(const csg_schedule* sched, int64_t M, int64_t N, int64_t K, csg_dtype in_dtype,
+                               csg_dtype out_dtype, void* a_landing, const void* a_staging, const void* b_nk, void* c,
+                               csg_mode mode, int32_t copy_workgroups, int device, void* stream_v) {
+  // ---- validation: nothing is queued or allocated before every check has passed
+  if (!sched) return fail(CSG_ERR_INVALID, "schedule is NULL");
+  const csg::Schedule& s = sched->s;
+  if ((in_dtype != CSG_BF16 && in_dtype != CSG_F32) || (out_dtype != CSG_BF16 && out_dtype != CSG_F32))
+    return fail(CSG_ERR_INVALID, "unknown dtype");
+  if (mode != CSG_MODE_OVERLAP && mode != CSG_MODE_COMPUTE_ONLY && mode != CSG_MODE_COPY_ONLY)
+    return fail(CSG_ERR_INVALID, "unknown mode %d", static_cast<int>(mode));
+  if (M < 1 || N < 1 || K < 1 || M > 0x7fffffff || N > 0x7fffffff || K > (1 << 22))
+    return fail(CSG_ERR_INVALID, "shape out of range");
+  if (s.total_rows != M) return fail(CSG_ERR_INVALID, "the schedule's chunks do not cover exactly M rows");
+  if (device < 0 || device >= 64) return fail(CSG_ERR_INVALID, "device %d out of range", device);
+  if (copy_workgroups == 0) copy_workgroups = kDefaultCopyWorkgroups;
+  if (copy_workgroups < 1 || copy_workgroups > 4096) return fail(CSG_ERR_INVALID, "copy_workgroups out of range");
+  const bool bf16 = in_dtype == CSG_BF16;
+  const int32_t bm = bf16 ? 256 : 64, bn = bf16 ? 256 : 64, bk = bf16 ? 64 : 16;
+  const int64_t ib = bf16 ? 2 : 4, ob = out_dtype == CSG_BF16 ? 2 : 4;
+  if (K % bk != 0 || N % 4 != 0)
+    return fail(CSG_ERR_UNSUPPORTED, "K must be a multiple of %d and N a multiple of 4", bk);
+  if (static_cast<int64_t>(std::max(bm, bn)) * K * ib >= (int64_t{1} << 31) ||
+      static_cast<int64_t>(bm) * N * ob >= (int64_t{1} << 30))
+    return fail(CSG_ERR_UNSUPPORTED, "a tile of A/B or of C exceeds the 32-bit offset range");
+  const int32_t n_chunks = static_cast<int32_t>(s.chunks.size());
+  if (n_chunks > kNaMaxChunks) return fail(CSG_ERR_UNSUPPORTED, "at most %d chunks", kNaMaxChunks);
+  std::vector<int32_t> remote;
+  for (int32_t cid : s.order)
+    if (!s.chunks[cid].is_local) remote.push_back(cid);
+  const bool copies = mode != CSG_MODE_COMPUTE_ONLY && !remote.empty();
+  if (!a_landing || !b_nk || !c || (copies && !a_staging)) return fail(CSG_ERR_INVALID, "NULL buffer");
+  if (!aligned16(a_landing) || !aligned16(a_staging) || !aligned16(b_nk) || !aligned16(c))
+    return fail(CSG_ERR_INVALID, "buffers must be 16-byte aligned");
+  const NaLayout L = na_layout();
+  if (L.end > csg::kNoAllocScratchBytes) return fail(CSG_ERR_STATE, "scratch layout exceeds the scratch array");
+  const csg::KernelKey key{bf16 ? csg::InType::BF16 : csg::InType::F32, out_dtype == CSG_BF16, false, bm, bn, bk,
+                           false};
+  const int kslot = (bf16 ? 0 : 2) + (out_dtype == CSG_BF16 ? 0 : 1);
+  const uint64_t sig = na_signature(s, M, N, K, in_dtype, out_dtype);
+
+  std::lock_guard<std::mutex> lock(g_na_mu);
+  NaDevice& nd = g_na[device];
+  // ---- the tables of this schedule and shape, on the host (only when they differ from
+  //      what the device's scratch holds)
+  std::vector<unsigned char> image;
+  int32_t n_units = 0, n_items = 0, n_tiles_n = 0;
+  bool lines_aligned = true;
+  if (nd.sig != sig) {
+    csg::TileMap map;
+    std::string err = csg::build_tile_map(s, M, N, bm, bn, false, {}, &map);
+    if (!err.empty()) return fail(CSG_ERR_INVALID, "%s", err.c_str());
+    csg::ExecOptions eo;
+    eo.consumer = true;
+    eo.K = K;
+    eo.in_bytes = ib;
+    eo.bk = bk;
+    csg::ExecTables et;
+    csg::build_exec_tables(s, map, eo, &et);
+    std::vector<csg::CopyItem> items;
+    std::vector<int32_t> parts;
+    csg::build_copy_items(s, remote, K * ib, kCopySlab, &items, &parts);
+    n_units = static_cast<int32_t>(et.units.size());
+    n_items = static_cast<int32_t>(items.size());
+    if (n_units > kNaMaxUnits || static_cast<int64_t>(et.list_ids.size()) > kNaMaxNnz || n_items > kNaMaxItems)
+      return fail(CSG_ERR_UNSUPPORTED,
+                  "%d tiles, %zu tile-chunk pairs and %d copy slabs of 256 KiB exceed the no-alloc scratch "
+                  "(at most %d, %d and %d)",
+                  n_units, et.list_ids.size(), n_items, kNaMaxUnits, kNaMaxNnz, kNaMaxItems);
+    n_tiles_n = map.n_tiles_n;
+    lines_aligned = et.lines_aligned;
+    image.assign(L.end - L.tables, 0);
+    auto put = [&](size_t at, const void* src, size_t bytes) {
+      if (bytes) std::memcpy(image.data() + (at - L.tables), src, bytes);
+    };
+    put(L.tiles, et.units.data(), et.units.size() * sizeof(csg::TileDesc));
+    put(L.list_ptr, et.list_ptr.data(), et.list_ptr.size() * 4);
+    put(L.list_ids, et.list_ids.data(), et.list_ids.size() * 4);
+    put(L.raster, et.raster.data(), et.raster.size() * 4);
+    put(L.list_begin, et.list_begin.data(), et.list_begin.size() * 4);
+    put(L.need, et.need.data(), et.need.size() * 4);
+    put(L.items, items.data(), items.size() * sizeof(csg::CopyItem));
+    put(L.copy_chunk, remote.data(), remote.size() * 4);
+    put(L.copy_parts, parts.data(), parts.size() * 4);
+    // the ready-value pointers need the device's scratch address: filled in below
+  }
+  // ---- the device
+  DeviceGuard g(device);
+  if (g.err != hipSuccess) return hip_fail(g.err, "hipSetDevice");
+  if (!nd.checked) {
+    char arch[64];
+    const csg_status st = csg_device_check(device, arch, sizeof arch);
+    if (st != CSG_OK) return st;
+    nd.checked = true;
+  }
+  void* base = nullptr;
+  CSG_HIP(csg::noalloc_scratch(device, &base));
+  unsigned char* ptr = static_cast<unsigned char*>(base);
+  if (!nd.grid[kslot]) CSG_HIP(csg::kernel_grid(key, device, &nd.grid[kslot]));
+  hipStream_t stream = static_cast<hipStream_t>(stream_v);
+  if (nd.sig != sig) {
+    // ready values: a local chunk's is the zero word; a remote chunk's, its ready word
+    std::vector<const int64_t*> ready(n_chunks, reinterpret_cast<const int64_t*>(ptr + L.zero));
+    for (int32_t cid : remote) ready[cid] = reinterpret_cast<const int64_t*>(ptr + L.kready) + cid;
+    std::memcpy(image.data() + (L.ready - L.tables), ready.data(), ready.size() * sizeof(int64_t*));
+    nd.sig = 0;  // the scratch holds no valid tables until the copy below is queued
+    CSG_HIP(hipMemcpyAsync(ptr + L.tables, image.data(), image.size(), hipMemcpyHostToDevice, stream));
+    nd.image.swap(image);
+    nd.sig = sig;
+    nd.n_units = n_units;
+    nd.n_remote = static_cast<int32_t>(remote.size());
+    nd.n_items = n_items;
+    nd.n_tiles_n = n_tiles_n;
+    nd.lines_aligned = lines_aligned;
+  }
+  nd.calls = nd.calls % 0x3ffffff0u + 1;  // the call number the kernel writes into its consumed words
+  const uint32_t epoch = nd.calls;
+  // ---- per-call words, then the kernel, on the caller's stream
+  csg::PrologueArgs pa{};
+  pa.counters = reinterpret_cast<uint32_t*>(ptr + L.counters);
+  pa.n_chunks = n_chunks;
+  pa.epoch = epoch;
+  pa.ticket = reinterpret_cast<uint32_t*>(ptr + L.ticket);
+  pa.diag = reinterpret_cast<csg::DeviceDiag*>(ptr + L.diag);
+  pa.ready_words = reinterpret_cast<int64_t*>(ptr + L.kready);
+  pa.ready_value = mode == CSG_MODE_COMPUTE_ONLY ? 0 : 1;
+  pa.copy_done = reinterpret_cast<uint32_t*>(ptr + L.copy_done);
+  pa.n_remote = nd.n_remote;
+  pa.copy_state = reinterpret_cast<csg::CopyState*>(ptr + L.copy_state);
+  CSG_HIP(csg::launch_prologue(pa, stream));
+  csg::GemmArgs a{};
+  a.A = a_landing;
+  a.B = b_nk;
+  a.C = c;
+  a.M = M;
+  a.N = N;
+  a.K = K;
+  a.tiles = reinterpret_cast<const csg::TileDesc*>(ptr + L.tiles);
+  a.list_ptr = reinterpret_cast<const int32_t*>(ptr + L.list_ptr);
+  a.list_ids = reinterpret_cast<const int32_t*>(ptr + L.list_ids);
+  a.raster = reinterpret_cast<const int32_t*>(ptr + L.raster);
+  a.ready = reinterpret_cast<const int64_t* const*>(ptr + L.ready);
+  a.counters = pa.counters;
+  a.need = reinterpret_cast<const int32_t*>(ptr + L.need);
+  a.out_flags = reinterpret_cast<uint32_t*>(ptr + L.out_flags);
+  a.ticket = pa.ticket;
+  a.list_begin = reinterpret_cast<const int32_t*>(ptr + L.list_begin);
+  a.diag = pa.diag;
+  a.timeout_ticks = 2000ull * 100000ull;  // 2 s of 100 MHz wall clock per wait
+  a.epoch = epoch;
+  a.n_tiles = mode == CSG_MODE_COPY_ONLY ? 0 : nd.n_units;
+  a.n_chunks = n_chunks;
+  a.dynamic_ticket = 1;
+  a.steal = 1;
+  a.n_tiles_n = mode == CSG_MODE_OVERLAP ? nd.n_tiles_n : 0;
+  a.acquire_fresh = (!nd.lines_aligned || reinterpret_cast<uintptr_t>(a_landing) % 128 != 0) ? 1 : 0;
+  int32_t grid = nd.grid[kslot];
+  if (copies && nd.n_items > 0) {
+    a.copy_items = reinterpret_cast<const csg::CopyItem*>(ptr + L.items);
+    a.n_copy_items = nd.n_items;
+    a.copy_wgs = copy_workgroups;
+    a.copy_src = static_cast<const unsigned char*>(a_staging);
+    a.copy_dst = static_cast<unsigned char*>(a_landing);
+    a.copy_chunk = reinterpret_cast<const int32_t*>(ptr + L.copy_chunk);
+    a.copy_parts = reinterpret_cast<const int32_t*>(ptr + L.copy_parts);
+    a.copy_done = pa.copy_done;
+    a.copy_ready = pa.ready_words;
+    a.copy_state = pa.copy_state;
+  }
+  if (mode == CSG_MODE_COPY_ONLY) {
+    if (!copies || nd.n_items == 0) return CSG_OK;  // nothing to move
+    grid = std::min(copy_workgroups, grid);
+  }
+  CSG_HIP(csg::launch_chunk_gemm(key, a, grid, stream, nullptr, nullptr));
+  return CSG_OK;
 }
 
 csg_status csg_grouped_gemm(csg_plan* p, void* x_landing, const void* x_staging, const void* b_enk, void* c,
