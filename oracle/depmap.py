@@ -16,7 +16,17 @@ Definitions used here (written out plainly; no blocking or shortcuts):
   T(c) = ascending raster ids of the tiles whose D contains c;  need(c) = |T(c)|;
   key(t) = max_{c in D(t)} pos(c) for consumers (all-gather, grouped),
            min_{c in D(t)} pos(c) for producers (reduce-scatter);
-  order = tiles sorted by (key(t), raster id).
+  order = tiles sorted by (key(t), raster id)                   [intra_order 0].
+
+Intra-chunk swizzle (Section 5.2, tile-scheduler swizzling: inside a chunk, visit the
+tiles in an order that keeps locality; Section 5.3: the tuner searches intra-tile
+orders). Reading used here [intra_order 1, band height G = group_m]: the tiles sharing
+one key form a group; the group's row tiles, ascending, are cut into bands of G
+consecutive ones, and each band is visited column by column, so consecutive tiles
+share B columns across the band's rows and A rows across the columns:
+  band(t) = (number of the group's row tiles below t's row tile) // G,
+  order = tiles sorted by (key(t), band(t), n, m).
+G = 1 gives the raster order again; the chunk order (the key) is never changed.
 """
 from __future__ import annotations
 
@@ -68,7 +78,8 @@ class DepMap:
 
 
 def dep_map(chunks: Sequence[Chunk], order: Sequence[int], M: int, N: int, BM: int, BN: int,
-            producer: bool = False, group_rows: Sequence[int] = None) -> DepMap:
+            producer: bool = False, group_rows: Sequence[int] = None, intra_order: int = 0,
+            group_m: int = 8) -> DepMap:
     grid = tile_grid(M, N, BM, BN, group_rows)
     nN = grid.n_tiles_n
     n_chunks = len(chunks)
@@ -95,5 +106,18 @@ def dep_map(chunks: Sequence[Chunk], order: Sequence[int], M: int, N: int, BM: i
     chunk_tiles = np.array([t for lst in T for t in lst], dtype=np.int32)
     need = np.array([len(lst) for lst in T], dtype=np.int32)
     keys = np.array([(min if producer else max)(pos[c] for c in d) for d in D], dtype=np.int64)
-    ord_ = np.array(sorted(range(grid.n_tiles), key=lambda t: (keys[t], t)), dtype=np.int32)
+    if intra_order == 0:
+        ord_ = np.array(sorted(range(grid.n_tiles), key=lambda t: (keys[t], t)), dtype=np.int32)
+    elif intra_order == 1:
+        # every tile of a row tile has the same D, hence the same key
+        n_rows = len(grid.row_tiles)
+        row_key = [int(keys[m * nN]) for m in range(n_rows)]
+        band = []
+        for m in range(n_rows):
+            below = sum(1 for mm in range(m) if row_key[mm] == row_key[m])
+            band.append(below // group_m)
+        ord_ = np.array(sorted(range(grid.n_tiles),
+                               key=lambda t: (keys[t], band[t // nN], t % nN, t // nN)), dtype=np.int32)
+    else:
+        raise ValueError("intra_order must be 0 or 1")
     return DepMap(tile_ptr, tile_chunks, chunk_ptr, chunk_tiles, need, ord_, keys)

@@ -39,7 +39,7 @@
 #include <thread>
 #include <vector>
 
-#include "../../include/csg.h"
+#include "csg.h"
 #include "attn.hpp"
 #include "exec_tables.hpp"
 #include "noalloc.hpp"

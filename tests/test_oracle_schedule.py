@@ -160,3 +160,46 @@ def test_tile_order_properties(producer):
     for i in range(1, n_tiles):
         if keys[i] == keys[i - 1]:
             assert dm.order[i] > dm.order[i - 1]
+
+
+@pytest.mark.parametrize("ex", GOLDEN["intra_orders"], ids=lambda e: e["name"])
+def test_intra_order_hand_examples(ex):
+    chunks, order = _chunks_of(ex)
+    dm = oracle.dep_map(chunks, order, ex["M"], ex["N"], ex["BM"], ex["BN"], producer=ex["producer"],
+                        intra_order=ex["intra_order"], group_m=ex["group_m"])
+    assert dm.order.tolist() == ex["order"]
+
+
+@pytest.mark.parametrize("producer", [False, True])
+@pytest.mark.parametrize("S,Q,BM,BN,N,G", [(128, 2, 32, 40, 160, 2),   # BM | h: bands inside a chunk
+                                           (96, 3, 80, 48, 100, 3),     # straddling tiles, ragged tails
+                                           (256, 1, 32, 64, 192, 3)])   # 8 row tiles per chunk, ragged band
+def test_intra_order_keeps_the_chunk_order_and_the_map(producer, S, Q, BM, BN, N, G):
+    W = 4
+    rng = np.random.default_rng(12)
+    chunks = oracle.uniform_chunks(W, 1, S, Q)
+    order = oracle.order_permutation(chunks, rng.permutation((W - 1) * Q))
+    base = oracle.dep_map(chunks, order, W * S, N, BM, BN, producer=producer)
+    sw = oracle.dep_map(chunks, order, W * S, N, BM, BN, producer=producer, intra_order=1, group_m=G)
+    for k in ("tile_ptr", "tile_chunks", "chunk_ptr", "chunk_tiles", "need", "keys"):
+        assert getattr(sw, k).tolist() == getattr(base, k).tolist(), k
+    assert sorted(sw.order.tolist()) == list(range(len(base.order)))
+    assert [int(base.keys[t]) for t in sw.order] == [int(base.keys[t]) for t in base.order]
+    # band height 1 is the raster order
+    one = oracle.dep_map(chunks, order, W * S, N, BM, BN, producer=producer, intra_order=1, group_m=1)
+    assert one.order.tolist() == base.order.tolist()
+
+
+def test_intra_order_whole_chunk_band_is_column_major():
+    """Closed form: with BM | h and G >= h / BM every chunk is one band, so its tiles are
+    visited column by column: n outer, the chunk's row tiles inner."""
+    W, S, Q, BM, BN, N = 3, 256, 2, 32, 64, 320
+    chunks, order = oracle.uniform_schedule(W, 2, S, Q, "ring")
+    nN = -(-N // BN)
+    rows_per_chunk = (S // Q) // BM
+    dm = oracle.dep_map(chunks, order, W * S, N, BM, BN, intra_order=1, group_m=rows_per_chunk)
+    want = []
+    for c in order:
+        m0 = chunks[c].row_begin // BM
+        want += [m * nN + n for n in range(nN) for m in range(m0, m0 + rows_per_chunk)]
+    assert dm.order.tolist() == want
