@@ -108,7 +108,12 @@ typedef struct {
 
 /* Tile and runtime knobs. Zero means "default" for every field.
  *   bm, bn, bk      tile shape; must name a compiled kernel variant on a device plan
- *   intra_order     0 = raster (m, n) inside a chunk (the local kernel's own traversal)
+ *   intra_order     tile order inside a chunk (Section 5.2, intra-chunk swizzle), the
+ *                   chunk order staying as it is: 0 = raster (m, n), the local kernel's
+ *                   own traversal; 1 = the row tiles sharing a chunk key, ascending, are
+ *                   cut into bands of group_m and each band is visited column by column:
+ *                   order = (key, band, n, m)
+ *   group_m         band height of intra_order 1 (0 = 8)
  *   tile_dispatch   0 or 1 = workgroups take the next entry of the tile list from an
  *                   atomic ticket; 2 = workgroup w takes entries w, w + G, w + 2G, ...
  *   num_workgroups  persistent grid size G (0 = one per co-resident slot)
@@ -122,9 +127,9 @@ typedef struct {
  *   tail_split      K-slices for the tiles on the overlap's critical path: the tiles that
  *   tail_chunks     read one of the tail_chunks last-arriving chunks (AG, grouped) or write
  *                   one of the tail_chunks first-emitted chunks (RS); 0 = none. Slices are
- *                   added as for split_k. A plan with split tiles keeps each tile's slices
- *                   on one die (they exchange partial sums through its L2), so its
- *                   num_workgroups, if given, must be a multiple of 8
+ *                   added as for split_k (the slices exchange fp32 partial sums through
+ *                   memory, so they may run on any die). A plan with split tiles of
+ *                   either kind takes a num_workgroups, if given, that is a multiple of 8
  *   trace           1 = the kernel records when each work unit was taken, started and
  *                   finished (read back with csg_plan_trace); 0 = off
  *   warm_rows       consumers: 0 or 1 = a workgroup that sees a chunk land first loads
@@ -132,7 +137,12 @@ typedef struct {
  *                   (copy-engine writes leave the rows only in HBM); 2 = off
  *   copy_backend    a csg_copy_backend value; 0 = CSG_COPY_SDMA
  *   copy_workgroups CSG_COPY_KERNEL: workgroups that move chunks (0 = 16); a copy-only
- *                   call launches exactly this many */
+ *                   call launches exactly this many
+ *   tail_wave       > 1: each die's tile list ends in a partial wave of L mod w tiles (w =
+ *                   the die's workgroups), which would run with the rest of the die idle;
+ *                   those tiles are split into min(tail_wave, w / (L mod w)) K-slices
+ *                   (added as for split_k). Per-die dispatch only (tile_dispatch 0/1);
+ *                   0 or 1 = off */
 typedef struct {
     int32_t bm, bn, bk;
     int32_t intra_order;
@@ -147,6 +157,8 @@ typedef struct {
     int32_t warm_rows;
     int32_t copy_backend;
     int32_t copy_workgroups;
+    int32_t group_m;
+    int32_t tail_wave;
 } csg_plan_cfg;
 
 typedef struct csg_schedule csg_schedule;

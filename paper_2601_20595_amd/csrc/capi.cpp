@@ -315,6 +315,8 @@ csg_status setup_device(csg_plan* p) {
   eo.tail_split = p->cfg.tail_split;
   eo.tail_chunks = p->cfg.tail_chunks;
   eo.tile_dispatch = p->cfg.tile_dispatch;
+  eo.grid = p->grid;
+  eo.tail_wave = p->cfg.tail_wave;
   csg::ExecTables et;
   csg::build_exec_tables(p->sched, m, eo, &et);
   const std::vector<csg::TileDesc>& tiles = et.units;
@@ -652,7 +654,9 @@ csg_status launch_gemm(csg_plan* p, const void* A, const void* B, void* C, csg_m
   }
   a.n_chunks = p->n_chunks();
   a.dynamic_ticket = p->cfg.tile_dispatch == 2 ? 0 : 1;
-  a.steal = (p->ws_slices > 0 && a.dynamic_ticket) ? 0 : 1;
+  // Idle workgroups take other dies' units (split tiles exchange partial sums through
+  // memory, so their slices may run on any die).
+  a.steal = 1;
   a.trace = p->d_trace;
   // only copies of this call leave rows fresh in HBM; without them the warm-up loads
   // would only cost time
@@ -1240,13 +1244,14 @@ csg_status csg_plan_create(csg_op op, int64_t M, int64_t N, int64_t K, csg_dtype
       c.split_k < 1 || c.split_k > 64 || c.tail_split < 0 || c.tail_split > 64 || c.tail_chunks < 0 ||
       c.trace < 0 || c.trace > 1 || c.warm_rows < 0 || c.warm_rows > 2 || c.copy_backend < 0 ||
       c.copy_backend > CSG_COPY_KERNEL || c.copy_workgroups < 0 || c.copy_workgroups > 4096 ||
-      c.num_workgroups < 0 || c.tile_dispatch < 0 || c.tile_dispatch > 2 || c.intra_order != 0)
+      c.num_workgroups < 0 || c.tile_dispatch < 0 || c.tile_dispatch > 2 || c.intra_order < 0 ||
+      c.intra_order > 1 || c.group_m < 0 || c.tail_wave < 0 || c.tail_wave > 64)
     return fail(CSG_ERR_INVALID, "bad plan configuration");
-  // split tiles run every slice on their own die (no stealing): every die needs
-  // workgroups, which the round-robin dispatch of a grid that is a multiple of the die
-  // count guarantees
-  if ((c.split_k > 1 || (c.tail_split > 1 && c.tail_chunks > 0)) && c.tile_dispatch != 2 && c.num_workgroups > 0 &&
-      c.num_workgroups % csg::kXcdLists != 0)
+  if (c.group_m == 0) c.group_m = 8;
+  // split plans keep the grid a multiple of the die count (round-robin dispatch then
+  // gives every die the same number of workgroups, and each die's list its share)
+  if ((c.split_k > 1 || (c.tail_split > 1 && c.tail_chunks > 0) || c.tail_wave > 1) && c.tile_dispatch != 2 &&
+      c.num_workgroups > 0 && c.num_workgroups % csg::kXcdLists != 0)
     return fail(CSG_ERR_INVALID, "with split tiles num_workgroups must be a multiple of %d", csg::kXcdLists);
 
   csg_plan* p = new (std::nothrow) csg_plan;
@@ -1260,7 +1265,8 @@ csg_status csg_plan_create(csg_op op, int64_t M, int64_t N, int64_t K, csg_dtype
   p->sched = s->s;
   p->group_rows = groups;
   p->cfg = c;
-  std::string err = csg::build_tile_map(p->sched, M, N, c.bm, c.bn, !p->consumer(), groups, &p->map);
+  std::string err =
+      csg::build_tile_map(p->sched, M, N, c.bm, c.bn, !p->consumer(), groups, &p->map, c.intra_order, c.group_m);
   if (!err.empty()) {
     delete p;
     return fail(CSG_ERR_INVALID, "%s", err.c_str());
@@ -1287,7 +1293,7 @@ csg_status csg_plan_create(csg_op op, int64_t M, int64_t N, int64_t K, csg_dtype
     if (why.empty() && M % S != 0) why = "M must be a multiple of the own shard's rows";
     if (why.empty() && (own0 % c.bm != 0 || (own1 % c.bm != 0 && own1 != M)))
       why = "the own shard must start and end on a tile-row boundary (bm)";
-    if (why.empty() && (c.split_k > 1 || (c.tail_split > 1 && c.tail_chunks > 0)))
+    if (why.empty() && (c.split_k > 1 || (c.tail_split > 1 && c.tail_chunks > 0) || c.tail_wave > 1))
       why = "GEMM + all-reduce splits no tile";
     if (why.empty() && c.copy_backend != CSG_COPY_SDMA) why = "GEMM + all-reduce copies with the SDMA engines";
     if (!why.empty()) {
@@ -1692,7 +1698,7 @@ csg_status csg_attn_plan_create(int32_t n_heads, int32_t n_kv_heads, int32_t hea
   if (c.timeout_ms == 0) c.timeout_ms = 2000;
   if (c.copy_engines < 0 || c.copy_engines > 32 || c.timeout_ms < 1 || c.num_workgroups < 0)
     return fail(CSG_ERR_INVALID, "bad plan configuration");
-  if (c.copy_backend != CSG_COPY_SDMA || c.split_k > 1 || c.tail_split > 1 || c.trace)
+  if (c.copy_backend != CSG_COPY_SDMA || c.split_k > 1 || c.tail_split > 1 || c.tail_wave > 1 || c.intra_order != 0 || c.trace)
     return fail(CSG_ERR_UNSUPPORTED, "attention plans copy with the SDMA engines and split or trace nothing");
   const csg::Schedule& sch = s->s;
   if (sch.chunks.size() > 4096) return fail(CSG_ERR_UNSUPPORTED, "at most 4096 chunks");

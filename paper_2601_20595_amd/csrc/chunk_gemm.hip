@@ -432,6 +432,18 @@ struct F32Loop {
 constexpr int kDropOffset = 0x7ffffff0;  // buffer offset past every C resource: store dropped
 constexpr int kPolicySc0 = 1, kPolicySc1 = 16;  // cache-policy bits of buffer instructions (scope)
 
+// Split-K partial sums. The slices of a tile may run on different dies, whose L2s are
+// not coherent with each other: every partial is written through to memory and read
+// back past both caches (system-coherent policy, sc0 sc1), so a store that has
+// completed is visible to a reader on any die and no cache is written back or
+// invalidated.
+__device__ __forceinline__ void store_partial(const f32x4& v, const __amdgpu_buffer_rsrc_t& rs, int voff, int soff) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), rs, voff, soff, kPolicySc0 | kPolicySc1);
+}
+__device__ __forceinline__ f32x4 load_partial(const __amdgpu_buffer_rsrc_t& rs, int voff, int soff) {
+  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, voff, soff, kPolicySc0 | kPolicySc1));
+}
+
 template <int S, int kRuns, class Load, class Store>
 __device__ __forceinline__ void reduce_fixed(Load load, Store store) {
   constexpr int B0 = (8 / S) > 0 ? (8 / S) : 1;
@@ -881,12 +893,8 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
       __syncthreads();
       if (!__builtin_amdgcn_readfirstlane(s_state)) {
 #pragma unroll
-        for (int r = 0; r < kRuns; ++r)
-          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc_run(r)), rsW, toff,
-                                                 me * kSliceBytes + r * kThreads * 16, 0);
-        // same-die slices meet in the die's L2 (see the general case below)
-        if (a.steal) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-        else wait_dma_all();
+        for (int r = 0; r < kRuns; ++r) store_partial(acc_run(r), rsW, toff, me * kSliceBytes + r * kThreads * 16);
+        wait_dma_all();  // this thread's partials have been written to memory
         __syncthreads();
         if (tid == 0) __hip_atomic_fetch_add(word, 1u << 16, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         wrote = false;
@@ -895,19 +903,11 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
         if (tid == 0) s_state = wait_slices_stored(a, word, 1, pos);
         __syncthreads();
         skip = __builtin_amdgcn_readfirstlane(s_state) < 0;
-        if (!skip) {
-          if (a.steal) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-          else asm volatile("buffer_inv sc0" ::: "memory");  // drop this CU's L1 copy, if any
-          skip = !wait_previous_copy_out();
-        }
+        if (!skip) skip = !wait_previous_copy_out();
         if (!skip) {
           const int other = (1 - me) * kSliceBytes;
-          add_stored_pair<kRuns>(
-              [&](int r) -> f32x4 {
-                return __builtin_bit_cast(
-                    f32x4, __builtin_amdgcn_raw_buffer_load_b128(rsW, toff, other + r * kThreads * 16, 0));
-              },
-              acc_run, store_run);
+          add_stored_pair<kRuns>([&](int r) -> f32x4 { return load_partial(rsW, toff, other + r * kThreads * 16); },
+                                 acc_run, store_run);
         }
         wrote = !skip;
       }
@@ -923,15 +923,10 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
       const int toff = tid * 16;
       const int mine = (td.slice & 0xffff) * kSliceBytes;
 #pragma unroll
-      for (int r = 0; r < kRuns; ++r)
-        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc_run(r)), rsW, toff,
-                                               mine + r * kThreads * 16, 0);
-      // Without stealing all slices of a tile run on one die and meet in its L2 (the
-      // vector L1 is write-through): waiting for the stores to complete is the release,
-      // and the reducer drops only its own L1. Otherwise slices may sit on other dies,
-      // whose L2s are not coherent with each other: write back and invalidate L2.
-      if (a.steal) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-      else wait_dma_all();
+      for (int r = 0; r < kRuns; ++r) store_partial(acc_run(r), rsW, toff, mine + r * kThreads * 16);
+      // waiting for the stores to complete (written through to memory) is the release;
+      // the reducer reads memory past its caches
+      wait_dma_all();
       __syncthreads();
       if (tid == 0)
         s_state = (__hip_atomic_fetch_add(a.slot_count + a.raster[pos], 1u, __ATOMIC_RELAXED,
@@ -940,14 +935,9 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
       if (!__builtin_amdgcn_readfirstlane(s_state)) {
         wrote = false;
       } else {
-        if (a.steal) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-        else asm volatile("buffer_inv sc0" ::: "memory");
         skip = !wait_previous_copy_out();
         if (!skip) {
-          auto load_part = [&](int sl, int r) -> f32x4 {
-            return __builtin_bit_cast(
-                f32x4, __builtin_amdgcn_raw_buffer_load_b128(rsW, toff, sl * kSliceBytes + r * kThreads * 16, 0));
-          };
+          auto load_part = [&](int sl, int r) -> f32x4 { return load_partial(rsW, toff, sl * kSliceBytes + r * kThreads * 16); };
           reduce_slices<kRuns>(nslices, load_part, store_run);
         }
         wrote = !skip;

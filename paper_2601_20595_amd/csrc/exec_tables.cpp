@@ -45,6 +45,21 @@ void build_exec_tables(const Schedule& s, const TileMap& m, const ExecOptions& o
       if (critical) tile_split[t] = std::max(tile_split[t], o.tail_split);
     }
   }
+  // Each die's last partial wave: with w workgroups on a die and L tiles in its list,
+  // the last L mod w tiles would run with the rest of the die idle; split each of them
+  // into up to w / (L mod w) K-slices (at most tail_wave) so that they fill the die.
+  if (o.tail_wave > 1 && o.tile_dispatch != 2 && o.grid >= kXcdLists) {
+    const int32_t w = o.grid / kXcdLists;
+    for (int x = 0; x < kXcdLists; ++x) {
+      const int32_t len = list_begin[x + 1] - list_begin[x];
+      const int32_t rem = len % w;
+      if (rem == 0) continue;
+      const int32_t sp = std::min(o.tail_wave, w / rem);
+      if (sp < 2) continue;
+      for (int32_t i = list_begin[x + 1] - rem; i < list_begin[x + 1]; ++i)
+        tile_split[exec_order[i]] = std::max(tile_split[exec_order[i]], sp);
+    }
+  }
   for (int32_t& sp : tile_split) sp = std::min(sp, KT);
   // work units: every tile, as tile_split[t] consecutive K-slices; the slices of a
   // split tile own consecutive partial-sum buffers of the workspace

@@ -83,8 +83,9 @@ struct GemmArgs {
   // share, 1 / n_tiles_n, of the tile's A rows; 0: off).
   int32_t n_tiles_n;
   // 1: a workgroup whose die's sub-list is exhausted takes entries of other dies'
-  // lists. 0: every entry runs on its own die, so the slices of a split tile share
-  // that die's L2 and exchange partial sums through it without L2 maintenance.
+  // lists. 0: every entry runs on its own die. The slices of a split tile exchange
+  // partial sums through memory either way (written through, read past the caches),
+  // so they may run on any die and need no L2 maintenance.
   int32_t steal;
   // Optional (nullptr = off): per execution position, kTraceWords words written by
   // the workgroup that ran it: wall-clock ticks (100 MHz) when it took the position,

@@ -3,6 +3,8 @@
 
 #include <algorithm>
 #include <numeric>
+#include <tuple>
+#include <utility>
 
 namespace csg {
 
@@ -112,8 +114,10 @@ std::string make_grouped_schedule(int32_t world, int32_t rank, int32_t n_groups,
 }
 
 std::string build_tile_map(const Schedule& s, int64_t M, int64_t N, int32_t bm, int32_t bn, bool producer,
-                           const std::vector<int64_t>& group_rows, TileMap* out) {
+                           const std::vector<int64_t>& group_rows, TileMap* out, int32_t intra_order,
+                           int32_t group_m) {
   if (M < 1 || N < 1 || bm < 1 || bn < 1) return "shape and tile sizes must be positive";
+  if (intra_order < 0 || intra_order > 1 || group_m < 1) return "unknown intra-chunk order";
   if (s.total_rows != M) return "the schedule's chunks do not cover exactly M rows";
   TileMap tm;
   const int64_t nN = (N + bn - 1) / bn;
@@ -180,8 +184,25 @@ std::string build_tile_map(const Schedule& s, int64_t M, int64_t N, int32_t bm, 
   }
   tm.order.resize(n_tiles);
   std::iota(tm.order.begin(), tm.order.end(), 0);
-  std::stable_sort(tm.order.begin(), tm.order.end(),
-                   [&](int32_t a, int32_t b) { return rowkey[a / nN] < rowkey[b / nN]; });
+  if (intra_order == 0) {
+    std::stable_sort(tm.order.begin(), tm.order.end(),
+                     [&](int32_t a, int32_t b) { return rowkey[a / nN] < rowkey[b / nN]; });
+  } else {
+    // band of a row tile: its rank among the row tiles of the same key (ascending), / group_m
+    std::vector<int32_t> band(tm.row_tiles.size());
+    std::vector<std::pair<int32_t, int32_t>> by_key(tm.row_tiles.size());
+    for (size_t m = 0; m < by_key.size(); ++m) by_key[m] = {rowkey[m], static_cast<int32_t>(m)};
+    std::sort(by_key.begin(), by_key.end());
+    for (size_t i = 0, rank = 0; i < by_key.size(); ++i) {
+      rank = (i > 0 && by_key[i].first == by_key[i - 1].first) ? rank + 1 : 0;
+      band[by_key[i].second] = static_cast<int32_t>(rank) / group_m;
+    }
+    auto sort_key = [&](int32_t t) {
+      const int32_t m = static_cast<int32_t>(t / nN), n = static_cast<int32_t>(t % nN);
+      return std::make_tuple(rowkey[m], band[m], n, m);
+    };
+    std::sort(tm.order.begin(), tm.order.end(), [&](int32_t a, int32_t b) { return sort_key(a) < sort_key(b); });
+  }
   *out = std::move(tm);
   return "";
 }

@@ -6,8 +6,8 @@
 // ordered list of chunk operations, instantiated from parameterised templates.
 // The map follows Section 5.2 (dependency parsing): a tile depends on the chunks
 // its rows read (consumer ops) or write (producer op); the tile list follows the
-// tile-scheduler swizzle: chunks in communication order, the local kernel's raster
-// order inside a chunk.
+// tile-scheduler swizzle: chunks in communication order, and inside a chunk the
+// local kernel's raster order or a band-by-band column order.
 #pragma once
 
 #include <cstdint>
@@ -60,7 +60,11 @@ struct TileMap {
 
 // producer = true selects the emission key (earliest chunk written), false the
 // arrival key (latest chunk read). group_rows empty = one group spanning M.
+// Inside a key, intra_order 0 keeps the raster order; 1 cuts the key's row tiles
+// (ascending) into bands of group_m and visits each band column by column
+// (Section 5.2, intra-chunk swizzle): order = (key, band, n, m).
 std::string build_tile_map(const Schedule& s, int64_t M, int64_t N, int32_t bm, int32_t bn, bool producer,
-                           const std::vector<int64_t>& group_rows, TileMap* out);
+                           const std::vector<int64_t>& group_rows, TileMap* out, int32_t intra_order = 0,
+                           int32_t group_m = 8);
 
 }  // namespace csg

@@ -11,6 +11,10 @@ exposes, for one operator at one shape:
     split gives the bit-identical product, as each output row depends on one chunk
     and each tile's K order is fixed;
   - tile dispatch (per-die tickets or a static stride);
+  - the intra-chunk tile order (raster, or bands of group_m row tiles visited
+    column by column; Section 5.2, intra-chunk swizzle; Section 5.3, intra-tile
+    orders);
+  - the wave-tail split (each die's last partial wave of tiles split along K);
   - split-K for every tile, or for the tiles on the overlap's critical path;
   - the copy realization: copy engines, or the kernel's own workgroups with a
     given number of copy workgroups;
@@ -77,7 +81,8 @@ def search_space(op: str, chunk_splits: Sequence[Optional[int]] = (None,), dispa
                  split_k: Sequence[int] = (1, 2), tail: Sequence[Tuple[int, int]] = ((0, 0), (2, 8)),
                  copy_workgroups: Sequence[int] = (32, 64, 128), sdma: bool = True,
                  kernel_copies: bool = True, tiles: Sequence[Optional[Tuple[int, int]]] = (None,),
-                 grids: Sequence[int] = (0,)) -> List[Candidate]:
+                 grids: Sequence[int] = (0,), intra: Sequence[Tuple[int, int]] = ((0, 0),),
+                 tail_wave: Sequence[int] = (0,)) -> List[Candidate]:
     """Candidates in a fixed order (the first one is the library's default plan).
 
     op: "ag", "rs" or "grouped". GEMM-RS has no copy workgroups (its kernel
@@ -87,7 +92,9 @@ def search_space(op: str, chunk_splits: Sequence[Optional[int]] = (None,), dispa
     the library's default tile. grids: persistent grid sizes to try, 0 for one
     workgroup per co-resident slot (the default); a grid that divides the tile count
     into whole waves (224 for 896 tiles on 256 CUs) keeps the waves in step and the
-    workgroups sharing a die's L2 at the same K steps."""
+    workgroups sharing a die's L2 at the same K steps. intra: (intra_order, group_m)
+    pairs, (0, 0) the raster order. tail_wave: maximum K-slices for each die's last
+    partial wave (0 = off); only combined with per-die dispatch and no other split."""
     if op not in ("ag", "rs", "grouped"):
         raise ValueError("unknown op %r" % op)
     backends: List[Tuple[int, Optional[int]]] = []
@@ -100,14 +107,17 @@ def search_space(op: str, chunk_splits: Sequence[Optional[int]] = (None,), dispa
             backends += [(1, cw) for cw in copy_workgroups]
     out: List[Candidate] = []
     seen = set()
-    for q, (be, cw), disp, sk, (ts, tc), tile, grid in itertools.product(chunk_splits, backends, dispatch, split_k,
-                                                                          tail, tiles, grids):
+    for q, (be, cw), disp, sk, (ts, tc), tile, grid, (io, gm), tw in itertools.product(
+            chunk_splits, backends, dispatch, split_k, tail, tiles, grids, intra, tail_wave):
         if sk > 1 and ts > 1:
+            continue
+        if tw > 1 and (disp == 2 or sk > 1 or ts > 1):
             continue
         bm, bn = tile if tile is not None else (None, None)
         c = Candidate(q, _cfg(copy_backend=be or None, copy_workgroups=cw, tile_dispatch=disp if disp != 1 else None,
                               split_k=sk if sk > 1 else None, tail_split=ts or None, tail_chunks=tc or None,
-                              bm=bm, bn=bn, bk=64 if tile is not None else None, num_workgroups=grid or None))
+                              bm=bm, bn=bn, bk=64 if tile is not None else None, num_workgroups=grid or None,
+                              intra_order=io or None, group_m=gm if io else None, tail_wave=tw if tw > 1 else None))
         if c not in seen:
             seen.add(c)
             out.append(c)

@@ -67,14 +67,17 @@ MAP_CASES = [
 ]
 
 
+@pytest.mark.parametrize("intra", [(0, 0), (1, 2), (1, 3), (1, 8)], ids=lambda i: "intra%d-g%d" % i)
 @pytest.mark.parametrize("case", MAP_CASES, ids=lambda c: "-".join(map(str, c)))
-def test_plan_map_matches_oracle_bit_exact(case):
+def test_plan_map_matches_oracle_bit_exact(case, intra):
     op, W, r, S, Q, kind, N, BM, BN = case
+    io, g = intra
     perm = si.draw_permutation(11, W + r, (W - 1) * Q) if kind == "permutation" else None
     ch, od = oracle.uniform_schedule(W, r, S, Q, kind, perm)
-    dm = oracle.dep_map(ch, od, W * S, N, BM, BN, producer=(op == "rs"))
+    dm = oracle.dep_map(ch, od, W * S, N, BM, BN, producer=(op == "rs"), intra_order=io, group_m=max(g, 1))
     s = csg.Schedule.uniform(W, r, S, Q, kind, perm)
-    p = csg.Plan(op, W * S, N, 64, "bf16", "bf16", s, cfg={"bm": BM, "bn": BN}, device=-1)
+    p = csg.Plan(op, W * S, N, 64, "bf16", "bf16", s, cfg={"bm": BM, "bn": BN, "intra_order": io, "group_m": g},
+                 device=-1)
     m = p.get_map()
     assert np.array_equal(m["tile_ptr"], dm.tile_ptr)
     assert np.array_equal(m["tile_chunks"], dm.tile_chunks)
@@ -83,15 +86,18 @@ def test_plan_map_matches_oracle_bit_exact(case):
     assert np.array_equal(m["tile_order"], dm.order)
 
 
+@pytest.mark.parametrize("intra", [(0, 0), (1, 2)], ids=lambda i: "intra%d-g%d" % i)
 @pytest.mark.parametrize("BM,BN", [(256, 256), (128, 64), (96, 128)])
-def test_grouped_plan_map_matches_oracle(BM, BN):
+def test_grouped_plan_map_matches_oracle(BM, BN, intra):
+    io, g = intra
     routing = si.draw_topk_routing(5, 3, 2048, 8, 2, 1.2)
     _, counts = si.grouped_layout(routing, 8, 8)
     ch, od, gr = oracle.grouped_schedule(8, 2, counts)
     M = sum(gr)
-    dm = oracle.dep_map(ch, od, M, 1792, BM, BN, group_rows=gr)
+    dm = oracle.dep_map(ch, od, M, 1792, BM, BN, group_rows=gr, intra_order=io, group_m=max(g, 1))
     s = csg.Schedule.grouped(8, 2, counts)
-    p = csg.Plan("grouped", M, 1792, 4096, "bf16", "bf16", s, group_rows=gr, cfg={"bm": BM, "bn": BN}, device=-1)
+    p = csg.Plan("grouped", M, 1792, 4096, "bf16", "bf16", s, group_rows=gr,
+                 cfg={"bm": BM, "bn": BN, "intra_order": io, "group_m": g}, device=-1)
     m = p.get_map()
     assert np.array_equal(m["tile_ptr"], dm.tile_ptr)
     assert np.array_equal(m["tile_chunks"], dm.tile_chunks)
@@ -149,6 +155,11 @@ def test_validation_errors():
         == csg.CSG_ERR_INVALID
     assert _status(csg.Plan, "ag", 128, 64, 64, "bf16", "bf16", s, cfg={"tail_split": -1}, device=-1) \
         == csg.CSG_ERR_INVALID
+    for bad in ({"intra_order": 2}, {"intra_order": -1}, {"group_m": -1}, {"tail_wave": 65}, {"tail_wave": -1}):
+        assert _status(csg.Plan, "ag", 128, 64, 64, "bf16", "bf16", s, cfg=bad, device=-1) == csg.CSG_ERR_INVALID
+    # a grid given with the wave-tail split must cover every die evenly
+    assert _status(csg.Plan, "ag", 128, 64, 64, "bf16", "bf16", s, cfg={"tail_wave": 2, "num_workgroups": 12},
+                   device=-1) == csg.CSG_ERR_INVALID
     # split tiles stay on their die: a given grid must cover every die evenly
     assert _status(csg.Plan, "ag", 128, 64, 64, "bf16", "bf16", s, cfg={"split_k": 2, "num_workgroups": 12},
                    device=-1) == csg.CSG_ERR_INVALID

@@ -2,8 +2,10 @@
 candidate, with stand-in plans (no GPU)."""
 import time
 
+import numpy as np
 import pytest
 
+import oracle
 import paper_2601_20595_amd as csg
 from paper_2601_20595_amd import tune
 
@@ -112,3 +114,28 @@ def test_search_space_grid_dimension():
     assert grids[0] == base[0]
     assert len(grids) == 2 * len(base)
     assert sum(1 for c in grids if ("num_workgroups", 224) in c.cfg) == len(base)
+
+
+def test_search_space_intra_order_and_wave_tail_dimensions():
+    """The intra-chunk order and the wave-tail split are search dimensions; the default
+    candidate stays first, and the wave-tail split is only combined with per-die
+    dispatch and no other split. Every candidate builds a host plan whose map equals
+    the oracle's for its intra order."""
+    base = tune.search_space("ag", kernel_copies=False)
+    sp = tune.search_space("ag", kernel_copies=False, intra=((0, 0), (1, 2), (1, 8)), tail_wave=(0, 2))
+    assert sp[0] == base[0]
+    # every other combination comes once in raster order and once per band height
+    assert sum(1 for c in sp if ("intra_order", 1) in c.cfg) == 2 * sum(1 for c in sp if ("intra_order", 1) not in c.cfg)
+    for c in sp:
+        d = c.cfg_dict()
+        if d.get("tail_wave"):
+            assert d.get("tile_dispatch", 1) != 2 and "split_k" not in d and "tail_split" not in d
+    make = tune.uniform_plan_factory("ag", 4 * 512, 768, 256, "bf16", "bf16", 4, 1, 512, "ring", 2, device=-1)
+    chunks, order = oracle.uniform_schedule(4, 1, 512, 2, "ring")
+    for c in sp:
+        p = make(c)
+        d = c.cfg_dict()
+        dm = oracle.dep_map(chunks, order, 2048, 768, 256, 256, intra_order=d.get("intra_order", 0),
+                            group_m=d.get("group_m", 8))
+        assert np.array_equal(p.get_map()["tile_order"], dm.order), c.label()
+        p.close()
