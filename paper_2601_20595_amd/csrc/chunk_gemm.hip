@@ -840,6 +840,44 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
         __syncthreads();
         skip = __builtin_amdgcn_readfirstlane(s_state) < 0;
         const int64_t prow = td.row_begin - a.own_row0;
+        if constexpr (kOutBf16 && Loop::BM == 256 && Loop::BN == 256 && kThreads == 512) {
+          // Each peer's partial tile (256 rows of 512 bytes) is staged in the main loop's
+          // LDS with row-contiguous 16-byte DMA (two rows per instruction), then read
+          // back in the accumulator layout. The 16-byte pieces of row r are stored at
+          // position (piece ^ (r % 32)), so the 32 rows a read instruction touches fall
+          // in distinct bank groups. Loads past the tile's last row read 0.
+          constexpr int kRowB = 512;
+          const uint32_t lds_base =
+              __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_ptr_t)lds)));
+          const int pitch = N32 * 2;
+          const int pr = lane >> 5, pc = lane & 31;
+          for (int j = 0; j < (skip ? 0 : a.n_peers); ++j) {
+            const __amdgpu_buffer_rsrc_t rsP =
+                make_rsrc(a.partials + ((static_cast<int64_t>(j) * a.own_rows + prow) * a.N + col0) * kOutBytes,
+                          static_cast<int64_t>(g.arows) * a.N * kOutBytes);
+            __syncthreads();  // every wave is done reading LDS (main loop or previous peer)
+#pragma unroll
+            for (int q2 = 0; q2 < 16; ++q2) {
+              const int r = wave * 32 + 2 * q2 + pr;
+              const uint32_t l0 = __builtin_amdgcn_readfirstlane(lds_base + (wave * 32 + 2 * q2) * kRowB);
+              dma16(rsP, l0, r * pitch + ((pc ^ (r & 31)) << 4), 0);
+            }
+            wait_dma_all();
+            __syncthreads();
+#pragma unroll
+            for (int r = 0; r < kRuns; ++r) {
+              const int i = r / (NI * 4), jj = (r / 4) % NI, q = r % 4;
+              const int row = vrow + 32 * i;
+              const int colb = (vcol + 32 * jj + 8 * q) * 2;
+              const u32x2 raw =
+                  *reinterpret_cast<const u32x2*>(lds + row * kRowB + (((colb >> 4) ^ (row & 31)) << 4) + (colb & 15));
+              acc[i][jj][4 * q + 0] += __builtin_bit_cast(float, raw.x << 16);
+              acc[i][jj][4 * q + 1] += __builtin_bit_cast(float, raw.x & 0xffff0000u);
+              acc[i][jj][4 * q + 2] += __builtin_bit_cast(float, raw.y << 16);
+              acc[i][jj][4 * q + 3] += __builtin_bit_cast(float, raw.y & 0xffff0000u);
+            }
+          }
+        } else {
         for (int j = 0; j < (skip ? 0 : a.n_peers); ++j) {
           const __amdgpu_buffer_rsrc_t rsP =
               make_rsrc(a.partials + ((static_cast<int64_t>(j) * a.own_rows + prow) * a.N + col0) * kOutBytes,
@@ -867,6 +905,7 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) acc[i][jj][4 * q + e] += f[e];
           }
+        }
         }
       }
     }
