@@ -18,10 +18,14 @@
 //   values, transposed: O^T += V^T . P^T. P^T is the score registers converted to bf16;
 //     the order in which those registers list the keys is matched by reading V^T rows
 //     from LDS in the same order (two 8-byte reads per fragment).
-// The K tile is row-major in LDS with 272-byte rows, the V tile is transposed through
-// registers into 136-byte rows: both paddings keep the fragment reads free of bank
-// conflicts. Scores are scaled into base 2 (exp2), and the log-sum-exp is returned in
-// natural log.
+// Both tiles reach LDS by DMA (buffer_load ... lds, no register staging) and stay
+// unpadded: the K tile's 16-byte pieces and the V tile's 32-byte units are placed by XOR
+// swizzles of the row index, and V^T fragments come from transposing reads
+// (ds_read_b64_tr_b16), so the fragment reads are free of bank conflicts. The loop is
+// software-pipelined by one block: on a chunk's last block the scores of the next block
+// are computed from the other K buffer and discarded, one score block (16 MFMAs per
+// wave) per chunk and unit. Scores are scaled into base 2 (exp2), and the log-sum-exp
+// is returned in natural log.
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
