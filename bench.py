@@ -63,6 +63,9 @@ def parse():
                     help="cold isolated calls per mode (0 = as many as --steps)")
     ap.add_argument("--plan-cfg", type=str, default="",
                     help="JSON object of plan configuration fields for the measured plan (e.g. tile order)")
+    ap.add_argument("--tune", action="store_true",
+                    help="instead of the bench line, run the autotuner on the workload (chunk split, intra-chunk "
+                         "order, dispatch, copy realization) and print its table as one JSON line")
     return ap.parse_args()
 
 
@@ -84,6 +87,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
+    if args.tune:
+        tune_workload(args)
+        return
     dev = "cuda:0"
     arch = csg.csg_device_check(0)
     w = si.WORKLOADS[args.config]
@@ -346,6 +352,90 @@ def kernel_copy_sweep(w, sched, group_rows, d, timed_loop, moved_bytes, args, sw
             "tflops": round(w.flops / (ms["overlap"] * 1e-3) / 1e12, 2),
             "copy_only_GBps": round(moved_bytes / (ms["copy_only"] * 1e-3) / 1e9, 2)}
     return out
+
+
+def tune_workload(args):
+    """The enumerate-and-measure autotuner on one workload: chunk splits (uniform
+    schedules), intra-chunk tile order, tile dispatch and copy realization, each
+    candidate timed as back-to-back overlap calls. Prints one JSON line with every
+    candidate's ms per step, the best one, and whether the best plan's product equals
+    the default plan's bit for bit."""
+    import torch
+    import paper_2601_20595_amd as csg
+    import seeded_inputs as si
+    from paper_2601_20595_amd import tune
+
+    dev = "cuda:0"
+    w = si.WORKLOADS[args.config]
+    if w.op not in ("ag", "rs", "grouped"):
+        print("bench.py --tune: the tuner covers the all-gather, reduce-scatter and grouped GEMMs", file=sys.stderr)
+        sys.exit(2)
+    d = si.draw(w)
+
+    def to_dev(arr):
+        if arr.dtype == np.uint16:
+            return torch.from_numpy(np.ascontiguousarray(arr).view(np.int16)).to(dev)
+        return torch.from_numpy(np.ascontiguousarray(arr)).to(dev)
+
+    A, B = to_dev(d.A.device_array), to_dev(d.B.device_array)
+    out_t = torch.int16 if w.out_dtype == "bf16" else torch.float32
+    C = torch.empty((w.M, w.N), dtype=out_t, device=dev)
+    comp, cp = torch.cuda.Stream(device=dev), torch.cuda.Stream(device=dev)
+    if w.op == "rs":
+        outgoing = torch.zeros((w.M, w.N), dtype=out_t, device=dev)
+        call = lambda p, m: p.gemm_rs(A, B, C, outgoing, m, comp, cp)
+    else:
+        landing = A.clone()
+        if w.op == "grouped":
+            call = lambda p, m: p.grouped_gemm(landing, A, B, C, m, comp, cp)
+        else:
+            call = lambda p, m: p.ag_gemm(landing, A, B, C, m, comp, cp)
+    if w.op == "grouped":
+        group_rows = [int(x) for x in d.counts.sum(axis=0)]
+
+        def make(c):
+            s = csg.Schedule.grouped(w.world, w.rank, d.counts)
+            try:
+                return csg.Plan(w.op, w.M, w.N, w.K, w.dtype, w.out_dtype, s, group_rows=group_rows,
+                                cfg=c.cfg_dict())
+            finally:
+                s.close()
+        splits = (None,)
+    else:
+        make = tune.uniform_plan_factory(w.op, w.M, w.N, w.K, w.dtype, w.out_dtype, w.world, w.rank,
+                                         w.shard_rows, w.order, w.chunks_per_shard,
+                                         perm_for=lambda q: d.perm, delays_for=lambda q: d.delays_us)
+        # the workload's own split first: the first candidate is the library's default plan
+        splits = (w.chunks_per_shard,) + tuple(q for q in (1, 2, 4, 8) if q != w.chunks_per_shard and
+                                               w.shard_rows % q == 0 and (w.shard_rows // q) % 128 == 0)
+        if d.delays_us is not None:
+            splits = (None,)  # the release delays are drawn per chunk of the workload's own split
+    cands = tune.search_space(w.op, chunk_splits=splits, split_k=(1,), tail=((0, 0),), copy_workgroups=(64,),
+                              intra=((0, 0), (1, 1), (1, 2), (1, 4)))
+    res, best = tune.autotune(make, call, cands, steps=args.steps, warmup=args.warmup, keep_best=True)
+    call(best, "overlap")
+    best.check()
+    torch.cuda.synchronize()
+    got = C.clone()
+    p0 = make(cands[0])
+    call(p0, "overlap")
+    p0.check()
+    torch.cuda.synchronize()
+    same = bool(torch.equal(got, C))
+    p0.close()
+    best.close()
+    ran = [t for t in res.trials if t.ms_per_step]
+    print(json.dumps({
+        "tune": {"workload": w.name, "candidates": len(cands), "ran": len(ran), "steps": args.steps,
+                 "warmup": args.warmup, "objective": "ms per step of back-to-back overlap calls",
+                 "default": cands[0].label(), "default_ms": next((round(t.ms_per_step, 4) for t in res.trials
+                                                                   if t.candidate == cands[0] and t.ms_per_step), None),
+                 "best": res.best.label(), "best_ms": round(res.best_ms, 4),
+                 "best_tflops": round(w.flops / (res.best_ms * 1e-3) / 1e12, 2),
+                 "worst_ms": round(max(t.ms_per_step for t in ran), 4),
+                 "best_equals_default_product": same,
+                 "table": [[t.candidate.label(), round(t.ms_per_step, 4) if t.ms_per_step else t.status]
+                           for t in res.trials]}}), flush=True)
 
 
 # Per measured kernel: its committed HBM-traffic summary and the sources it was taken from.
