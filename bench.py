@@ -44,6 +44,17 @@ sys.path.insert(0, ROOT)
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}  # MI355X dense MFMA peaks
 HBM_PEAK_GBS = 8000.0
 CAL_BYTES = 256 << 20    # bytes read (and written) by the calibration copy
+# The operator implementation per workload, as the autotuner selected it with cold
+# isolated calls as the objective (`bench.py --config N --tune --objective isolated`),
+# among the copy-engine candidates (the copy engines stand in for the links of a real
+# collective; the kernel's own copies move chunks inside HBM faster than links would):
+# plan configuration fields. --default-plan measures the library's defaults instead.
+TUNED_PLAN_CFG = {
+    2: {"tail_split": 2, "tail_chunks": 4},
+    3: {"tail_split": 2, "tail_chunks": 4, "tile_dispatch": 2},
+    4: {"bm": 128, "bn": 256, "bk": 64, "tile_dispatch": 2, "tail_split": 2, "tail_chunks": 8},
+    5: {"tail_split": 2, "tail_chunks": 8},
+}
 FLUSH_BYTES = 512 << 20  # written before each isolated call: more than the last-level cache and every L2
 
 
@@ -63,6 +74,11 @@ def parse():
                     help="cold isolated calls per mode (0 = as many as --steps)")
     ap.add_argument("--plan-cfg", type=str, default="",
                     help="JSON object of plan configuration fields for the measured plan (e.g. tile order)")
+    ap.add_argument("--default-plan", action="store_true",
+                    help="measure the library's default plan instead of the workload's tuned plan configuration")
+    ap.add_argument("--objective", choices=("steady", "isolated"), default="steady",
+                    help="--tune: time each candidate as back-to-back overlap calls (steady) or as cold "
+                         "isolated overlap calls (isolated, the median device time per call)")
     ap.add_argument("--tune", action="store_true",
                     help="instead of the bench line, run the autotuner on the workload (chunk split, intra-chunk "
                          "order, dispatch, copy realization) and print its table as one JSON line")
@@ -106,7 +122,10 @@ def main():
     else:
         sched = csg.Schedule.uniform(w.world, w.rank, w.shard_rows, w.chunks_per_shard, w.order, d.perm)
         group_rows = None
-    cfg = {"copy_engines": args.lanes} if args.lanes else {}
+    tuned = not args.default_plan and args.config in TUNED_PLAN_CFG
+    cfg = dict(TUNED_PLAN_CFG[args.config]) if tuned else {}
+    if args.lanes:
+        cfg["copy_engines"] = args.lanes
     if args.plan_cfg:
         cfg.update(json.loads(args.plan_cfg))
     cfg = cfg or None
@@ -205,14 +224,15 @@ def main():
         wall = time.perf_counter() - t0
         return wall, p.kernel_times(steps)
 
-    def isolated(mode, reps, warmup):
+    def isolated(mode, reps, warmup, p=None):
         """Cold isolated calls: the caches flushed and the device idle before each one;
         per call, the device time (ms) from an event queued on the compute stream just
         before the call to one queued after csg_plan_join (the call's kernel and every
         copy it issued have completed)."""
+        p = p or plan
         for _ in range(warmup):
-            call(mode)
-        plan.check()
+            call(mode, p)
+        p.check()
         ev0 = torch.cuda.Event(enable_timing=True)
         ev1 = torch.cuda.Event(enable_timing=True)
         tot = []
@@ -221,11 +241,11 @@ def main():
                 flush_buf.fill_(i)
             torch.cuda.synchronize()
             ev0.record(compute)
-            call(mode)
-            plan.join(compute)
+            call(mode, p)
+            p.join(compute)
             ev1.record(compute)
             ev1.synchronize()
-            plan.check()
+            p.check()
             tot.append(ev0.elapsed_time(ev1))
         return np.array(tot)
 
@@ -257,6 +277,26 @@ def main():
     t_comp = float(np.median(tot_c))
     t_copy = float(np.median(tot_x))
     overlap_eff = max(t_comp, t_copy) / t_total
+    default_iso = None
+    if tuned:
+        # the same cold isolated calls on the library's default plan, for comparison
+        if w.op == "attn":
+            p0 = csg.AttnPlan(e["heads"], e["kv_heads"], e["head_dim"], w.M, sched)
+        else:
+            p0 = csg.Plan(w.op, w.M, w.N, w.K, w.dtype, w.out_dtype, sched, group_rows=group_rows)
+        if d.delays_us is not None:
+            p0.set_copy_delays(d.delays_us)
+        d_tot = float(np.median(isolated("overlap", reps, args.warmup, p0)))
+        d_comp = float(np.median(isolated("compute_only", reps, args.warmup, p0)))
+        d_copy = float(np.median(isolated("copy_only", reps, args.warmup, p0)))
+        _, d_ker_c = timed_loop("compute_only", args.steps, args.warmup, p0)
+        p0.close()
+        d_kc = float(np.mean(d_ker_c))
+        default_iso = {"plan_cfg": {}, "t_total_ms": round(d_tot, 4), "t_compute_only_ms": round(d_comp, 4),
+                       "t_copy_only_ms": round(d_copy, 4), "overlap_eff": round(max(d_comp, d_copy) / d_tot, 4),
+                       "e2e_tflops_isolated": round(w.flops / (d_tot * 1e-3) / 1e12, 2),
+                       "compute_only_kernel_ms_mean": round(d_kc, 4),
+                       "roofline_compute_only_frac": round(w.flops / (d_kc * 1e-3) / 1e12 / MFMA_PEAK_TFLOPS[w.dtype], 4)}
 
     peak = MFMA_PEAK_TFLOPS[w.dtype]
     k_overlap = float(np.mean(ker))
@@ -288,6 +328,8 @@ def main():
                    "num_workgroups": plan.info.num_workgroups,
                    "tile": [plan.info.bm, plan.info.bn, plan.info.bk],
                    "plan_cfg": cfg or {},
+                   "plan_cfg_source": ("autotuner, cold isolated calls (bench.py --tune --objective isolated)"
+                                       if tuned else "library defaults" if not cfg else "command line"),
                    "landing_buffers": 1 if landing is not None else None},
         # cold isolated calls (device events; caches flushed before each)
         "overlap_eff": round(overlap_eff, 4),
@@ -308,7 +350,7 @@ def main():
         "compute_only_tflops": round(w.flops / (ms_comp * 1e-3) / 1e12, 2),
         "roofline": {"bound": "mfma", "achieved": round(tf_overlap, 2), "peak": peak,
                      "unit": "TFLOP/s", "frac": round(tf_overlap / peak, 4),
-                     "traffic": kernel_traffic(w.name, kernel_name), "kernel": kernel_name,
+                     "traffic": kernel_traffic(w.name, kernel_name, cfg), "kernel": kernel_name,
                      "phase": "overlap (timed region)",
                      "kernel_ms_mean": round(k_overlap, 4),
                      "frac_of_measured_peak": round(tf_overlap / mpeak, 4) if mpeak else None},
@@ -319,6 +361,8 @@ def main():
                                   "frac_of_measured_peak": round(tf_comp / mpeak, 4) if mpeak else None},
         "mfma_peak_measured": measured,
     }
+    if default_iso is not None:
+        rec["default_plan_isolated"] = default_iso
     if not args.no_kernel_copies and w.op not in ("ar", "attn"):  # these copy with the engines only
         rec["kernel_copy_backend"] = kernel_copy_sweep(w, sched, group_rows, d, timed_loop, moved_bytes, args)
     if not args.no_cpu_baseline:
@@ -410,9 +454,41 @@ def tune_workload(args):
                                                w.shard_rows % q == 0 and (w.shard_rows // q) % 128 == 0)
         if d.delays_us is not None:
             splits = (None,)  # the release delays are drawn per chunk of the workload's own split
-    cands = tune.search_space(w.op, chunk_splits=splits, split_k=(1,), tail=((0, 0),), copy_workgroups=(64,),
-                              intra=((0, 0), (1, 1), (1, 2), (1, 4)))
-    res, best = tune.autotune(make, call, cands, steps=args.steps, warmup=args.warmup, keep_best=True)
+    measure_fn = None
+    if args.objective == "isolated":
+        # cold isolated calls: a 512 MiB write evicts the inputs from every cache, then
+        # the device time from an event before the call to one after csg_plan_join
+        flush = torch.empty(FLUSH_BYTES // 4, dtype=torch.int32, device=dev)
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+        def measure_fn(plan, call_, steps, warmup):
+            for _ in range(warmup):
+                call_(plan, "overlap")
+            plan.check()
+            ts = []
+            for i in range(steps):
+                with torch.cuda.stream(comp):
+                    flush.fill_(i)
+                torch.cuda.synchronize()
+                ev0.record(comp)
+                call_(plan, "overlap")
+                plan.join(comp)
+                ev1.record(comp)
+                ev1.synchronize()
+                plan.check()
+                ts.append(ev0.elapsed_time(ev1))
+            return float(np.median(ts))
+
+        # the chunk split stays the workload's; the tile shape and the tail splits join
+        # the space (they decide how much work is left when the last chunk lands)
+        cands = tune.search_space(w.op, chunk_splits=splits[:1], split_k=(1,),
+                                  tail=((0, 0), (2, 4), (2, 8), (2, 16)), copy_workgroups=(64,),
+                                  tiles=(None, (128, 256)), intra=((0, 0), (1, 4)))
+    else:
+        cands = tune.search_space(w.op, chunk_splits=splits, split_k=(1,), tail=((0, 0),), copy_workgroups=(64,),
+                                  intra=((0, 0), (1, 1), (1, 2), (1, 4)))
+    res, best = tune.autotune(make, call, cands, steps=args.steps, warmup=args.warmup, keep_best=True,
+                              measure_fn=measure_fn)
     call(best, "overlap")
     best.check()
     torch.cuda.synchronize()
@@ -427,7 +503,9 @@ def tune_workload(args):
     ran = [t for t in res.trials if t.ms_per_step]
     print(json.dumps({
         "tune": {"workload": w.name, "candidates": len(cands), "ran": len(ran), "steps": args.steps,
-                 "warmup": args.warmup, "objective": "ms per step of back-to-back overlap calls",
+                 "warmup": args.warmup,
+                 "objective": ("median ms of cold isolated overlap calls" if args.objective == "isolated"
+                               else "ms per step of back-to-back overlap calls"),
                  "default": cands[0].label(), "default_ms": next((round(t.ms_per_step, 4) for t in res.trials
                                                                    if t.candidate == cands[0] and t.ms_per_step), None),
                  "best": res.best.label(), "best_ms": round(res.best_ms, 4),
@@ -456,10 +534,11 @@ def kernel_sources_sha256(kernel: str = "chunk_gemm") -> str:
     return h.hexdigest()
 
 
-def kernel_traffic(workload: str, kernel: str = "chunk_gemm"):
+def kernel_traffic(workload: str, kernel: str = "chunk_gemm", plan_cfg=None):
     """HBM bytes per launch of the kernel (FETCH_SIZE + WRITE_SIZE, scaled by the
     calibration copy) from the committed counter summary, or None when that summary is
-    missing, covers another workload, or was taken from a different kernel source."""
+    missing, covers another workload or plan configuration, or was taken from a
+    different kernel source."""
     try:
         with open(KERNEL_TRAFFIC[kernel][0]) as f:
             t = json.load(f)
@@ -467,6 +546,8 @@ def kernel_traffic(workload: str, kernel: str = "chunk_gemm"):
         return None
     entry = t.get("workloads", {}).get(workload)
     if not entry or t.get("source_sha256") != kernel_sources_sha256(kernel):
+        return None
+    if entry.get("plan_cfg", {}) != (plan_cfg or {}):
         return None
     return entry.get("bytes_per_launch")
 

@@ -434,8 +434,9 @@ csg_status csg_ring_attn(csg_plan* p, const void* q, void* k_landing, void* v_la
 csg_status csg_plan_check(csg_plan* p, csg_diag* out);
 
 /* Makes `stream` (a hipStream_t of the plan's device) wait, on the device, until every
- * copy the plan's last call issued has completed: a one-thread kernel is queued on it
- * that polls the copies' completion signals, at most the plan's timeout_ms per copy
+ * copy the plan's last call issued has completed: a one-workgroup kernel is queued on
+ * it whose threads poll the copies' completion signals (one thread per signal, up to
+ * 256 at a time), at most the plan's timeout_ms per copy
  * (a copy still running then is reported by csg_plan_check, not here). Work queued on
  * `stream` afterwards follows the copies without a host wait, e.g. a consumer of
  * GEMM-RS's outgoing buffer, or an event that timestamps the end of the call's copies.

@@ -1,8 +1,8 @@
 // Two small kernels that serve measurement and stream ordering, outside the GEMM:
 //
-//   chunk_join   one thread waits (bounded) until the completion values of a list of
-//                copies read 0, so work queued behind it on its stream follows those
-//                copies on the device (csg_plan_join);
+//   chunk_join   waits (bounded) until the completion values of a list of copies read
+//                0, so work queued behind it on its stream follows those copies on the
+//                device (csg_plan_join);
 //   mfma_peak    every SIMD of every CU issues independent v_mfma_f32_32x32x16_bf16
 //                back to back on register operands: the bf16 matrix rate the chip
 //                sustains under that load, and the shader clock it runs at
@@ -18,13 +18,16 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-// One thread polls each value in turn, about every 20 ns, for at most timeout_ticks
-// (100 MHz wall clock) per value; a value still not 0 then sets *timed_out and the
-// kernel ends anyway. No barrier, no other thread: the kernel always finishes.
-__global__ __launch_bounds__(64) void chunk_join(const int64_t* const* values, int32_t n, uint64_t timeout_ticks,
-                                                  uint32_t* timed_out) {
-  if (threadIdx.x != 0) return;
-  for (int32_t i = 0; i < n; ++i) {
+constexpr int kJoinThreads = 256;
+
+// Thread t polls values t, t + 256, ..., each about every 20 ns for at most
+// timeout_ticks (100 MHz wall clock); a value still not 0 then sets *timed_out and
+// the thread moves on. A completion value sits in memory that a load reaches with
+// over a microsecond of latency, so the threads' loads overlap instead of queueing
+// behind one another. No barrier: every thread ends on its own, and so the kernel.
+__global__ __launch_bounds__(kJoinThreads) void chunk_join(const int64_t* const* values, int32_t n,
+                                                           uint64_t timeout_ticks, uint32_t* timed_out) {
+  for (int32_t i = static_cast<int32_t>(threadIdx.x); i < n; i += kJoinThreads) {
     const int64_t* p = values[i];
     const uint64_t t0 = wall_clock64();
     while (__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) != 0) {
@@ -39,7 +42,7 @@ __global__ __launch_bounds__(64) void chunk_join(const int64_t* const* values, i
 
 hipError_t launch_join(const int64_t* const* values, int32_t n, uint64_t timeout_ticks, uint32_t* timed_out,
                        hipStream_t stream) {
-  hipLaunchKernelGGL(chunk_join, dim3(1), dim3(64), 0, stream, values, n, timeout_ticks, timed_out);
+  hipLaunchKernelGGL(chunk_join, dim3(1), dim3(kJoinThreads), 0, stream, values, n, timeout_ticks, timed_out);
   return hipGetLastError();
 }
 

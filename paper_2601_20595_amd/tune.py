@@ -138,12 +138,18 @@ def measure(plan: Plan, call: Callable[[Plan, str], None], steps: int, warmup: i
 
 def autotune(make_plan: Callable[[Candidate], Plan], call: Callable[[Plan, str], None],
              candidates: Sequence[Candidate], steps: int = 10, warmup: int = 3,
-             keep_best: bool = False) -> Tuple[TuneResult, Optional[Plan]]:
+             keep_best: bool = False,
+             measure_fn: Optional[Callable[[Plan, Callable[[Plan, str], None], int, int], float]] = None
+             ) -> Tuple[TuneResult, Optional[Plan]]:
     """Times every candidate; returns the result and, with keep_best, the best plan
     (the others are destroyed as soon as they are measured).
 
     make_plan(candidate) builds the plan (and sets its copy delays, if any);
-    call(plan, mode) makes one call with the caller's buffers and streams."""
+    call(plan, mode) makes one call with the caller's buffers and streams;
+    measure_fn(plan, call, steps, warmup) gives the candidate's time in ms (default:
+    `measure`, the steady state of back-to-back overlap calls; a caller may time cold
+    isolated calls instead, whose end it can see on the device)."""
+    measure_fn = measure_fn or measure
     if not candidates:
         raise ValueError("no candidates")
     trials: List[Trial] = []
@@ -156,7 +162,7 @@ def autotune(make_plan: Callable[[Candidate], Plan], call: Callable[[Plan, str],
             trials.append(Trial(cand, None, "rejected: %s" % e))
             continue
         try:
-            ms = measure(plan, call, steps, warmup)
+            ms = measure_fn(plan, call, steps, warmup)
         except CsgError as e:
             plan.close()
             trials.append(Trial(cand, None, "failed: %s" % e))

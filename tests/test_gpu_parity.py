@@ -473,11 +473,16 @@ def _full(cfg_id):
     return w, d, chunks, order, s, None
 
 
-@pytest.mark.parametrize("cfg_id", [1, 2, 3, 4, 5])
-def test_full_size_workload_sampled(cfg_id):
+@pytest.mark.parametrize("cfg_id,tuned", [(1, False), (2, False), (2, True), (3, False), (3, True), (4, False),
+                                          (4, True), (5, False), (5, True)])
+def test_full_size_workload_sampled(cfg_id, tuned):
+    """Each workload at full size with the library's default plan and, where bench.py
+    measures a tuned plan configuration, with that one."""
+    import bench
     w, d, chunks, order, s, gr = _full(cfg_id)
-    _say("full size %s" % w.name)
-    plan = csg.Plan(w.op, w.M, w.N, w.K, w.dtype, w.out_dtype, s, group_rows=gr)
+    cfg = dict(bench.TUNED_PLAN_CFG[cfg_id]) if tuned else None
+    _say("full size %s plan %s" % (w.name, cfg))
+    plan = csg.Plan(w.op, w.M, w.N, w.K, w.dtype, w.out_dtype, s, group_rows=gr, cfg=cfg)
     if d.delays_us is not None:
         plan.set_copy_delays(d.delays_us)
     rows = sample_rows(chunks, extra=24, seed=cfg_id, M=w.M) if w.M > 256 else list(range(w.M))

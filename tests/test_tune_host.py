@@ -139,3 +139,25 @@ def test_search_space_intra_order_and_wave_tail_dimensions():
                             group_m=d.get("group_m", 8))
         assert np.array_equal(p.get_map()["tile_order"], dm.order), c.label()
         p.close()
+
+
+def test_bench_tuned_plan_configurations_are_accepted():
+    """Every plan configuration bench.py measures as a workload's tuned plan is one the
+    library accepts for that workload's shape and schedule (host-only plans)."""
+    import bench
+    import paper_2601_20595_amd as csg
+    import seeded_inputs as si
+    for cid, cfg in bench.TUNED_PLAN_CFG.items():
+        w = si.WORKLOADS[cid]
+        d = si.draw(w) if w.op == "grouped" or w.order == "permutation" else None
+        if w.op == "grouped":
+            s = csg.Schedule.grouped(w.world, w.rank, d.counts)
+            gr = [int(x) for x in d.counts.sum(axis=0)]
+        else:
+            s = csg.Schedule.uniform(w.world, w.rank, w.shard_rows, w.chunks_per_shard, w.order,
+                                     d.perm if d is not None else None)
+            gr = None
+        p = csg.Plan(w.op, w.M, w.N, w.K, w.dtype, w.out_dtype, s, group_rows=gr, cfg=dict(cfg), device=-1)
+        assert (p.info.bm, p.info.bn) == (cfg.get("bm", 256), cfg.get("bn", 256))
+        p.close()
+        s.close()
