@@ -258,7 +258,12 @@ void csg_schedule_destroy(csg_schedule* s);
  * device < 0 makes a host-only plan: the map can be read, no GEMM can run.
  * op CSG_GROUPED_GEMM needs group_rows_host[n_groups] (rows per expert, summing to
  * M) and chunks that stay inside their group; other ops pass NULL, 0.
- * The schedule is copied; it may be destroyed afterwards. */
+ * The schedule is copied; it may be destroyed afterwards.
+ * CSG_ERR_INVALID for a malformed request (M not the rows the chunks cover, a bad
+ * configuration field); CSG_ERR_UNSUPPORTED, for host-only plans too, when K is not a
+ * multiple of the main loop's K step (cfg bk: 64 for bf16, 16 for fp32), N is not a
+ * multiple of 4, or there are more than 4096 chunks; on a device also when no kernel
+ * variant has the tile shape, or a tile's rows exceed 32-bit buffer offsets. */
 csg_status csg_plan_create(csg_op op, int64_t M, int64_t N, int64_t K, csg_dtype in_dtype,
                            csg_dtype out_dtype, const csg_schedule* s,
                            const int64_t* group_rows_host, int32_t n_groups,

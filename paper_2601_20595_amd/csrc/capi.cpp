@@ -1321,6 +1321,12 @@ csg_status csg_plan_create(csg_op op, int64_t M, int64_t N, int64_t K, csg_dtype
     delete p;
     return fail(CSG_ERR_UNSUPPORTED, "at most %d chunks", csg::kernel_max_chunks());
   }
+  // the main loops step K by bk with no partial step, and the epilogue stores runs of
+  // four columns (host-only plans too: they describe a plan a device would run)
+  if (K % c.bk != 0 || N % 4 != 0) {
+    delete p;
+    return fail(CSG_ERR_UNSUPPORTED, "K must be a multiple of %d and N a multiple of 4", c.bk);
+  }
   if (device >= 0) {
     p->key = csg::KernelKey{bf16 ? csg::InType::BF16 : csg::InType::F32, out_dtype == CSG_BF16, !p->consumer(),
                             c.bm, c.bn, c.bk, p->allreduce()};
@@ -1328,10 +1334,6 @@ csg_status csg_plan_create(csg_op op, int64_t M, int64_t N, int64_t K, csg_dtype
       delete p;
       return fail(CSG_ERR_UNSUPPORTED, "no kernel for dtype %d->%d tile %dx%dx%d", in_dtype, out_dtype, c.bm, c.bn,
                   c.bk);
-    }
-    if (K % c.bk != 0 || N % 4 != 0) {
-      delete p;
-      return fail(CSG_ERR_UNSUPPORTED, "K must be a multiple of %d and N a multiple of 4", c.bk);
     }
     // a tile's rows of A, B and C are addressed with 32-bit buffer offsets
     const int64_t ib = bf16 ? 2 : 4, ob = out_dtype == CSG_BF16 ? 2 : 4;

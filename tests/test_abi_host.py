@@ -160,11 +160,25 @@ def test_validation_errors():
     # a grid given with the wave-tail split must cover every die evenly
     assert _status(csg.Plan, "ag", 128, 64, 64, "bf16", "bf16", s, cfg={"tail_wave": 2, "num_workgroups": 12},
                    device=-1) == csg.CSG_ERR_INVALID
-    # split tiles stay on their die: a given grid must cover every die evenly
+    # split plans: a given grid must cover every die evenly (each die's list gets its share)
     assert _status(csg.Plan, "ag", 128, 64, 64, "bf16", "bf16", s, cfg={"split_k": 2, "num_workgroups": 12},
                    device=-1) == csg.CSG_ERR_INVALID
     assert _status(csg.Plan, "ag", 128, 64, 64, "bf16", "bf16", s, cfg={"split_k": 2, "num_workgroups": 16},
                    device=-1) == csg.CSG_OK
+
+
+def test_shapes_the_kernels_do_not_cover_are_rejected():
+    """K must be a multiple of the main loop's K step (64 for bf16, 16 for fp32) and N a
+    multiple of 4 (a store run is four columns): other shapes are refused at plan
+    creation, for every GEMM op, instead of reading past a row or storing a partial run."""
+    s = csg.Schedule.uniform(2, 0, 256, 2, "ring")
+    rs = csg.Schedule.uniform(2, 0, 256, 2, "rs_ring")
+    for op, sched in (("ag", s), ("rs", rs), ("ar", rs)):
+        assert _status(csg.Plan, op, 512, 64, 96, "bf16", "bf16", sched, device=-1) == csg.CSG_ERR_UNSUPPORTED, op
+        assert _status(csg.Plan, op, 512, 64, 24, "f32", "f32", sched, device=-1) == csg.CSG_ERR_UNSUPPORTED, op
+        assert _status(csg.Plan, op, 512, 66, 64, "bf16", "bf16", sched, device=-1) == csg.CSG_ERR_UNSUPPORTED, op
+        assert _status(csg.Plan, op, 512, 64, 128, "bf16", "bf16", sched, device=-1) == csg.CSG_OK, op
+        assert _status(csg.Plan, op, 512, 68, 32, "f32", "f32", sched, device=-1) == csg.CSG_OK, op
 
 
 def test_every_op_rejects_more_chunks_than_the_kernels_track():
