@@ -983,7 +983,52 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
       }
     } else {
       skip = !wait_previous_copy_out();
-      if (!skip) {
+      if constexpr (kOutBf16 && Loop::BN == 256 && (Loop::BM == 256 || Loop::BM == 128) && kThreads == 512) {
+        // Stored straight from the accumulator layout, one instruction writes 16 bytes
+        // of each of 32 rows: partial lines, which for the producer (written through to
+        // memory) the memory side takes at twice their size. The tile is staged in LDS
+        // instead (rows of 512 bytes, 16-byte piece p of row r at position p ^ (r % 32),
+        // the same conflict-free layout as the all-reduce staging) and written out as
+        // whole rows, two per instruction.
+        if (!skip) {
+          constexpr int kRowB = 512;
+          static_assert(Loop::BM * kRowB <= Loop::LDS_BYTES, "the staged tile fits the main loop's LDS");
+          // the lane index passes through an empty asm, so the addresses derived from it
+          // are computed here, per tile, instead of being hoisted out of the tile loop
+          // and held in registers across the main loop
+          int lw = lane;
+          asm volatile("" : "+v"(lw));
+          const int l_row = lw & 31, l_half = lw >> 5;
+          const int wbase = (wm * Loop::WTM + l_row) * kRowB + 8 * l_half;
+          __syncthreads();  // every wave is done reading LDS
+#pragma unroll
+          for (int r = 0; r < kRuns; ++r) {
+            // run (i, j, q): row wm WTM + 32 i + l_row, 16-byte piece wn 8 + 4 j + q (< 32), half l_half
+            const int i = r / (NI * 4), j = (r / 4) % NI, q = r % 4;
+            const int piece = (wn * (Loop::WTN / 8) + 4 * j + q) ^ l_row;
+            *reinterpret_cast<u32x2*>(lds + wbase + i * 32 * kRowB + (piece << 4)) =
+                __builtin_bit_cast(u32x2, __builtin_convertvector(acc_run(r), bf16x4));
+            __builtin_amdgcn_sched_barrier(0);  // convert-and-write one run at a time
+          }
+          __syncthreads();
+          const int pr = lw >> 5, pc = lw & 31;
+          const int c8 = pc * 8;  // first of the piece's 8 columns
+          const int vlane = pr * N32 * 2 + pc * 16;
+          constexpr int kRowsPerWave = Loop::BM / 8;
+#pragma unroll
+          for (int q2 = 0; q2 < kRowsPerWave / 2; ++q2) {
+            const int row0 = wave * kRowsPerWave + 2 * q2;  // this instruction's rows: row0 + pr
+            const u32x4 v =
+                *reinterpret_cast<const u32x4*>(lds + (row0 + pr) * kRowB + ((pc ^ ((row0 + pr) & 31)) << 4));
+            const int voff = row0 + pr < g.arows ? vlane : kDropOffset;
+            const int soff = __builtin_amdgcn_readfirstlane(row0 * N32 * 2);
+            if (c8 + 8 <= g.brows)
+              __builtin_amdgcn_raw_buffer_store_b128(v, rsC, voff, soff, kCStorePolicy);
+            else if (c8 + 4 <= g.brows)  // N is a multiple of 4: a half piece ends the row
+              __builtin_amdgcn_raw_buffer_store_b64(u32x2{v.x, v.y}, rsC, voff, soff, kCStorePolicy);
+          }
+        }
+      } else if (!skip) {
 #pragma unroll
         for (int r = 0; r < kRuns; ++r) {
           store_run(r, acc_run(r));

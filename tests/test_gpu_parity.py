@@ -552,3 +552,61 @@ def test_plan_destroyed_right_after_a_call_waits_for_its_work(op):
             if not ch.is_local:
                 assert np.array_equal(O[ch.row_begin:ch.row_end], G[ch.row_begin:ch.row_end])
     s.close()
+
+
+# ---------------------------------------------------------------------------------
+# The LDS-staged epilogue (bf16 output, 256 x 256 and 128 x 256 tiles): rows written
+# whole from LDS, with ragged row tiles and a last column tile that ends in a half
+# 16-byte piece (N = 8 k + 4), on the consumer and on the producer. C sits at the start
+# of a larger buffer whose tail holds a sentinel: nothing may be written past C's end.
+# ---------------------------------------------------------------------------------
+@pytest.mark.parametrize("op,bm", [("ag", 256), ("ag", 128), ("rs", 256)])
+@pytest.mark.parametrize("N", [260, 516, 772])
+def test_staged_epilogue_ragged_edges(op, bm, N):
+    W, r, S, Q, K = 4, 1, 200, 2, 192
+    M = W * S
+    _say("staged epilogue %s bm=%d N=%d" % (op, bm, N))
+    cfg = {"timeout_ms": 1000, "bm": bm, "bn": 256, "bk": 64}
+    st = streams()
+    guard = 4096
+    flat = torch.full((M * N + guard,), 0x7fc1, dtype=torch.int16, device="cuda")  # bf16 NaN bits
+    c = flat[:M * N].view(M, N)
+    if op == "ag":
+        w, d, perm, chunks, order = _small_ag(W, r, S, Q, "ring", N, K, "bf16", "bf16")
+        s = csg.Schedule.uniform(W, r, S, Q, "ring")
+        plan = csg.Plan("ag", M, N, K, "bf16", "bf16", s, cfg=cfg)
+        a = to_dev(d.A.device_array)
+        landing = a.clone()
+        for ch in chunks:
+            if not ch.is_local:
+                landing[ch.row_begin:ch.row_end].zero_()
+        torch.cuda.synchronize()
+        plan.ag_gemm(landing, a, to_dev(d.B.device_array), c, "overlap", st.compute, st.copy)
+        plan.check()
+        torch.cuda.synchronize()
+        R = oracle.ag_gemm(d.A.device_array, d.B.device_array, chunks, order)
+        assert_close(out_to_f64(c, "bf16"), R, tol_for("bf16", "bf16"), "ag staged epilogue")
+    else:
+        w = si.Workload(103, "rs", "rs", M=M, N=N, K=K, dtype="bf16", out_dtype="bf16", dist="normal", world=W,
+                        rank=r, shard_rows=S, chunks_per_shard=Q, order="rs_ring")
+        d = si.draw(w)
+        chunks, order = oracle.uniform_schedule(W, r, S, Q, "rs_ring")
+        s = csg.Schedule.uniform(W, r, S, Q, "rs_ring")
+        plan = csg.Plan("rs", M, N, K, "bf16", "bf16", s, cfg=cfg)
+        out = empty_out(M, N, "bf16")
+        out.zero_()
+        torch.cuda.synchronize()
+        plan.gemm_rs(to_dev(d.A.device_array), to_dev(d.B.device_array), c, out, "overlap", st.compute, st.copy)
+        plan.check()
+        torch.cuda.synchronize()
+        R, _, _ = oracle.gemm_rs(d.A.device_array, d.B.device_array, chunks, order)
+        G = out_to_f64(c, "bf16")
+        assert_close(G, R, tol_for("bf16", "bf16"), "rs staged epilogue")
+        O = out_to_f64(out, "bf16")
+        for ch in chunks:
+            if not ch.is_local:
+                assert np.array_equal(O[ch.row_begin:ch.row_end], G[ch.row_begin:ch.row_end])
+    assert (plan.info.bm, plan.info.bn) == (bm, 256)
+    assert bool((flat[M * N:] == 0x7fc1).all()), "a store landed past the end of C"
+    plan.close()
+    s.close()
