@@ -50,9 +50,9 @@ CAL_BYTES = 256 << 20    # bytes read (and written) by the calibration copy
 # collective; the kernel's own copies move chunks inside HBM faster than links would):
 # plan configuration fields. --default-plan measures the library's defaults instead.
 TUNED_PLAN_CFG = {
-    3: {"tail_split": 2, "tail_chunks": 4, "tile_dispatch": 2},
+    3: {"intra_order": 1, "group_m": 4, "tile_dispatch": 2},
     4: {"bm": 128, "bn": 256, "bk": 64, "tile_dispatch": 2, "tail_split": 2, "tail_chunks": 8},
-    5: {"tail_split": 2, "tail_chunks": 8},
+    5: {"intra_order": 1, "group_m": 4, "tail_split": 2, "tail_chunks": 8},
 }
 FLUSH_BYTES = 512 << 20  # written before each isolated call: more than the last-level cache and every L2
 
@@ -366,6 +366,10 @@ def main():
         rec["kernel_copy_backend"] = kernel_copy_sweep(w, sched, group_rows, d, timed_loop, moved_bytes, args)
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(w, d, chunks, args.cpu_seconds)
+        if w.op != "attn":
+            rec["cpu_baseline"]["torch_cpu_fp32"] = torch_cpu_reference(w, d, rec["cpu_baseline"])
+    if w.op in ("ag", "rs", "ar"):
+        rec["hipblaslt_reference"] = hipblaslt_reference(w, a_full, b, compute)
     print(json.dumps(rec), flush=True)
 
 
@@ -560,6 +564,46 @@ def cpu_model() -> str:
     except OSError:
         pass
     return "unknown"
+
+
+def hipblaslt_reference(w, a, b, stream, reps=20):
+    """Context, not part of any figure above: the same product as one library GEMM
+    (torch.matmul, which runs hipBLASLt), A (M x K) times B^T with B^T made contiguous,
+    bf16 in and out, timed warm on the device (median of `reps` launches)."""
+    import torch
+    bt = b.view(torch.bfloat16).t().contiguous()
+    x = a.view(torch.bfloat16)
+    with torch.cuda.stream(stream):
+        for _ in range(3):
+            y = torch.matmul(x, bt)
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            y = torch.matmul(x, bt)
+            e1.record(stream)
+            ts.append((e0, e1))
+    torch.cuda.synchronize()
+    ms = float(np.median([e0.elapsed_time(e1) for e0, e1 in ts]))
+    del y, bt
+    return {"ms": round(ms, 4), "tflops": round(w.flops / (ms * 1e-3) / 1e12, 2),
+            "what": "torch.matmul (hipBLASLt), one GEMM of the whole M x N x K, warm, no communication"}
+
+
+def torch_cpu_reference(w, d, base):
+    """Context beside the oracle: torch's fp32 CPU matmul (its BLAS) over as many
+    output rows as the oracle's sample, all columns, on the same cores."""
+    import torch
+    rows = int(base["sample"].split(" of ")[0])
+    A = torch.from_numpy(np.ascontiguousarray(d.A.values[:rows], dtype=np.float32))
+    B = d.B.values if w.op != "grouped" else d.B.values[0]
+    Bt = torch.from_numpy(np.ascontiguousarray(np.asarray(B, dtype=np.float32).T))
+    torch.matmul(A[:64], Bt)
+    t0 = time.perf_counter()
+    torch.matmul(A, Bt)
+    t = time.perf_counter() - t0
+    return {"value": round(2.0 * rows * w.N * w.K / t / 1e12, 4), "unit": "TFLOP/s", "threads": torch.get_num_threads(),
+            "seconds": round(t, 3), "what": "torch.matmul fp32 on the CPU, as many output rows as the oracle's sample"}
 
 
 def cpu_baseline(w, d, chunks, target_s):
