@@ -15,8 +15,10 @@
 // Main loops (each wave owns a sub-tile of 32 x 32 MFMA blocks):
 //   bf16: 512 threads = 2 (M) x 4 (N) waves, two per SIMD, so one wave's MFMAs issue
 //         while the other waits on LDS or issues its loads; v_mfma_f32_32x32x16_bf16;
-//         tiles stream HBM -> LDS with buffer_load ... lds (no register staging),
-//         double-buffered; LDS rows are 128 bytes with an XOR swizzle of their 16-byte
+//         tiles stream HBM -> LDS with buffer_load ... lds (no register staging)
+//         through a ring of K stages: two for 256 x 256 tiles, three for the smaller
+//         tiles, whose stages take fewer MFMAs to consume than a load takes to land;
+//         LDS rows are 128 bytes with an XOR swizzle of their 16-byte
 //         vectors that keeps both the DMA writes and the ds_read_b128 fragment reads
 //         free of bank conflicts.
 //   fp32: 256 threads = 2 x 2 waves; v_mfma_f32_32x32x2_f32 with register-staged,
@@ -193,6 +195,17 @@ __device__ __forceinline__ void dma16(const __amdgpu_buffer_rsrc_t& rs, uint32_t
 // stores acknowledged).
 __device__ __forceinline__ void wait_dma_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// Waits until at most N of this wave's vector-memory operations are outstanding. The
+// main loop issues nothing but its LDS DMA loads between such waits, and loads complete
+// in issue order, so this lets the newest N loads (the stage issued last) stay in
+// flight while every older one has landed. The immediate keeps expcnt and lgkmcnt at
+// their maxima (gfx9 encoding: vmcnt bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8).
+template <int N>
+__device__ __forceinline__ void wait_dma_keep() {
+  static_assert(N >= 0 && N < 64, "vmcnt holds 6 bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
 // Pulls part `part` of `parts` of [0, bytes) of a buffer into the caches: one 4-byte
 // load per 128-byte line, written to this wave's 256-byte scratch area of LDS (so no
 // register waits for it; the next wait for the wave's loads covers it). Rows that a
@@ -218,7 +231,7 @@ __device__ __forceinline__ void warm_lines(const __amdgpu_buffer_rsrc_t& rs, int
   }
 }
 
-template <int BM_, int BN_, int WAVES_M_ = 2, int WAVES_N_ = 4>
+template <int BM_, int BN_, int WAVES_M_ = 2, int WAVES_N_ = 4, int STAGES_ = 2>
 struct Bf16Loop {
   static constexpr int BM = BM_, BN = BN_, BK = 64, IN_BYTES = 2;
   // 8 waves, two per SIMD: while one wave of a SIMD waits on LDS or issues its DMA,
@@ -229,9 +242,16 @@ struct Bf16Loop {
   static constexpr int ROWB = 128;                           // bytes per LDS row (64 bf16)
   static constexpr int STAGE_A = BM * ROWB, STAGE_B = BN * ROWB;
   static constexpr int STAGE = STAGE_A + STAGE_B;
-  static constexpr int LDS_BYTES = 2 * STAGE;
+  // A ring of STAGES stages: STAGES - 1 of them in flight while one is computed on
+  static constexpr int STAGES = STAGES_;
+  static constexpr int LDS_BYTES = STAGES * STAGE;
   static constexpr int A_GROUPS = BM / 8, B_GROUPS = BN / 8;  // a stage is loaded in groups of 8 rows
+  // DMA loads each wave issues per stage, when every wave issues the same number
+  static constexpr bool EVEN_ISSUE = A_GROUPS % (2 * WAVES_M_ * WAVES_N_) == 0 && B_GROUPS % (2 * WAVES_M_ * WAVES_N_) == 0;
+  static constexpr int DMA_PER_STAGE = (A_GROUPS + B_GROUPS) / (WAVES_M_ * WAVES_N_);
   static_assert(WAVES == 8 && BM % 8 == 0 && BN % 8 == 0 && WTM % 32 == 0 && WTN % 32 == 0, "bf16 tile shape");
+  static_assert(STAGES == 2 || ((STAGES == 3 || STAGES == 4) && EVEN_ISSUE && (STAGES - 2) * DMA_PER_STAGE < 64),
+                "a deeper ring counts each wave's loads per stage");
 
   // LDS swizzle: logical 16-byte vector v of tile row r sits at physical vector
   // v ^ swz(r), swz(r) = (r & 7) ^ ((r >> 3) & 1). Any 8 consecutive aligned rows,
@@ -311,15 +331,24 @@ struct Bf16Loop {
     };
 
     issue(lds_base, 0, 0, rsA, rsB, K, wave, lane);
+    // Nothing older than the ring's loads stays outstanding (stores of the previous
+    // tile included), so the partial waits below count ring loads only.
     wait_dma_all();
+#pragma unroll
+    for (int s = 1; s < STAGES - 1; ++s)
+      if (s < nk) issue(lds_base, s, s * BK * 2, rsA, rsB, K, wave, lane);
     __syncthreads();
     load_frags(0, 0, 0);
     constexpr int kSteps = BK / 16;
     constexpr int kPairs = MI * NI < MI + NI ? MI * NI : MI + NI;
+    int buf = 0;  // the ring slot of stage t
     for (int t = 0; t < nk; ++t) {
-      const int buf = t & 1;
       const bool more = t + 1 < nk;
-      if (more) issue(lds_base, buf ^ 1, (t + 1) * BK * 2, rsA, rsB, K, wave, lane);
+      const int next = buf + 1 == STAGES ? 0 : buf + 1;  // slot of stage t + 1
+      // Stage t + STAGES - 1 goes into the slot that stage t - 1 used; every wave's
+      // reads of it completed before the barrier that ended stage t - 1.
+      const bool ahead = t + STAGES - 1 < nk;
+      if (ahead) issue(lds_base, buf == 0 ? STAGES - 1 : buf - 1, (t + STAGES - 1) * BK * 2, rsA, rsB, K, wave, lane);
 #pragma unroll
       for (int ks = 0; ks < kSteps; ++ks) {
         const int cur = ks & 1;
@@ -327,12 +356,19 @@ struct Bf16Loop {
           load_frags(cur ^ 1, buf, ks + 1);  // next sub-step's fragments in flight
         } else {
           // This stage's last fragments are in registers. Wait until the next stage has
-          // landed and every wave is done reading this one, then read the next stage's
-          // first fragments under this sub-step's MFMAs: the matrix core has queued work
-          // on both sides of the barrier instead of draining at it.
-          wait_dma_all();
+          // landed (the stages issued after it may still be in flight) and every wave is
+          // done reading this one, then read the next stage's first fragments under this
+          // sub-step's MFMAs: the matrix core has queued work on both sides of the
+          // barrier instead of draining at it.
+          const int later = nk - 2 - t < STAGES - 2 ? nk - 2 - t : STAGES - 2;
+          if (STAGES >= 4 && later >= 2)
+            wait_dma_keep<2 * DMA_PER_STAGE>();
+          else if (STAGES >= 3 && later >= 1)
+            wait_dma_keep<DMA_PER_STAGE>();
+          else
+            wait_dma_all();
           __syncthreads();
-          if (more) load_frags(cur ^ 1, buf ^ 1, 0);
+          if (more) load_frags(cur ^ 1, next, 0);
         }
 #pragma unroll
         for (int i = 0; i < MI; ++i)
@@ -350,6 +386,7 @@ struct Bf16Loop {
           if (MI + NI > kPairs) __builtin_amdgcn_sched_group_barrier(0x100, MI + NI - kPairs, 0);
         }
       }
+      buf = next;
     }
   }
 };
@@ -1104,9 +1141,12 @@ __global__ __launch_bounds__(kPrologueThreads) void chunk_prologue(PrologueArgs 
 // Variant table
 // ---------------------------------------------------------------------------------
 using LoopBf16_256 = Bf16Loop<256, 256>;
-using LoopBf16_256x128 = Bf16Loop<256, 128>;
-using LoopBf16_128x256 = Bf16Loop<128, 256>;
-using LoopBf16_128 = Bf16Loop<128, 128>;
+// Tiles smaller than 256 x 256 finish a stage's MFMAs sooner than its DMA lands when
+// only one stage is in flight; a ring of three keeps two in flight (48 KiB stages: three
+// fit the 160 KiB of LDS).
+using LoopBf16_256x128 = Bf16Loop<256, 128, 2, 4, 3>;
+using LoopBf16_128x256 = Bf16Loop<128, 256, 2, 4, 3>;
+using LoopBf16_128 = Bf16Loop<128, 128, 2, 4, 3>;
 using LoopBf16_256x224 = Bf16Loop<256, 224, 8, 1>;
 using LoopF32_64 = F32Loop<64, 64>;
 
