@@ -115,7 +115,10 @@ typedef struct {
  *                   order = (key, band, n, m)
  *   group_m         band height of intra_order 1 (0 = 8)
  *   tile_dispatch   0 or 1 = workgroups take the next entry of the tile list from an
- *                   atomic ticket; 2 = workgroup w takes entries w, w + G, w + 2G, ...
+ *                   atomic ticket; 2 = static: workgroup w takes entries s, s + G, s + 2G,
+ *                   ... with s = (w mod 8) * (G / 8) + w / 8 when G is a multiple of 8
+ *                   (else s = w), so that the workgroups of one die (the dispatcher
+ *                   deals workgroups to the 8 dies round robin) take consecutive entries
  *   num_workgroups  persistent grid size G (0 = one per co-resident slot)
  *   copy_engines    SDMA engines the chunk copies are spread over (0 = every engine the
  *                   device offers for device-to-device copies)

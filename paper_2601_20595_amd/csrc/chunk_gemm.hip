@@ -731,12 +731,18 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
   if (a.n_copy_items > 0 && static_cast<int>(blockIdx.x) < n_copiers)
     copy_chunks<kThreads>(a, tid, static_cast<int>(blockIdx.x), n_copiers);
 
+  // Static dispatch: workgroup w takes entries slot, slot + G, slot + 2G, ... The
+  // dispatcher hands workgroups to the dies round robin (w mod 8), so with
+  // slot = (w mod 8) * (G / 8) + w / 8 the workgroups of one die take consecutive
+  // entries of every round of G: the tiles of one chunk start together on one die and
+  // share its L2 (its A rows, and the B columns of the chunks that follow).
+  const int grid = static_cast<int>(gridDim.x), wg = static_cast<int>(blockIdx.x);
+  const int slot = grid % kXcdLists == 0 ? (wg % kXcdLists) * (grid / kXcdLists) + wg / kXcdLists : wg;
   int iter = 0;
   for (;; ++iter) {
     __syncthreads();  // everyone is done with s_pos / s_state / LDS of the previous tile
     if (tid == 0) {
-      const int pos = a.dynamic_ticket ? next_tile(a, xcd)
-                                       : static_cast<int>(blockIdx.x) + iter * static_cast<int>(gridDim.x);
+      const int pos = a.dynamic_ticket ? next_tile(a, xcd) : slot + iter * grid;
       int state = 0;
       if (pos < a.n_tiles) {
         const uint64_t t_take = a.trace ? wall_clock64() : 0;

@@ -306,6 +306,27 @@ def test_ag_split_k_and_dispatch_parity(case):
     assert torch.equal(c.cpu(), c2.cpu())
 
 
+STATIC_GRIDS = [(8, 1), (12, 1), (40, 2), (24, 3)]  # (num_workgroups, split_k): 12 is no multiple of 8
+
+
+@pytest.mark.parametrize("grid,split", STATIC_GRIDS, ids=lambda v: str(v))
+def test_static_dispatch_die_major_slots_cover_every_unit(grid, split):
+    """Static dispatch with small grids, several rounds each: a grid that is a multiple
+    of 8 deals each round to the dies in consecutive runs of entries, any other grid
+    takes entry w + iG; either way every work unit runs exactly once (the plan checks
+    the kernel's unit count) and the output matches the oracle."""
+    _say("static dispatch grid %d split %d" % (grid, split))
+    W, r, S, Q, kind, N, K = 4, 1, 512, 2, "ring", 776, 640
+    w, d, perm, chunks, order = _small_ag(W, r, S, Q, kind, N, K, "bf16", "bf16")
+    s = csg.Schedule.uniform(W, r, S, Q, kind, perm)
+    plan = csg.Plan("ag", W * S, N, K, "bf16", "bf16", s,
+                    cfg={"timeout_ms": 1000, "split_k": split, "tile_dispatch": 2, "num_workgroups": grid})
+    assert plan.info.num_workgroups == grid
+    R = oracle.ag_gemm(d.A.device_array, d.B.device_array, chunks, order)
+    c, _ = run_ag(plan, chunks, d.A, d.B, "bf16")
+    assert_close(out_to_f64(c, "bf16"), R, tol_for("bf16", "bf16"), "ag static dispatch")
+
+
 # ---------------------------------------------------------------------------------
 # Smaller bf16 tiles (256x128, 128x256, 128x128): the same results, to the same bar
 # ---------------------------------------------------------------------------------
