@@ -50,6 +50,8 @@ CAL_BYTES = 256 << 20    # bytes read (and written) by the calibration copy
 # collective; the kernel's own copies move chunks inside HBM faster than links would):
 # plan configuration fields. --default-plan measures the library's defaults instead.
 TUNED_PLAN_CFG = {
+    2: {"bm": 128, "bn": 256, "bk": 64, "intra_order": 1, "group_m": 4, "tile_dispatch": 2, "tail_split": 2,
+        "tail_chunks": 4},
     3: {"intra_order": 1, "group_m": 4, "tile_dispatch": 2},
     4: {"bm": 128, "bn": 256, "bk": 64, "tile_dispatch": 2, "tail_split": 2, "tail_chunks": 8},
     5: {"intra_order": 1, "group_m": 4, "tail_split": 2, "tail_chunks": 8},

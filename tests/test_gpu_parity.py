@@ -494,7 +494,7 @@ def _full(cfg_id):
     return w, d, chunks, order, s, None
 
 
-@pytest.mark.parametrize("cfg_id,tuned", [(1, False), (2, False), (3, False), (3, True), (4, False),
+@pytest.mark.parametrize("cfg_id,tuned", [(1, False), (2, False), (2, True), (3, False), (3, True), (4, False),
                                           (4, True), (5, False), (5, True)])
 def test_full_size_workload_sampled(cfg_id, tuned):
     """Each workload at full size with the library's default plan and, where bench.py
