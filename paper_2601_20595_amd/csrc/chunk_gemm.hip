@@ -206,6 +206,21 @@ __device__ __forceinline__ void wait_dma_keep() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
+// Waits until at most `later` groups of PER loads each are outstanding (later is
+// workgroup-uniform; more than kMax counts as kMax, less than 1 as none).
+template <int PER, int kMax>
+__device__ __forceinline__ void wait_dma_stages(int later) {
+  if constexpr (kMax >= 1) {
+    if (later >= kMax) {
+      wait_dma_keep<kMax * PER>();
+      return;
+    }
+    wait_dma_stages<PER, kMax - 1>(later);
+  } else {
+    wait_dma_all();
+  }
+}
+
 // Pulls part `part` of `parts` of [0, bytes) of a buffer into the caches: one 4-byte
 // load per 128-byte line, written to this wave's 256-byte scratch area of LDS (so no
 // register waits for it; the next wait for the wave's loads covers it). Rows that a
@@ -360,13 +375,7 @@ struct Bf16Loop {
           // done reading this one, then read the next stage's first fragments under this
           // sub-step's MFMAs: the matrix core has queued work on both sides of the
           // barrier instead of draining at it.
-          const int later = nk - 2 - t < STAGES - 2 ? nk - 2 - t : STAGES - 2;
-          if (STAGES >= 4 && later >= 2)
-            wait_dma_keep<2 * DMA_PER_STAGE>();
-          else if (STAGES >= 3 && later >= 1)
-            wait_dma_keep<DMA_PER_STAGE>();
-          else
-            wait_dma_all();
+          wait_dma_stages<DMA_PER_STAGE, STAGES - 2>(nk - 2 - t);
           __syncthreads();
           if (more) load_frags(cur ^ 1, next, 0);
         }
@@ -883,41 +892,68 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
         __syncthreads();
         skip = __builtin_amdgcn_readfirstlane(s_state) < 0;
         const int64_t prow = td.row_begin - a.own_row0;
-        if constexpr (kOutBf16 && Loop::BM == 256 && Loop::BN == 256 && kThreads == 512) {
-          // Each peer's partial tile (256 rows of 512 bytes) is staged in the main loop's
-          // LDS with row-contiguous 16-byte DMA (two rows per instruction), then read
-          // back in the accumulator layout. The 16-byte pieces of row r are stored at
-          // position (piece ^ (r % 32)), so the 32 rows a read instruction touches fall
-          // in distinct bank groups. Loads past the tile's last row read 0.
-          constexpr int kRowB = 512;
+        if constexpr (kOutBf16 && Loop::BM == 256 && Loop::BN == 256 && kThreads == 512 &&
+                      Loop::WAVES_M == 2 && Loop::MI == 4) {
+          // The peers' partial tiles (256 rows of 512 bytes each) stream through the main
+          // loop's LDS in 64-row quarters: quarter k of every peer goes to ring slot k
+          // (32 KiB), three quarters in flight while one is added. Each wave stages 8
+          // rows of a quarter with row-contiguous 16-byte DMA (two rows per
+          // instruction, four instructions); the 16-byte pieces of row r sit at position
+          // (piece ^ (r % 32)), so the 32 rows a read instruction touches fall in
+          // distinct bank groups. A quarter's rows belong to the four waves of one M
+          // half (wm = k / 2), which read their two row blocks of it (i = 2 (k % 2) and
+          // 2 (k % 2) + 1) back in the accumulator layout and add them. Peers are added
+          // in ascending rank order. Loads past the tile's last row read 0.
+          constexpr int kRowB = 512, kQuarterB = 64 * kRowB, kPerUnit = 4;
           const uint32_t lds_base =
               __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_ptr_t)lds)));
           const int pitch = N32 * 2;
-          const int pr = lane >> 5, pc = lane & 31;
-          for (int j = 0; j < (skip ? 0 : a.n_peers); ++j) {
+          const int units = skip ? 0 : 4 * a.n_peers;
+          auto issue_quarter = [&](int j, int k) {
             const __amdgpu_buffer_rsrc_t rsP =
                 make_rsrc(a.partials + ((static_cast<int64_t>(j) * a.own_rows + prow) * a.N + col0) * kOutBytes,
                           static_cast<int64_t>(g.arows) * a.N * kOutBytes);
-            __syncthreads();  // every wave is done reading LDS (main loop or previous peer)
+            // The lane's offsets derive from the lane through an empty asm, so they are
+            // computed here (a few ALU operations) instead of being hoisted out of the
+            // loops and held, or spilled, across them: a spill reload here would make
+            // the compiler wait for every load in flight, the ring's included.
+            int lw = lane;
+            asm volatile("" : "+v"(lw));
+            const int qr = lw >> 5, qc = lw & 31;
 #pragma unroll
-            for (int q2 = 0; q2 < 16; ++q2) {
-              const int r = wave * 32 + 2 * q2 + pr;
-              const uint32_t l0 = __builtin_amdgcn_readfirstlane(lds_base + (wave * 32 + 2 * q2) * kRowB);
-              dma16(rsP, l0, r * pitch + ((pc ^ (r & 31)) << 4), 0);
+            for (int q2 = 0; q2 < kPerUnit; ++q2) {
+              const int lr = wave * 8 + 2 * q2;  // first of this instruction's two rows in the quarter
+              const int r = 64 * k + lr + qr;    // tile row of this lane
+              const uint32_t l0 = __builtin_amdgcn_readfirstlane(lds_base + k * kQuarterB + lr * kRowB);
+              dma16(rsP, l0, r * pitch + ((qc ^ (r & 31)) << 4), 0);
             }
-            wait_dma_all();
-            __syncthreads();
+          };
+          wait_dma_all();   // only the ring's loads are outstanding from here on
+          __syncthreads();  // every wave is done reading the main loop's LDS
+          for (int u = 0; u < 3 && u < units; ++u) issue_quarter(u >> 2, u & 3);
+          for (int j = 0; j < (units >> 2); ++j) {
 #pragma unroll
-            for (int r = 0; r < kRuns; ++r) {
-              const int i = r / (NI * 4), jj = (r / 4) % NI, q = r % 4;
-              const int row = vrow + 32 * i;
-              const int colb = (vcol + 32 * jj + 8 * q) * 2;
-              const u32x2 raw =
-                  *reinterpret_cast<const u32x2*>(lds + row * kRowB + (((colb >> 4) ^ (row & 31)) << 4) + (colb & 15));
-              acc[i][jj][4 * q + 0] += __builtin_bit_cast(float, raw.x << 16);
-              acc[i][jj][4 * q + 1] += __builtin_bit_cast(float, raw.x & 0xffff0000u);
-              acc[i][jj][4 * q + 2] += __builtin_bit_cast(float, raw.y << 16);
-              acc[i][jj][4 * q + 3] += __builtin_bit_cast(float, raw.y & 0xffff0000u);
+            for (int k = 0; k < 4; ++k) {
+              const int u = 4 * j + k;
+              // quarter u has landed; up to two later ones may still be in flight
+              wait_dma_stages<kPerUnit, 2>(units - 1 - u);
+              __syncthreads();  // every wave's share of quarter u is in, quarter u - 1 is read
+              if (u + 3 < units) issue_quarter(j + (k + 3) / 4, (k + 3) & 3);
+              if (wm == k / 2) {
+#pragma unroll
+                for (int r = 0; r < kRuns; ++r) {
+                  const int i = r / (NI * 4), jj = (r / 4) % NI, q = r % 4;
+                  if (i / 2 != k % 2) continue;
+                  const int row = vrow + 32 * i - 64 * k;  // row inside the quarter
+                  const int colb = (vcol + 32 * jj + 8 * q) * 2;
+                  const u32x2 raw = *reinterpret_cast<const u32x2*>(lds + k * kQuarterB + row * kRowB +
+                                                                    (((colb >> 4) ^ (row & 31)) << 4) + (colb & 15));
+                  acc[i][jj][4 * q + 0] += __builtin_bit_cast(float, raw.x << 16);
+                  acc[i][jj][4 * q + 1] += __builtin_bit_cast(float, raw.x & 0xffff0000u);
+                  acc[i][jj][4 * q + 2] += __builtin_bit_cast(float, raw.y << 16);
+                  acc[i][jj][4 * q + 3] += __builtin_bit_cast(float, raw.y & 0xffff0000u);
+                }
+              }
             }
           }
         } else {
