@@ -360,6 +360,29 @@ def test_ag_tile_shape_parity(case, mode):
     assert torch.equal(c.cpu(), c2.cpu())
 
 
+RING_DEPTH = [(bm, bn, K, split) for bm, bn in ((128, 256), (256, 128), (128, 128))
+              for K, split in ((64, 1), (128, 1), (192, 1), (256, 1), (192, 2), (320, 3))]
+
+
+@pytest.mark.parametrize("bm,bn,K,split", RING_DEPTH, ids=lambda v: str(v))
+def test_three_stage_ring_short_k_bit_exact(bm, bn, K, split):
+    """The tiles with a three-stage DMA ring at K steps of 1 to 5 stages per unit (fewer
+    stages than the ring holds, exactly as many, a few more), whole and split along K:
+    integer inputs give exact sums, so the bf16 output must equal the RNE of the oracle's
+    exact value in every element, and repeated calls the same bits."""
+    W, r, S, Q, kind, N = 4, 2, 160, 2, "ring", 520
+    _say("three-stage ring %dx%d K=%d split=%d" % (bm, bn, K, split))
+    w, d, perm, chunks, order = _small_ag(W, r, S, Q, kind, N, K, "bf16", "bf16", dist="int")
+    s = csg.Schedule.uniform(W, r, S, Q, kind, perm)
+    plan = csg.Plan("ag", W * S, N, K, "bf16", "bf16", s,
+                    cfg={"timeout_ms": 1000, "bm": bm, "bn": bn, "bk": 64, "split_k": split})
+    assert (plan.info.bm, plan.info.bn) == (bm, bn)
+    R = oracle.ag_gemm(d.A.device_array, d.B.device_array, chunks, order)     # exact integers
+    for mode in ("overlap", "compute_only"):
+        c, _ = run_ag(plan, chunks, d.A, d.B, "bf16", mode=mode, repeats=2)
+        assert np.array_equal(out_to_f64(c, "bf16"), bf16_rne_of_f64(R)), mode
+
+
 def test_ag_256x224_fp32_output_integer_inputs_bit_exact():
     W, r, S, Q, kind, N, K = 4, 1, 256, 2, "ring", 448, 640
     _say("ag 256x224 fp32 out, integer inputs")
