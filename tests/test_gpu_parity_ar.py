@@ -93,6 +93,7 @@ AR_CASES = [
     (8, 5, 256, 1, 256, 128, "bf16", "bf16"),      # 8 ranks, one chunk per shard
     (3, 0, 128, 2, 200, 96, "f32", "f32"),         # ragged N, fp32 (64-row tiles)
     (2, 1, 512, 4, 520, 192, "bf16", "f32"),       # ragged N, own shard last rows, fp32 out
+    (4, 2, 512, 2, 520, 192, "bf16", "bf16"),      # ragged N, bf16 out: two own row tiles, 3 peers
 ]
 AR_IDS = ["W%d-r%d-S%d-Q%d-N%d-K%d-%s-%s" % c for c in AR_CASES]
 
