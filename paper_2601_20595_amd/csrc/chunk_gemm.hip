@@ -195,10 +195,11 @@ __device__ __forceinline__ void dma16(const __amdgpu_buffer_rsrc_t& rs, uint32_t
 // stores acknowledged).
 __device__ __forceinline__ void wait_dma_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
-// Waits until at most N of this wave's vector-memory operations are outstanding. The
-// main loop issues nothing but its LDS DMA loads between such waits, and loads complete
-// in issue order, so this lets the newest N loads (the stage issued last) stay in
-// flight while every older one has landed. The immediate keeps expcnt and lgkmcnt at
+// Waits until at most N of this wave's vector-memory operations are outstanding. Its
+// callers (the main loop's ring, the all-reduce's partial-tile ring) issue nothing but
+// LDS DMA loads between such waits, and loads complete in issue order, so this lets the
+// newest N loads (the stages issued last) stay in flight while every older one has
+// landed; an access of the compiler's own in between (a spill) only makes it wait longer. The immediate keeps expcnt and lgkmcnt at
 // their maxima (gfx9 encoding: vmcnt bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8).
 template <int N>
 __device__ __forceinline__ void wait_dma_keep() {
