@@ -10,7 +10,8 @@ exposes, for one operator at one shape:
   - chunks per shard (the chunk split factor; only for uniform schedules): every
     split gives the bit-identical product, as each output row depends on one chunk
     and each tile's K order is fixed;
-  - tile dispatch (per-die tickets or a static stride);
+  - tile dispatch (per-die tickets, or a static deal that gives each die consecutive
+    entries of every round);
   - the intra-chunk tile order (raster, or bands of group_m row tiles visited
     column by column; Section 5.2, intra-chunk swizzle; Section 5.3, intra-tile
     orders);

@@ -41,7 +41,7 @@ ORDER_CASES = [
     # W, r, S, Q, kind, N, K, group_m, extra cfg
     (4, 1, 1024, 1, "ring", 1280, 512, 2, {}),                       # 4 row tiles per chunk
     (4, 2, 768, 2, "permutation", 1000, 384, 3, {}),                 # ragged N, 384-row chunks straddling tiles
-    (2, 0, 1024, 2, "ring", 768, 256, 8, {"tile_dispatch": 2}),      # static stride
+    (2, 0, 1024, 2, "ring", 768, 256, 8, {"tile_dispatch": 2}),      # static, die-major
     (4, 0, 1024, 1, "ring", 512, 512, 2, {"bm": 128, "bn": 128}),    # smaller tiles
 ]
 
