@@ -14,7 +14,10 @@
 //
 // Main loops (each wave owns a sub-tile of 32 x 32 MFMA blocks):
 //   bf16: 512 threads = 2 (M) x 4 (N) waves, two per SIMD, so one wave's MFMAs issue
-//         while the other waits on LDS or issues its loads; v_mfma_f32_32x32x16_bf16;
+//         while the other waits on LDS or issues its loads; v_mfma_f32_32x32x16_bf16
+//         for 256-row and 256-column tiles, v_mfma_f32_16x16x32_bf16 for the smaller
+//         ones (the chip holds a higher clock with it, and the smaller tiles have the
+//         registers for its twice as many fragments);
 //         tiles stream HBM -> LDS with buffer_load ... lds (no register staging)
 //         through a ring of K stages: two for 256 x 256 tiles, three for the smaller
 //         tiles, whose stages take fewer MFMAs to consume than a load takes to land;
@@ -23,9 +26,10 @@
 //         free of bank conflicts.
 //   fp32: 256 threads = 2 x 2 waves; v_mfma_f32_32x32x2_f32 with register-staged,
 //         padded LDS tiles.
-// The MFMA takes the B fragment as its first operand, so each lane ends up with
-// four runs of four consecutive output columns of one output row, which the
-// epilogue writes as 8-byte (bf16) or 16-byte (fp32) stores.
+// The MFMA takes the B fragment as its first operand, so each lane ends up with runs
+// of four consecutive output columns of one output row (the loop's lane_row,
+// lane_col, run_row and run_col say where), which the epilogue writes as 8-byte
+// (bf16) or 16-byte (fp32) stores.
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
@@ -247,9 +251,13 @@ __device__ __forceinline__ void warm_lines(const __amdgpu_buffer_rsrc_t& rs, int
   }
 }
 
-template <int BM_, int BN_, int WAVES_M_ = 2, int WAVES_N_ = 4, int STAGES_ = 2>
+template <int BM_, int BN_, int WAVES_M_ = 2, int WAVES_N_ = 4, int STAGES_ = 2, int MF_ = 32>
 struct Bf16Loop {
   static constexpr int BM = BM_, BN = BN_, BK = 64, IN_BYTES = 2;
+  // MFMA shape: 32 = v_mfma_f32_32x32x16_bf16, 16 = v_mfma_f32_16x16x32_bf16 (the same
+  // MACs per cycle; under sustained load the chip holds a higher clock with it)
+  static constexpr int MF = MF_;
+  static_assert(MF == 32 || MF == 16, "MFMA shape");
   // 8 waves, two per SIMD: while one wave of a SIMD waits on LDS or issues its DMA,
   // the other keeps the matrix core busy. Waves are laid out WAVES_M (M) x WAVES_N (N):
   // 2 x 4 by default; 8 x 1 for tiles whose N side (224 = 7 x 32) splits no further.
@@ -275,6 +283,19 @@ struct Bf16Loop {
   // swizzles, so a ds_read_b128 of one logical vector by 16 lanes on 16 consecutive
   // rows touches 16 distinct 4-bank groups whether LDS is 32 or 64 banks wide.
   __device__ static int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
+  // Output layout. The accumulators of a 32 x 32 block (i, j) of the wave's sub-tile
+  // hold four runs q of four consecutive fp32 columns each, at row lane_row(lane) +
+  // run_row(i, q) and column lane_col(lane) + run_col(j, q) of the sub-tile. The MFMA
+  // takes the B fragment as its first operand, which makes each lane's results runs
+  // of columns of one row:
+  //   32 x 32 x 16: row lane % 32, columns 4 (lane / 32) + 8 q + 0..3;
+  //   16 x 16 x 32: the block is four 16 x 16 blocks, run q = 2 bi + bj; row
+  //                 16 bi + lane % 16, columns 16 bj + 4 (lane / 16) + 0..3.
+  __device__ static int lane_row(int lane) { return MF == 32 ? (lane & 31) : (lane & 15); }
+  __device__ static int lane_col(int lane) { return MF == 32 ? 4 * (lane >> 5) : 4 * (lane >> 4); }
+  static constexpr int run_row(int i, int q) { return MF == 32 ? 32 * i : 32 * i + 16 * (q >> 1); }
+  static constexpr int run_col(int j, int q) { return MF == 32 ? 32 * j + 8 * q : 32 * j + 16 * (q & 1); }
 
   // One operand's share of a stage, kGroups groups of 8 rows starting at LDS byte
   // address rows0. When the groups divide evenly, wave w takes a contiguous run of
@@ -327,23 +348,28 @@ struct Bf16Loop {
     const int nk = g.nk;
     const uint32_t lds_base =
         __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_ptr_t)lds)));
-    const int lrow = lane & 31, lhalf = lane >> 5;
-    // byte offset of this lane's fragment row inside a stage; every fragment block
-    // starts on a multiple of 32 rows, so the row's swizzle is swz(lane % 32)
+    // A fragment is MF rows of 8 consecutive k values per lane: row lane % MF of the
+    // block, 16-byte vector (64 / MF) ks + lane / MF of the row at k sub-step ks (k16
+    // sub-steps with 32-row blocks, k32 with 16-row blocks). Every block starts on a
+    // multiple of 16 rows, so the row's swizzle is swz(lane % 16) (= swz(lane % 32) on
+    // 32-row blocks, whose rows 16..31 repeat the pattern of rows 0..15 ^ 1).
+    constexpr int FI = WTM / MF, FJ = WTN / MF;  // fragments per operand and sub-step
+    constexpr int VPS = 64 / MF;                 // 16-byte vectors per k sub-step
+    const int lrow = lane % MF, lk = lane / MF;
     const int a_off = (wm * WTM + lrow) * ROWB;
     const int b_off = STAGE_A + (wn * WTN + lrow) * ROWB;
     const int sw = swz(lrow);
 
-    bf16x8 fa[2][MI], fb[2][NI];  // fragments of two consecutive k sub-steps
+    bf16x8 fa[2][FI], fb[2][FJ];  // fragments of two consecutive k sub-steps
     auto load_frags = [&](int set, int buf, int ks) {
       const unsigned char* st = lds + buf * STAGE;
-      const int vec = ((ks * 2 + lhalf) ^ sw) * 16;
+      const int vec = ((ks * VPS + lk) ^ sw) * 16;
 #pragma unroll
-      for (int i = 0; i < MI; ++i)
-        fa[set][i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(st + a_off + i * 32 * ROWB + vec));
+      for (int i = 0; i < FI; ++i)
+        fa[set][i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(st + a_off + i * MF * ROWB + vec));
 #pragma unroll
-      for (int j = 0; j < NI; ++j)
-        fb[set][j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(st + b_off + j * 32 * ROWB + vec));
+      for (int j = 0; j < FJ; ++j)
+        fb[set][j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u16x8*>(st + b_off + j * MF * ROWB + vec));
     };
 
     issue(lds_base, 0, 0, rsA, rsB, K, wave, lane);
@@ -355,8 +381,9 @@ struct Bf16Loop {
       if (s < nk) issue(lds_base, s, s * BK * 2, rsA, rsB, K, wave, lane);
     __syncthreads();
     load_frags(0, 0, 0);
-    constexpr int kSteps = BK / 16;
-    constexpr int kPairs = MI * NI < MI + NI ? MI * NI : MI + NI;
+    constexpr int kSteps = BK / (512 / MF);  // k sub-steps per stage: 16 (32 x 32) or 32 (16 x 16) each
+    constexpr int kMfma = FI * FJ, kReads = FI + FJ;  // per sub-step
+    constexpr int kPairs = kMfma < kReads ? kMfma : kReads;
     int buf = 0;  // the ring slot of stage t
     for (int t = 0; t < nk; ++t) {
       const bool more = t + 1 < nk;
@@ -380,11 +407,29 @@ struct Bf16Loop {
           __syncthreads();
           if (more) load_frags(cur ^ 1, next, 0);
         }
+        if constexpr (MF == 32) {
 #pragma unroll
-        for (int i = 0; i < MI; ++i)
+          for (int i = 0; i < MI; ++i)
 #pragma unroll
-          for (int j = 0; j < NI; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[cur][j], fa[cur][i], acc[i][j], 0, 0, 0);
+            for (int j = 0; j < NI; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[cur][j], fa[cur][i], acc[i][j], 0, 0, 0);
+        } else {
+          // 16 x 16 block (bi, bj) accumulates into run 2 (bi % 2) + bj % 2 of 32 x 32
+          // block (bi / 2, bj / 2)
+#pragma unroll
+          for (int bi = 0; bi < FI; ++bi)
+#pragma unroll
+            for (int bj = 0; bj < FJ; ++bj) {
+              f32x16& blk = acc[bi >> 1][bj >> 1];
+              const int e = 4 * (2 * (bi & 1) + (bj & 1));
+              f32x4 c = f32x4{blk[e + 0], blk[e + 1], blk[e + 2], blk[e + 3]};
+              c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[cur][bj], fa[cur][bi], c, 0, 0, 0);
+              blk[e + 0] = c[0];
+              blk[e + 1] = c[1];
+              blk[e + 2] = c[2];
+              blk[e + 3] = c[3];
+            }
+        }
         if (ks + 1 < kSteps || more) {
           // interleave the fragment reads in flight with this sub-step's MFMAs
 #pragma unroll
@@ -392,8 +437,8 @@ struct Bf16Loop {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
           }
-          if (MI * NI > kPairs) __builtin_amdgcn_sched_group_barrier(0x008, MI * NI - kPairs, 0);
-          if (MI + NI > kPairs) __builtin_amdgcn_sched_group_barrier(0x100, MI + NI - kPairs, 0);
+          if (kMfma > kPairs) __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kPairs, 0);
+          if (kReads > kPairs) __builtin_amdgcn_sched_group_barrier(0x100, kReads - kPairs, 0);
         }
       }
       buf = next;
@@ -406,6 +451,13 @@ struct Bf16Loop {
 // ---------------------------------------------------------------------------------
 template <int BM_, int BN_>
 struct F32Loop {
+  // output layout: as the bf16 loop's 32 x 32 x 16 one (row lane % 32, runs of four
+  // columns at 4 (lane / 32) + 8 q)
+  static constexpr int MF = 32;
+  __device__ static int lane_row(int lane) { return lane & 31; }
+  __device__ static int lane_col(int lane) { return 4 * (lane >> 5); }
+  static constexpr int run_row(int i, int) { return 32 * i; }
+  static constexpr int run_col(int j, int q) { return 32 * j + 8 * q; }
   static constexpr int BM = BM_, BN = BN_, BK = 16, IN_BYTES = 4;
   static constexpr int WAVES_M = 2, WAVES_N = 2, THREADS = 256;
   static constexpr int WTM = BM / 2, WTN = BN / 2, MI = WTM / 32, NI = WTN / 32;
@@ -837,7 +889,6 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
     // in L2 until the kernel's end.
     constexpr int kCStorePolicy = kProducer ? (kPolicySc0 | kPolicySc1) : 0;
     const int N32 = static_cast<int>(a.N);
-    const int lrow = lane & 31, lhalf = lane >> 5;
     // C is written through a buffer resource over the tile's rows; a run outside the
     // valid tile gets a lane offset past the resource's end, and the hardware drops
     // it (the plan keeps BM * N * out_bytes below that offset). No branch, so the
@@ -846,17 +897,17 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
         make_rsrc(static_cast<unsigned char*>(a.C) + (static_cast<int64_t>(td.row_begin) * a.N + col0) * kOutBytes,
                   static_cast<int64_t>(g.arows) * a.N * kOutBytes);
     // the offset of run (i, j, q) is split into a per-lane part (one register), a
-    // per-row-block scalar part (i) and a constant that fits the instruction's
-    // immediate field (j, q), so no per-run offsets stay live across tiles
-    const int vrow = wm * Loop::WTM + lrow;         // row of block i: vrow + 32 i
-    const int vcol = wn * Loop::WTN + 4 * lhalf;    // column of run (j, q): vcol + 32 j + 8 q
+    // per-row scalar part (i, q) and a constant that fits the instruction's immediate
+    // field (j, q), so no per-run offsets stay live across tiles
+    const int vrow = wm * Loop::WTM + Loop::lane_row(lane);  // row of run (i, q): vrow + run_row(i, q)
+    const int vcol = wn * Loop::WTN + Loop::lane_col(lane);  // column of run (j, q): vcol + run_col(j, q)
     const int voff_c = (vrow * N32 + vcol) * kOutBytes;
     auto store_run = [&](int r, const f32x4& f) {
       const int i = r / (NI * 4), j = (r / 4) % NI, q = r % 4;
       // N is a multiple of 4: a run is all in or all out
-      const bool ok = (vrow + 32 * i < g.arows) && (vcol + 32 * j + 8 * q < g.brows);
-      const int voff = (ok ? voff_c : kDropOffset) + (32 * j + 8 * q) * kOutBytes;
-      const int soff = __builtin_amdgcn_readfirstlane(32 * i * N32 * kOutBytes);
+      const bool ok = (vrow + Loop::run_row(i, q) < g.arows) && (vcol + Loop::run_col(j, q) < g.brows);
+      const int voff = (ok ? voff_c : kDropOffset) + Loop::run_col(j, q) * kOutBytes;
+      const int soff = __builtin_amdgcn_readfirstlane(Loop::run_row(i, q) * N32 * kOutBytes);
       if constexpr (kOutBf16)  // v_cvt_pk_bf16_f32: round to nearest even (the default rounding mode)
         __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, __builtin_convertvector(f, bf16x4)), rsC, voff,
                                               soff, kCStorePolicy);
@@ -894,7 +945,7 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
         skip = __builtin_amdgcn_readfirstlane(s_state) < 0;
         const int64_t prow = td.row_begin - a.own_row0;
         if constexpr (kOutBf16 && Loop::BM == 256 && Loop::BN == 256 && kThreads == 512 &&
-                      Loop::WAVES_M == 2 && Loop::MI == 4) {
+                      Loop::WAVES_M == 2 && Loop::MI == 4 && Loop::MF == 32) {
           // The peers' partial tiles (256 rows of 512 bytes each) stream through the main
           // loop's LDS in 64-row quarters: quarter k of every peer goes to ring slot k
           // (32 KiB), three quarters in flight while one is added. Each wave stages 8
@@ -965,9 +1016,9 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
 #pragma unroll
           for (int r = 0; r < kRuns; ++r) {
             const int i = r / (NI * 4), jj = (r / 4) % NI, q = r % 4;
-            const bool ok = (vrow + 32 * i < g.arows) && (vcol + 32 * jj + 8 * q < g.brows);
-            const int voff = (ok ? voff_c : kDropOffset) + (32 * jj + 8 * q) * kOutBytes;
-            const int soff = __builtin_amdgcn_readfirstlane(32 * i * N32 * kOutBytes);
+            const bool ok = (vrow + Loop::run_row(i, q) < g.arows) && (vcol + Loop::run_col(jj, q) < g.brows);
+            const int voff = (ok ? voff_c : kDropOffset) + Loop::run_col(jj, q) * kOutBytes;
+            const int soff = __builtin_amdgcn_readfirstlane(Loop::run_row(i, q) * N32 * kOutBytes);
             float f[4];
             if constexpr (kOutBf16) {
               const u32x2 raw = __builtin_amdgcn_raw_buffer_load_b64(rsP, voff, soff, 0);
@@ -1078,15 +1129,17 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
           // and held in registers across the main loop
           int lw = lane;
           asm volatile("" : "+v"(lw));
-          const int l_row = lw & 31, l_half = lw >> 5;
-          const int wbase = (wm * Loop::WTM + l_row) * kRowB + 8 * l_half;
+          const int l_row = wm * Loop::WTM + Loop::lane_row(lw);  // the lane's row of run (0, q = 0)
+          const int l_col2 = (wn * Loop::WTN + Loop::lane_col(lw)) * 2;  // its byte in the row, run (0, 0)
           __syncthreads();  // every wave is done reading LDS
 #pragma unroll
           for (int r = 0; r < kRuns; ++r) {
-            // run (i, j, q): row wm WTM + 32 i + l_row, 16-byte piece wn 8 + 4 j + q (< 32), half l_half
+            // run (i, j, q): 8 bytes at row l_row + run_row(i, q), byte l_col2 + 2 run_col(j, q)
+            // of the row, that is 16-byte piece (byte / 16) at position piece ^ (row % 32)
             const int i = r / (NI * 4), j = (r / 4) % NI, q = r % 4;
-            const int piece = (wn * (Loop::WTN / 8) + 4 * j + q) ^ l_row;
-            *reinterpret_cast<u32x2*>(lds + wbase + i * 32 * kRowB + (piece << 4)) =
+            const int row = l_row + Loop::run_row(i, q);
+            const int colb = l_col2 + 2 * Loop::run_col(j, q);
+            *reinterpret_cast<u32x2*>(lds + row * kRowB + ((((colb >> 4) ^ row) & 31) << 4) + (colb & 15)) =
                 __builtin_bit_cast(u32x2, __builtin_convertvector(acc_run(r), bf16x4));
             __builtin_amdgcn_sched_barrier(0);  // convert-and-write one run at a time
           }
@@ -1186,10 +1239,10 @@ __global__ __launch_bounds__(kPrologueThreads) void chunk_prologue(PrologueArgs 
 using LoopBf16_256 = Bf16Loop<256, 256>;
 // Tiles smaller than 256 x 256 finish a stage's MFMAs sooner than its DMA lands when
 // only one stage is in flight; a ring of three keeps two in flight (48 KiB stages: three
-// fit the 160 KiB of LDS).
-using LoopBf16_256x128 = Bf16Loop<256, 128, 2, 4, 3>;
-using LoopBf16_128x256 = Bf16Loop<128, 256, 2, 4, 3>;
-using LoopBf16_128 = Bf16Loop<128, 128, 2, 4, 3>;
+// fit the 160 KiB of LDS). Their loops issue 16 x 16 x 32 MFMAs.
+using LoopBf16_256x128 = Bf16Loop<256, 128, 2, 4, 3, 16>;
+using LoopBf16_128x256 = Bf16Loop<128, 256, 2, 4, 3, 16>;
+using LoopBf16_128 = Bf16Loop<128, 128, 2, 4, 3, 16>;
 using LoopBf16_256x224 = Bf16Loop<256, 224, 8, 1>;
 using LoopF32_64 = F32Loop<64, 64>;
 
