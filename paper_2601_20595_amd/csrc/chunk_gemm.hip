@@ -1290,6 +1290,9 @@ const Variant kVariants[] = {
     // sooner after it lands)
     CSG_VARIANT(InType::BF16, LoopBf16_256x128, true, false, false),
     CSG_VARIANT(InType::BF16, LoopBf16_128x256, true, false, false),
+    // ... and for GEMM + reduce-scatter: twice the tiles, so the emitted chunks
+    // complete over more waves and fewer are left to copy after the last one
+    CSG_VARIANT(InType::BF16, LoopBf16_128x256, true, true, false),
     CSG_VARIANT(InType::BF16, LoopBf16_128, true, false, false),
     // 256 x 224 tiles: N = 7 x 256 and 14 x 256 shapes fill every CU in whole waves
     CSG_VARIANT(InType::BF16, LoopBf16_256x224, true, false, false),

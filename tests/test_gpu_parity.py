@@ -241,6 +241,50 @@ def test_rs_small_parity(case, mode):
             assert np.array_equal(O[rows], G[rows])      # copy-out of the finished C rows (C was NaN before)
 
 
+RS_TILE = [
+    # W, r, S, Q, N, K, split, backend
+    (4, 1, 256, 4, 520, 320, 1, "sdma"),    # 64-row chunks: each 128-row tile writes 2; ragged N
+    (4, 2, 512, 2, 512, 256, 1, "sdma"),    # 256-row chunks: 2 row tiles each
+    (4, 0, 384, 3, 776, 192, 2, "sdma"),    # split-K
+    (8, 5, 256, 2, 256, 128, 1, "kernel"),  # sends from the epilogue
+]
+
+
+@pytest.mark.parametrize("case", RS_TILE, ids=lambda c: "W%d-r%d-S%d-Q%d-N%d-K%d-split%d-%s" % c)
+@pytest.mark.parametrize("mode", ["overlap", "compute_only"])
+def test_rs_128x256_tiles_parity(case, mode):
+    """GEMM + reduce-scatter with 128 x 256 tiles (three-stage ring, 16 x 16 x 32 MFMAs):
+    C matches the oracle, every sent chunk's outgoing rows equal C's, and integer inputs
+    give the bf16 RNE of the exact sum in every element."""
+    W, r, S, Q, N, K, split, backend = case
+    _say("rs 128x256 %s mode=%s" % (case, mode))
+    for dist in ("normal", "int"):
+        w = si.Workload(104, "rs128", "rs", M=W * S, N=N, K=K, dtype="bf16", out_dtype="bf16", dist=dist, world=W,
+                        rank=r, shard_rows=S, chunks_per_shard=Q, order="rs_ring")
+        d = si.draw(w)
+        chunks, order = oracle.uniform_schedule(W, r, S, Q, "rs_ring")
+        s = csg.Schedule.uniform(W, r, S, Q, "rs_ring")
+        cfg = {"timeout_ms": 1000, "bm": 128, "bn": 256, "bk": 64, "split_k": split}
+        if backend == "kernel":
+            cfg["copy_backend"] = "kernel"
+        plan = csg.Plan("rs", W * S, N, K, "bf16", "bf16", s, cfg=cfg)
+        assert (plan.info.bm, plan.info.bn) == (128, 256)
+        c, out = run_rs(plan, d.A, d.B, "bf16", mode=mode)
+        R, _, _ = oracle.gemm_rs(d.A.device_array, d.B.device_array, chunks, order)
+        G = out_to_f64(c, "bf16")
+        if dist == "int":
+            assert np.array_equal(G, bf16_rne_of_f64(R))
+        else:
+            assert_close(G, R, tol_for("bf16", "bf16"), "rs 128x256")
+        O = out_to_f64(out, "bf16")
+        for ch in chunks:
+            rows = slice(ch.row_begin, ch.row_end)
+            if ch.is_local or mode == "compute_only":
+                assert (O[rows] == 0).all()
+            else:
+                assert np.array_equal(O[rows], G[rows])
+
+
 def test_grouped_small_parity_with_empty_segments_and_partial_tiles():
     _say("grouped small")
     W, E, N, K = 4, 3, 264, 256
