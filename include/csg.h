@@ -108,6 +108,10 @@ typedef struct {
 
 /* Tile and runtime knobs. Zero means "default" for every field.
  *   bm, bn, bk      tile shape; must name a compiled kernel variant on a device plan
+ *                   (bk = 64 for bf16, 16 for fp32): bf16 inputs 256 x 256 (every operation;
+ *                   the default), 256 x 224 (all-gather and grouped GEMMs), 128 x 256
+ *                   (those and GEMM + reduce-scatter, bf16 output), 256 x 128 and 128 x 128
+ *                   (all-gather and grouped GEMMs, bf16 output); fp32 inputs 64 x 64
  *   intra_order     tile order inside a chunk (Section 5.2, intra-chunk swizzle), the
  *                   chunk order staying as it is: 0 = raster (m, n), the local kernel's
  *                   own traversal; 1 = the row tiles sharing a chunk key, ascending, are
