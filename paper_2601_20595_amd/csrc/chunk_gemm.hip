@@ -351,8 +351,8 @@ struct Bf16Loop {
     // A fragment is MF rows of 8 consecutive k values per lane: row lane % MF of the
     // block, 16-byte vector (64 / MF) ks + lane / MF of the row at k sub-step ks (k16
     // sub-steps with 32-row blocks, k32 with 16-row blocks). Every block starts on a
-    // multiple of 16 rows, so the row's swizzle is swz(lane % 16) (= swz(lane % 32) on
-    // 32-row blocks, whose rows 16..31 repeat the pattern of rows 0..15 ^ 1).
+    // multiple of 16 rows and swz repeats every 16 rows, so the row's swizzle is
+    // swz(lane % MF).
     constexpr int FI = WTM / MF, FJ = WTN / MF;  // fragments per operand and sub-step
     constexpr int VPS = 64 / MF;                 // 16-byte vectors per k sub-step
     const int lrow = lane % MF, lk = lane / MF;
@@ -1290,10 +1290,10 @@ const Variant kVariants[] = {
     // sooner after it lands)
     CSG_VARIANT(InType::BF16, LoopBf16_256x128, true, false, false),
     CSG_VARIANT(InType::BF16, LoopBf16_128x256, true, false, false),
-    // ... and for GEMM + reduce-scatter: twice the tiles, so the emitted chunks
+    CSG_VARIANT(InType::BF16, LoopBf16_128, true, false, false),
+    // 128 x 256 for GEMM + reduce-scatter too: twice the tiles, so the emitted chunks
     // complete over more waves and fewer are left to copy after the last one
     CSG_VARIANT(InType::BF16, LoopBf16_128x256, true, true, false),
-    CSG_VARIANT(InType::BF16, LoopBf16_128, true, false, false),
     // 256 x 224 tiles: N = 7 x 256 and 14 x 256 shapes fill every CU in whole waves
     CSG_VARIANT(InType::BF16, LoopBf16_256x224, true, false, false),
     CSG_VARIANT(InType::BF16, LoopBf16_256x224, false, false, false),
