@@ -12,12 +12,13 @@
 //   producer: after a tile, count it against every chunk it wrote; the tile that
 //             completes a chunk releases the chunk's flag for the copy engine.
 //
-// Main loops (each wave owns a sub-tile of 32 x 32 MFMA blocks):
+// Main loops (each wave owns a sub-tile of 32 x 32 output blocks, each one 32 x 32 or
+// four 16 x 16 MFMA blocks):
 //   bf16: 512 threads = 2 (M) x 4 (N) waves, two per SIMD, so one wave's MFMAs issue
 //         while the other waits on LDS or issues its loads; v_mfma_f32_32x32x16_bf16
-//         for 256-row and 256-column tiles, v_mfma_f32_16x16x32_bf16 for the smaller
-//         ones (the chip holds a higher clock with it, and the smaller tiles have the
-//         registers for its twice as many fragments);
+//         for 256 x 256 and 256 x 224 tiles, v_mfma_f32_16x16x32_bf16 for 128 x 256,
+//         256 x 128 and 128 x 128 (the chip holds a higher clock with it, and these
+//         tiles have the registers for its twice as many fragments);
 //         tiles stream HBM -> LDS with buffer_load ... lds (no register staging)
 //         through a ring of K stages: two for 256 x 256 tiles, three for the smaller
 //         tiles, whose stages take fewer MFMAs to consume than a load takes to land;
