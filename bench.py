@@ -83,6 +83,10 @@ def parse():
     ap.add_argument("--tune", action="store_true",
                     help="instead of the bench line, run the autotuner on the workload (chunk split, intra-chunk "
                          "order, dispatch, copy realization) and print its table as one JSON line")
+    ap.add_argument("--timeline", action="store_true",
+                    help="instead of the bench line, trace the work units of cold isolated overlap calls "
+                         "(when each unit was taken, started after its chunk waits, and finished) and print "
+                         "their distribution as one JSON line")
     return ap.parse_args()
 
 
@@ -107,6 +111,9 @@ def main():
     if args.tune:
         tune_workload(args)
         return
+    if args.timeline and si.WORKLOADS[args.config].op == "attn":
+        print("bench.py --timeline: the unit trace covers the GEMM operations", file=sys.stderr)
+        sys.exit(2)
     dev = "cuda:0"
     arch = csg.csg_device_check(0)
     w = si.WORKLOADS[args.config]
@@ -129,6 +136,8 @@ def main():
         cfg["copy_engines"] = args.lanes
     if args.plan_cfg:
         cfg.update(json.loads(args.plan_cfg))
+    if args.timeline:
+        cfg["trace"] = 1
     cfg = cfg or None
     if w.op == "attn":
         e = w.extras
@@ -249,6 +258,10 @@ def main():
             p.check()
             tot.append(ev0.elapsed_time(ev1))
         return np.array(tot)
+
+    if args.timeline:
+        print(json.dumps(timeline(w, plan, call, isolated, args, cfg, tuned)), flush=True)
+        return
 
     # ---- the timed region: overlap steps ------------------------------------------
     wall, ker = timed_loop("overlap", args.steps, args.warmup)
@@ -373,6 +386,39 @@ def main():
     if w.op in ("ag", "rs", "ar"):
         rec["hipblaslt_reference"] = hipblaslt_reference(w, a_full, b, compute)
     print(json.dumps(rec), flush=True)
+
+
+def timeline(w, plan, call, isolated, args, cfg, tuned):
+    """The work-unit trace of cold isolated overlap calls: per call, the device time
+    around the call (ms), and, in microseconds from the first unit's take (the kernel's
+    start), when the units were taken, started (after waiting for their chunks) and
+    finished, as percentiles over the call's units; wait = start - take; tail = the
+    kernel's end - the last start. The per-call lists hold one entry per call."""
+    reps = args.isolated_reps or 10
+    tot = isolated("overlap", reps, 3)            # warm-up calls included; the trace holds the last call
+    calls = []
+    qs = (0, 10, 25, 50, 75, 90, 100)
+    for i in range(reps):
+        t = isolated("overlap", 1, 0)
+        tr = plan.trace()
+        t0 = int(tr["t_take"].min())
+        take = (tr["t_take"].astype(np.int64) - t0) / 100.0
+        start = (tr["t_start"].astype(np.int64) - t0) / 100.0
+        end = (tr["t_end"].astype(np.int64) - t0) / 100.0
+        wait = start - take
+        calls.append({
+            "t_total_ms": round(float(t[0]), 4), "units": int(len(tr)), "kernel_us": round(float(end.max()), 1),
+            "start_us_pctl": [round(float(np.percentile(start, q)), 1) for q in qs],
+            "end_us_pctl": [round(float(np.percentile(end, q)), 1) for q in qs],
+            "unit_us_p10_p50_p90": [round(float(np.percentile(end - start, q)), 1) for q in (10, 50, 90)],
+            "wait_us_mean_p90_max": [round(float(wait.mean()), 1), round(float(np.percentile(wait, 90)), 1),
+                                     round(float(wait.max()), 1)],
+            "tail_us": round(float(end.max() - start.max()), 1),
+        })
+    return {"timeline": {"workload": w.name, "plan_cfg": cfg, "plan": "tuned" if tuned else "default",
+                         "calls": len(calls), "percentiles": list(qs),
+                         "t_total_ms_median_of_isolated_calls": round(float(np.median(tot)), 4),
+                         "per_call": calls}}
 
 
 def kernel_copy_sweep(w, sched, group_rows, d, timed_loop, moved_bytes, args, sweep=(32, 64, 128)):
