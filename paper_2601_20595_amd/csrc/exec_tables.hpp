@@ -21,7 +21,7 @@ struct ExecOptions {
   int32_t split_k = 1;      // K-slices of every tile
   int32_t tail_split = 0;   // K-slices of the tiles on the critical path (0/1: none)
   int32_t tail_chunks = 0;  // ... those reading one of the last (consumers) / first (producer) chunks
-  int32_t tile_dispatch = 0;  // 2: one plain list (static stride), else per-die sub-lists
+  int32_t tile_dispatch = 0;  // 2: one plain list (dealt statically, die-major), else per-die sub-lists
   int32_t grid = 0;         // persistent workgroups (round-robin over the dies)
   int32_t tail_wave = 0;    // > 1: K-slices (at most) for each die's last partial wave of tiles
 };
