@@ -285,8 +285,12 @@ def test_rs_128x256_tiles_parity(case, mode):
                 assert np.array_equal(O[rows], G[rows])
 
 
-def test_grouped_small_parity_with_empty_segments_and_partial_tiles():
-    _say("grouped small")
+@pytest.mark.parametrize("tile", [None, (128, 256), (256, 128), (128, 128)], ids=lambda t: str(t))
+def test_grouped_small_parity_with_empty_segments_and_partial_tiles(tile):
+    """Experts with empty, tiny and ragged segments, with the default tile and the
+    three-stage 16 x 16 x 32 tiles (which cut expert row ranges into more, smaller
+    partial tiles)."""
+    _say("grouped small tile=%s" % (tile,))
     W, E, N, K = 4, 3, 264, 256
     counts = np.array([[70, 0, 5], [0, 3, 1], [130, 0, 0], [1, 2, 300]], dtype=np.int64)
     chunks, order, gr = oracle.grouped_schedule(W, 1, counts)
@@ -294,7 +298,10 @@ def test_grouped_small_parity_with_empty_segments_and_partial_tiles():
     X = si.draw_matrix(104, 0, 0, (M, K), "normal", "bf16")
     B = si.draw_matrix(104, 1, 0, (E, N, K), "normal", "bf16")
     s = csg.Schedule.grouped(W, 1, counts)
-    plan = csg.Plan("grouped", M, N, K, "bf16", "bf16", s, group_rows=gr, cfg={"timeout_ms": 1000})
+    cfg = {"timeout_ms": 1000}
+    if tile:
+        cfg.update(bm=tile[0], bn=tile[1], bk=64)
+    plan = csg.Plan("grouped", M, N, K, "bf16", "bf16", s, group_rows=gr, cfg=cfg)
     c, _ = run_ag(plan, chunks, X, B, "bf16")
     R = oracle.grouped_gemm(X.device_array, B.device_array, chunks, order)
     assert_close(out_to_f64(c, "bf16"), R, 2e-2, "grouped small")
