@@ -52,9 +52,9 @@ CAL_BYTES = 256 << 20    # bytes read (and written) by the calibration copy
 TUNED_PLAN_CFG = {
     2: {"bm": 128, "bn": 256, "bk": 64, "intra_order": 1, "group_m": 4, "tile_dispatch": 2, "tail_split": 2,
         "tail_chunks": 4},
-    3: {"intra_order": 1, "group_m": 4, "tile_dispatch": 2},
-    4: {"bm": 128, "bn": 256, "bk": 64, "tile_dispatch": 2, "tail_split": 2, "tail_chunks": 8},
-    5: {"intra_order": 1, "group_m": 4, "tail_split": 2, "tail_chunks": 8},
+    3: {"bm": 128, "bn": 256, "bk": 64, "tile_dispatch": 2, "tail_split": 2, "tail_chunks": 4, "copy_split": 2},
+    4: {"bm": 128, "bn": 256, "bk": 64, "tile_dispatch": 2, "tail_split": 2, "tail_chunks": 8, "copy_split": 2},
+    5: {"intra_order": 1, "group_m": 4, "tile_dispatch": 2, "tail_split": 2, "tail_chunks": 4, "copy_split": 2},
 }
 FLUSH_BYTES = 512 << 20  # written before each isolated call: more than the last-level cache and every L2
 
@@ -530,14 +530,15 @@ def tune_workload(args):
                 ts.append(ev0.elapsed_time(ev1))
             return float(np.median(ts))
 
-        # the chunk split stays the workload's; the tile shape and the tail splits join
-        # the space (they decide how much work is left when the last chunk lands)
+        # the chunk split stays the workload's; the tile shape, the tail splits and the
+        # pieces of a chunk copy join the space (they decide how much work is left when
+        # the last chunk lands)
         cands = tune.search_space(w.op, chunk_splits=splits[:1], split_k=(1,),
                                   tail=((0, 0), (2, 4), (2, 8), (2, 16)), copy_workgroups=(64,),
-                                  tiles=(None, (128, 256)), intra=((0, 0), (1, 4)))
+                                  tiles=(None, (128, 256)), intra=((0, 0), (1, 4)), copy_split=(0, 2))
     else:
         cands = tune.search_space(w.op, chunk_splits=splits, split_k=(1,), tail=((0, 0),), copy_workgroups=(64,),
-                                  intra=((0, 0), (1, 1), (1, 2), (1, 4)))
+                                  intra=((0, 0), (1, 1), (1, 2), (1, 4)), copy_split=(0, 2))
     res, best = tune.autotune(make, call, cands, steps=args.steps, warmup=args.warmup, keep_best=True,
                               measure_fn=measure_fn)
     call(best, "overlap")

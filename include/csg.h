@@ -149,7 +149,17 @@ typedef struct {
  *                   the die's workgroups), which would run with the rest of the die idle;
  *                   those tiles are split into min(tail_wave, w / (L mod w)) K-slices
  *                   (added as for split_k). Per-die dispatch only (tile_dispatch 0/1);
- *                   0 or 1 = off */
+ *                   0 or 1 = off
+ *   copy_split      copy engines, all-gather, grouped and reduce-scatter plans: > 1 = a
+ *                   chunk copy may be cut into up to copy_split pieces (of at least
+ *                   512 KiB), each on its own engine. The library models each engine's
+ *                   queue (about 48 GB/s per engine) and gives a copy the engines
+ *                   expected to be free first, in the number of pieces that lands it
+ *                   soonest: copies issued while the engines are busy stay whole, a copy
+ *                   issued to idle engines lands in a fraction of one engine's time.
+ *                   The chunk's signal is armed to 1 and raised by pieces - 1 before the
+ *                   pieces are issued; each piece brings it down by one. 0 or 1 = every
+ *                   chunk whole, on engine (i mod engines) for the i-th copy */
 typedef struct {
     int32_t bm, bn, bk;
     int32_t intra_order;
@@ -166,6 +176,7 @@ typedef struct {
     int32_t copy_workgroups;
     int32_t group_m;
     int32_t tail_wave;
+    int32_t copy_split;
 } csg_plan_cfg;
 
 typedef struct csg_schedule csg_schedule;

@@ -74,7 +74,8 @@ class csg_plan_cfg(ctypes.Structure):
                 ("num_workgroups", ctypes.c_int32), ("copy_engines", ctypes.c_int32), ("timeout_ms", ctypes.c_int32),
                 ("split_k", ctypes.c_int32), ("tail_split", ctypes.c_int32), ("tail_chunks", ctypes.c_int32),
                 ("trace", ctypes.c_int32), ("warm_rows", ctypes.c_int32), ("copy_backend", ctypes.c_int32),
-                ("copy_workgroups", ctypes.c_int32), ("group_m", ctypes.c_int32), ("tail_wave", ctypes.c_int32)]
+                ("copy_workgroups", ctypes.c_int32), ("group_m", ctypes.c_int32), ("tail_wave", ctypes.c_int32),
+                ("copy_split", ctypes.c_int32)]
 
 
 class csg_plan_info(ctypes.Structure):

@@ -4,10 +4,12 @@
 //
 // Copy-engine realization (Section 5.2, realization (1): copy engine with
 // global-memory signals). Every chunk copy goes straight to an SDMA engine through
-// the HSA runtime (sdma.cpp), consecutive chunks on consecutive engines. A chunk's
+// the HSA runtime (sdma.cpp), consecutive chunks on consecutive engines, or, with
+// copy_split, cut into pieces on the engines expected to be free first. A chunk's
 // ready flag is the completion signal of its copy: a GPU-only HSA signal whose value
 // the host sets to 1 before the call's kernel is launched and the engine brings to 0
-// when the copy has landed; the kernel polls that value in memory. Signals come in
+// when the copy has landed (each piece of a cut copy brings it down by one, from the
+// number of pieces); the kernel polls that value in memory. Signals come in
 // two sets used by alternate calls, so a kernel still finishing the previous call
 // never sees its signals reset. No copy enters a HIP stream: on this platform a
 // stream wait (and the stream write/wait-value operations, which run as kernels)
@@ -842,8 +844,14 @@ struct CopyIssuer {
       const int64_t off = c.row_begin * row_bytes;
       const int64_t bytes = (c.row_end - c.row_begin) * row_bytes;
       const int eng = static_cast<int>(i % p->sdma.count());
-      hsa_status_t hs = p->sdma.copy(static_cast<char*>(landing) + off, static_cast<const char*>(staging) + off,
-                                     static_cast<size_t>(bytes), eng, nullptr, sigs[i]);
+      int pieces = 1;
+      hsa_status_t hs =
+          p->cfg.copy_split > 1
+              ? p->sdma.copy_pieces(static_cast<char*>(landing) + off, static_cast<const char*>(staging) + off,
+                                    static_cast<size_t>(bytes), p->cfg.copy_split, sigs[i], p->cfg.timeout_ms * 4,
+                                    &pieces)
+              : p->sdma.copy(static_cast<char*>(landing) + off, static_cast<const char*>(staging) + off,
+                             static_cast<size_t>(bytes), eng, nullptr, sigs[i]);
       // ring attention: the values follow on the next engine; the chunk's signal,
       // armed to 2, reaches 0 when both copies have completed
       if (hs == HSA_STATUS_SUCCESS && landing2)
@@ -1245,8 +1253,12 @@ csg_status csg_plan_create(csg_op op, int64_t M, int64_t N, int64_t K, csg_dtype
       c.trace < 0 || c.trace > 1 || c.warm_rows < 0 || c.warm_rows > 2 || c.copy_backend < 0 ||
       c.copy_backend > CSG_COPY_KERNEL || c.copy_workgroups < 0 || c.copy_workgroups > 4096 ||
       c.num_workgroups < 0 || c.tile_dispatch < 0 || c.tile_dispatch > 2 || c.intra_order < 0 ||
-      c.intra_order > 1 || c.group_m < 0 || c.tail_wave < 0 || c.tail_wave > 64)
+      c.intra_order > 1 || c.group_m < 0 || c.tail_wave < 0 || c.tail_wave > 64 || c.copy_split < 0 ||
+      c.copy_split > 32)
     return fail(CSG_ERR_INVALID, "bad plan configuration");
+  if (c.copy_split > 1 && (c.copy_backend != CSG_COPY_SDMA || op == CSG_GEMM_AR))
+    return fail(CSG_ERR_UNSUPPORTED, "copy_split cuts the copy engines' chunk copies of all-gather, grouped and "
+                                     "reduce-scatter plans");
   if (c.group_m == 0) c.group_m = 8;
   // split plans keep the grid a multiple of the die count (round-robin dispatch then
   // gives every die the same number of workgroups, and each die's list its share)
@@ -1672,10 +1684,14 @@ csg_status csg_gemm_rs(csg_plan* p, const void* a, const void* b_nk, void* c, vo
       return fail(CSG_ERR_TIMEOUT, "an earlier copy out of chunk %d did not complete", cid);
     }
     hsa_signal_store_relaxed(sig, 1);
+    const size_t bytes = static_cast<size_t>((ch.row_end - ch.row_begin) * row_bytes);
+    int pieces = 1;
     const hsa_status_t hs =
-        p->sdma.copy(static_cast<char*>(c_outgoing) + off, static_cast<const char*>(c) + off,
-                     static_cast<size_t>((ch.row_end - ch.row_begin) * row_bytes), static_cast<int>(i % p->sdma.count()),
-                     nullptr, sig);
+        p->cfg.copy_split > 1
+            ? p->sdma.copy_pieces(static_cast<char*>(c_outgoing) + off, static_cast<const char*>(c) + off, bytes,
+                                  p->cfg.copy_split, sig, p->cfg.timeout_ms * 4, &pieces)
+            : p->sdma.copy(static_cast<char*>(c_outgoing) + off, static_cast<const char*>(c) + off, bytes,
+                           static_cast<int>(i % p->sdma.count()), nullptr, sig);
     if (hs != HSA_STATUS_SUCCESS) {
       hsa_signal_store_relaxed(sig, 0);
       return fail(CSG_ERR_HIP, "SDMA copy: %s", csg::hsa_error(hs).c_str());
@@ -1700,7 +1716,8 @@ csg_status csg_attn_plan_create(int32_t n_heads, int32_t n_kv_heads, int32_t hea
   if (c.timeout_ms == 0) c.timeout_ms = 2000;
   if (c.copy_engines < 0 || c.copy_engines > 32 || c.timeout_ms < 1 || c.num_workgroups < 0)
     return fail(CSG_ERR_INVALID, "bad plan configuration");
-  if (c.copy_backend != CSG_COPY_SDMA || c.split_k > 1 || c.tail_split > 1 || c.tail_wave > 1 || c.intra_order != 0 || c.trace)
+  if (c.copy_backend != CSG_COPY_SDMA || c.split_k > 1 || c.tail_split > 1 || c.tail_wave > 1 || c.intra_order != 0 ||
+      c.trace || c.copy_split > 1)
     return fail(CSG_ERR_UNSUPPORTED, "attention plans copy with the SDMA engines and split or trace nothing");
   const csg::Schedule& sch = s->s;
   if (sch.chunks.size() > 4096) return fail(CSG_ERR_UNSUPPORTED, "at most 4096 chunks");

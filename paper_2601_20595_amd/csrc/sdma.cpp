@@ -3,7 +3,9 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <chrono>
+#include <numeric>
 
 namespace csg {
 
@@ -86,12 +88,14 @@ std::string SdmaEngines::open(int hip_device, int max_engines, void* scratch_dst
     close();
     return "no SDMA engine completed a device-to-device copy";
   }
+  free_at_.assign(engines_.size(), std::chrono::steady_clock::time_point{});
   opened_ = true;
   return "";
 }
 
 void SdmaEngines::close() {
   engines_.clear();
+  free_at_.clear();
   opened_ = false;
   if (hsa_inited_) {
     (void)hsa_shut_down();
@@ -104,6 +108,53 @@ hsa_status_t SdmaEngines::copy(void* dst, const void* src, size_t bytes, int eng
   const hsa_amd_sdma_engine_id_t id = engines_[static_cast<size_t>(engine) % engines_.size()];
   return hsa_amd_memory_async_copy_on_engine(dst, agent_, src, agent_, bytes, dep ? 1u : 0u, dep, done, id,
                                              /*force_copy_on_sdma=*/true);
+}
+
+hsa_status_t SdmaEngines::copy_pieces(void* dst, const void* src, size_t bytes, int max_pieces, hsa_signal_t done,
+                                      int budget_ms, int* pieces) {
+  using Clock = std::chrono::steady_clock;
+  const int n = count();
+  const Clock::time_point now = Clock::now();
+  auto start_us = [&](int e) {
+    return std::chrono::duration<double, std::micro>(std::max(now, free_at_[static_cast<size_t>(e)]) - now).count();
+  };
+  std::vector<int> order(static_cast<size_t>(n));
+  std::iota(order.begin(), order.end(), 0);
+  std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return start_us(x) < start_us(y); });
+  const int pmax = static_cast<int>(std::max<size_t>(
+      1, std::min<size_t>({static_cast<size_t>(std::max(max_pieces, 1)), static_cast<size_t>(n), bytes / kMinPieceBytes})));
+  // P pieces on the P engines free first land when the last of those engines is
+  // through its share
+  int best = 1;
+  double best_us = start_us(order[0]) + static_cast<double>(bytes) / kEngineBytesPerUs;
+  for (int q = 2; q <= pmax; ++q) {
+    const double t = start_us(order[static_cast<size_t>(q - 1)]) + static_cast<double>(bytes) / q / kEngineBytesPerUs;
+    if (t <= best_us - kPieceGainUs) {
+      best = q;
+      best_us = t;
+    }
+  }
+  *pieces = best;
+  if (best > 1) hsa_signal_add_relaxed(done, best - 1);
+  // piece k covers [k * step, (k + 1) * step), the last one the rest; 64 KiB multiples
+  const size_t step = (bytes / static_cast<size_t>(best)) & ~size_t{65535};
+  for (int k = 0; k < best; ++k) {
+    const size_t off = static_cast<size_t>(k) * step;
+    const size_t len = k + 1 < best ? step : bytes - off;
+    const int e = order[static_cast<size_t>(k)];
+    const hsa_status_t s = copy(static_cast<char*>(dst) + off, static_cast<const char*>(src) + off, len, e, nullptr,
+                                done);
+    if (s != HSA_STATUS_SUCCESS) {
+      // the k pieces issued bring `done` down to best - k; then no piece is in flight
+      (void)sdma_wait(done, best - k, budget_ms);
+      hsa_signal_subtract_relaxed(done, best - k - 1);
+      return s;
+    }
+    free_at_[static_cast<size_t>(e)] =
+        std::max(now, free_at_[static_cast<size_t>(e)]) +
+        std::chrono::nanoseconds(static_cast<int64_t>(static_cast<double>(len) / kEngineBytesPerUs * 1000.0));
+  }
+  return HSA_STATUS_SUCCESS;
 }
 
 hsa_signal_value_t sdma_wait(hsa_signal_t s, hsa_signal_value_t value, int budget_ms) {

@@ -11,6 +11,7 @@
 #include <hsa/hsa.h>
 #include <hsa/hsa_ext_amd.h>
 
+#include <chrono>
 #include <cstddef>
 #include <string>
 #include <vector>
@@ -52,11 +53,32 @@ class SdmaEngines {
   hsa_status_t copy(void* dst, const void* src, size_t bytes, int engine, const hsa_signal_t* dep,
                     hsa_signal_t done) const;
 
+  // Copy `bytes` from src to dst in up to `max_pieces` pieces of at least kMinPieceBytes,
+  // each on its own engine. The engines are chosen by a model of their queues: each
+  // engine works through the pieces given to it in order at kEngineBytesPerUs, so it
+  // is expected to be free at a known time. The pieces go to the engines expected to
+  // be free first, and their number is the one that lands the copy soonest; one piece
+  // more is taken only when it brings the landing forward by at least kPieceGainUs. So
+  // a copy issued while most engines are busy stays whole, and one issued while
+  // engines are idle is spread over them.
+  // `done` must read 1 for this copy when it is called: it is raised by pieces - 1
+  // before the pieces are issued, and each piece decrements it, so it reads 0 once
+  // every piece has landed. If issuing a piece fails, the call waits (at most
+  // budget_ms) for the pieces already issued, sets `done` back to 1 and returns the
+  // error: the state of a copy that was never issued. *pieces is the number chosen.
+  hsa_status_t copy_pieces(void* dst, const void* src, size_t bytes, int max_pieces, hsa_signal_t done,
+                           int budget_ms, int* pieces);
+
+  static constexpr size_t kMinPieceBytes = size_t{512} << 10;
+  static constexpr double kEngineBytesPerUs = 48000.0;  // about 48 GB/s per engine
+  static constexpr double kPieceGainUs = 2.0;
+
  private:
   bool opened_ = false;
   bool hsa_inited_ = false;
   hsa_agent_t agent_{0};
   std::vector<hsa_amd_sdma_engine_id_t> engines_;
+  std::vector<std::chrono::steady_clock::time_point> free_at_;  // copy_pieces' model, per engine
 };
 
 // Polls `s` until it reads `value` or `budget_ms` pass. Returns the last value read.

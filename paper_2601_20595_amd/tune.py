@@ -83,7 +83,7 @@ def search_space(op: str, chunk_splits: Sequence[Optional[int]] = (None,), dispa
                  copy_workgroups: Sequence[int] = (32, 64, 128), sdma: bool = True,
                  kernel_copies: bool = True, tiles: Sequence[Optional[Tuple[int, int]]] = (None,),
                  grids: Sequence[int] = (0,), intra: Sequence[Tuple[int, int]] = ((0, 0),),
-                 tail_wave: Sequence[int] = (0,)) -> List[Candidate]:
+                 tail_wave: Sequence[int] = (0,), copy_split: Sequence[int] = (0,)) -> List[Candidate]:
     """Candidates in a fixed order (the first one is the library's default plan).
 
     op: "ag", "rs" or "grouped". GEMM-RS has no copy workgroups (its kernel
@@ -95,7 +95,9 @@ def search_space(op: str, chunk_splits: Sequence[Optional[int]] = (None,), dispa
     into whole waves (224 for 896 tiles on 256 CUs) keeps the waves in step and the
     workgroups sharing a die's L2 at the same K steps. intra: (intra_order, group_m)
     pairs, (0, 0) the raster order. tail_wave: maximum K-slices for each die's last
-    partial wave (0 = off); only combined with per-die dispatch and no other split."""
+    partial wave (0 = off); only combined with per-die dispatch and no other split.
+    copy_split: the most pieces a chunk copy may be cut into on idle copy engines
+    (0 = whole chunks); copy-engine candidates only."""
     if op not in ("ag", "rs", "grouped"):
         raise ValueError("unknown op %r" % op)
     backends: List[Tuple[int, Optional[int]]] = []
@@ -108,17 +110,20 @@ def search_space(op: str, chunk_splits: Sequence[Optional[int]] = (None,), dispa
             backends += [(1, cw) for cw in copy_workgroups]
     out: List[Candidate] = []
     seen = set()
-    for q, (be, cw), disp, sk, (ts, tc), tile, grid, (io, gm), tw in itertools.product(
-            chunk_splits, backends, dispatch, split_k, tail, tiles, grids, intra, tail_wave):
+    for q, (be, cw), disp, sk, (ts, tc), tile, grid, (io, gm), tw, cs in itertools.product(
+            chunk_splits, backends, dispatch, split_k, tail, tiles, grids, intra, tail_wave, copy_split):
         if sk > 1 and ts > 1:
             continue
         if tw > 1 and (disp == 2 or sk > 1 or ts > 1):
+            continue
+        if cs > 1 and be != 0:
             continue
         bm, bn = tile if tile is not None else (None, None)
         c = Candidate(q, _cfg(copy_backend=be or None, copy_workgroups=cw, tile_dispatch=disp if disp != 1 else None,
                               split_k=sk if sk > 1 else None, tail_split=ts or None, tail_chunks=tc or None,
                               bm=bm, bn=bn, bk=64 if tile is not None else None, num_workgroups=grid or None,
-                              intra_order=io or None, group_m=gm if io else None, tail_wave=tw if tw > 1 else None))
+                              intra_order=io or None, group_m=gm if io else None, tail_wave=tw if tw > 1 else None,
+                              copy_split=cs if cs > 1 else None))
         if c not in seen:
             seen.add(c)
             out.append(c)

@@ -161,3 +161,20 @@ def test_bench_tuned_plan_configurations_are_accepted():
         assert (p.info.bm, p.info.bn) == (cfg.get("bm", 256), cfg.get("bn", 256))
         p.close()
         s.close()
+
+
+def test_search_space_copy_split_dimension():
+    """Cutting chunk copies into pieces is a dimension of the copy-engine candidates only;
+    the default candidate stays first and every copy-engine candidate comes once whole
+    and once per piece count."""
+    base = tune.search_space("rs")
+    sp = tune.search_space("rs", copy_split=(0, 2, 4))
+    assert sp[0] == base[0]
+    sdma = [c for c in sp if ("copy_backend", 1) not in c.cfg]
+    for c in sp:
+        d = c.cfg_dict()
+        if d.get("copy_split"):
+            assert d.get("copy_backend", 0) == 0
+    assert len(sdma) == 3 * sum(1 for c in sdma if "copy_split" not in c.cfg_dict())
+    assert len(sp) - len(sdma) == len(base) - sum(1 for c in base if ("copy_backend", 1) not in c.cfg)
+
