@@ -52,7 +52,7 @@ CAL_BYTES = 256 << 20    # bytes read (and written) by the calibration copy
 TUNED_PLAN_CFG = {
     2: {"bm": 128, "bn": 256, "bk": 64, "intra_order": 1, "group_m": 4, "tile_dispatch": 2, "tail_split": 2,
         "tail_chunks": 4},
-    3: {"bm": 128, "bn": 256, "bk": 64, "tile_dispatch": 2, "tail_split": 2, "tail_chunks": 4, "copy_split": 2},
+    3: {"intra_order": 1, "group_m": 4, "tile_dispatch": 2},
     4: {"bm": 128, "bn": 256, "bk": 64, "tile_dispatch": 2, "tail_split": 2, "tail_chunks": 8, "copy_split": 2},
     5: {"intra_order": 1, "group_m": 4, "tile_dispatch": 2, "tail_split": 2, "tail_chunks": 4, "copy_split": 2},
 }
