@@ -50,10 +50,10 @@ CAL_BYTES = 256 << 20    # bytes read (and written) by the calibration copy
 # collective; the kernel's own copies move chunks inside HBM faster than links would):
 # plan configuration fields. --default-plan measures the library's defaults instead.
 TUNED_PLAN_CFG = {
-    2: {"bm": 128, "bn": 256, "bk": 64, "intra_order": 1, "group_m": 4, "tile_dispatch": 2, "tail_split": 2,
-        "tail_chunks": 4},
+    2: {"bm": 128, "bn": 256, "bk": 64, "tile_dispatch": 2, "tail_split": 2, "tail_chunks": 4},
     3: {"intra_order": 1, "group_m": 4, "tile_dispatch": 2},
-    4: {"bm": 128, "bn": 256, "bk": 64, "tile_dispatch": 2, "tail_split": 2, "tail_chunks": 8, "copy_split": 2},
+    4: {"bm": 128, "bn": 256, "bk": 64, "tile_dispatch": 2, "tail_split": 4, "tail_chunks": 12, "tail_taper": 1,
+        "copy_split": 2},
     5: {"intra_order": 1, "group_m": 4, "tile_dispatch": 2, "tail_split": 2, "tail_chunks": 4, "copy_split": 2},
 }
 FLUSH_BYTES = 512 << 20  # written before each isolated call: more than the last-level cache and every L2
@@ -530,12 +530,13 @@ def tune_workload(args):
                 ts.append(ev0.elapsed_time(ev1))
             return float(np.median(ts))
 
-        # the chunk split stays the workload's; the tile shape, the tail splits and the
-        # pieces of a chunk copy join the space (they decide how much work is left when
-        # the last chunk lands)
+        # the chunk split stays the workload's; the tile shape, the tail splits (even or
+        # tapered) and the pieces of a chunk copy join the space (they decide how much
+        # work is left when the last chunk lands)
         cands = tune.search_space(w.op, chunk_splits=splits[:1], split_k=(1,),
-                                  tail=((0, 0), (2, 4), (2, 8), (2, 16)), copy_workgroups=(64,),
-                                  tiles=(None, (128, 256)), intra=((0, 0), (1, 4)), copy_split=(0, 2))
+                                  tail=((0, 0), (2, 4), (2, 8), (2, 16), (4, 12), (6, 12)), copy_workgroups=(64,),
+                                  tiles=(None, (128, 256)), intra=((0, 0), (1, 4)), copy_split=(0, 2),
+                                  tail_taper=(0, 1))
     else:
         cands = tune.search_space(w.op, chunk_splits=splits, split_k=(1,), tail=((0, 0),), copy_workgroups=(64,),
                                   intra=((0, 0), (1, 1), (1, 2), (1, 4)), copy_split=(0, 2))

@@ -122,7 +122,10 @@ typedef struct {
  *                   atomic ticket; 2 = static: workgroup w takes entries s, s + G, s + 2G,
  *                   ... with s = (w mod 8) * (G / 8) + w / 8 when G is a multiple of 8
  *                   (else s = w), so that the workgroups of one die (the dispatcher
- *                   deals workgroups to the 8 dies round robin) take consecutive entries
+ *                   deals workgroups to the 8 dies round robin) take consecutive entries;
+ *                   with a tail split (all-gather and grouped GEMMs) the units of the
+ *                   split tail tiles, which end the list, are taken in order from a
+ *                   shared ticket by whichever workgroup is free first
  *   num_workgroups  persistent grid size G (0 = one per co-resident slot)
  *   copy_engines    SDMA engines the chunk copies are spread over (0 = every engine the
  *                   device offers for device-to-device copies)
@@ -159,7 +162,12 @@ typedef struct {
  *                   issued to idle engines lands in a fraction of one engine's time.
  *                   The chunk's signal is armed to 1 and raised by pieces - 1 before the
  *                   pieces are issued; each piece brings it down by one. 0 or 1 = every
- *                   chunk whole, on engine (i mod engines) for the i-th copy */
+ *                   chunk whole, on engine (i mod engines) for the i-th copy
+ *   tail_taper      1 = the tail split tapers: the tiles of the j-th of the tail_chunks
+ *                   chunks, counted from the last to arrive (AG, grouped) or the first
+ *                   emitted (RS), get ceil(S / (1 + j (S - 1) / (C - 1))) K-slices, S =
+ *                   tail_split, C = tail_chunks (S for the last chunk, 1 for the C-th);
+ *                   0 = every tail tile gets tail_split slices */
 typedef struct {
     int32_t bm, bn, bk;
     int32_t intra_order;
@@ -177,6 +185,7 @@ typedef struct {
     int32_t group_m;
     int32_t tail_wave;
     int32_t copy_split;
+    int32_t tail_taper;
 } csg_plan_cfg;
 
 typedef struct csg_schedule csg_schedule;

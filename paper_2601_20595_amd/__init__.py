@@ -75,7 +75,7 @@ class csg_plan_cfg(ctypes.Structure):
                 ("split_k", ctypes.c_int32), ("tail_split", ctypes.c_int32), ("tail_chunks", ctypes.c_int32),
                 ("trace", ctypes.c_int32), ("warm_rows", ctypes.c_int32), ("copy_backend", ctypes.c_int32),
                 ("copy_workgroups", ctypes.c_int32), ("group_m", ctypes.c_int32), ("tail_wave", ctypes.c_int32),
-                ("copy_split", ctypes.c_int32)]
+                ("copy_split", ctypes.c_int32), ("tail_taper", ctypes.c_int32)]
 
 
 class csg_plan_info(ctypes.Structure):

@@ -127,6 +127,7 @@ struct csg_plan {
   float* d_ws = nullptr;               // split-K partial sums
   uint32_t* d_slot_count = nullptr;    // split-K finished slices per tile, [2][n_tiles]
   int32_t ws_slices = 0;               // partial-sum buffers of split tiles (0: nothing is split)
+  int32_t tail_begin = 0;              // static dispatch: first unit dealt from the shared ticket
   uint64_t* d_trace = nullptr;         // per-unit trace words (cfg.trace)
   std::vector<csg::TileDesc> units;    // host copy of the execution list
   std::vector<int32_t> unit_raster;    // raster id per execution position
@@ -316,6 +317,7 @@ csg_status setup_device(csg_plan* p) {
   eo.split_k = p->cfg.split_k;
   eo.tail_split = p->cfg.tail_split;
   eo.tail_chunks = p->cfg.tail_chunks;
+  eo.tail_taper = p->cfg.tail_taper;
   eo.tile_dispatch = p->cfg.tile_dispatch;
   eo.grid = p->grid;
   eo.tail_wave = p->cfg.tail_wave;
@@ -330,6 +332,7 @@ csg_status setup_device(csg_plan* p) {
   const int32_t ws_slices = et.ws_slices;
   const int32_t n_units = static_cast<int32_t>(tiles.size());
   p->ws_slices = ws_slices;
+  p->tail_begin = et.tail_begin;
   p->units = tiles;
   p->unit_raster = raster;
   p->n_units = n_units;
@@ -656,6 +659,7 @@ csg_status launch_gemm(csg_plan* p, const void* A, const void* B, void* C, csg_m
   }
   a.n_chunks = p->n_chunks();
   a.dynamic_ticket = p->cfg.tile_dispatch == 2 ? 0 : 1;
+  a.tail_begin = p->tail_begin;
   // Idle workgroups take other dies' units (split tiles exchange partial sums through
   // memory, so their slices may run on any die).
   a.steal = 1;
@@ -1254,7 +1258,7 @@ csg_status csg_plan_create(csg_op op, int64_t M, int64_t N, int64_t K, csg_dtype
       c.copy_backend > CSG_COPY_KERNEL || c.copy_workgroups < 0 || c.copy_workgroups > 4096 ||
       c.num_workgroups < 0 || c.tile_dispatch < 0 || c.tile_dispatch > 2 || c.intra_order < 0 ||
       c.intra_order > 1 || c.group_m < 0 || c.tail_wave < 0 || c.tail_wave > 64 || c.copy_split < 0 ||
-      c.copy_split > 32)
+      c.copy_split > 32 || c.tail_taper < 0 || c.tail_taper > 1)
     return fail(CSG_ERR_INVALID, "bad plan configuration");
   if (c.copy_split > 1 && (c.copy_backend != CSG_COPY_SDMA || op == CSG_GEMM_AR))
     return fail(CSG_ERR_UNSUPPORTED, "copy_split cuts the copy engines' chunk copies of all-gather, grouped and "

@@ -798,14 +798,22 @@ __global__ __launch_bounds__(Loop::THREADS, 1) void chunk_gemm(GemmArgs a) {
   // dispatcher hands workgroups to the dies round robin (w mod 8), so with
   // slot = (w mod 8) * (G / 8) + w / 8 the workgroups of one die take consecutive
   // entries of every round of G: the tiles of one chunk start together on one die and
-  // share its L2 (its A rows, and the B columns of the chunks that follow).
+  // share its L2 (its A rows, and the B columns of the chunks that follow). Entries
+  // from tail_begin on (the K-slices of the last chunks' tiles) go to whichever
+  // workgroup asks first: a workgroup whose next static entry lies there takes the next
+  // one from a shared ticket instead, so those slices start as soon as their chunk
+  // lands rather than behind their fixed workgroup's previous tile.
   const int grid = static_cast<int>(gridDim.x), wg = static_cast<int>(blockIdx.x);
   const int slot = grid % kXcdLists == 0 ? (wg % kXcdLists) * (grid / kXcdLists) + wg / kXcdLists : wg;
   int iter = 0;
   for (;; ++iter) {
     __syncthreads();  // everyone is done with s_pos / s_state / LDS of the previous tile
     if (tid == 0) {
-      const int pos = a.dynamic_ticket ? next_tile(a, xcd) : slot + iter * grid;
+      int pos = a.dynamic_ticket ? next_tile(a, xcd) : slot + iter * grid;
+      if (!a.dynamic_ticket && a.tail_begin > 0 && pos >= a.tail_begin) {
+        const int t = static_cast<int>(atomicAdd(a.ticket, 1u));
+        pos = t < a.n_tiles - a.tail_begin ? a.tail_begin + t : a.n_tiles;
+      }
       int state = 0;
       if (pos < a.n_tiles) {
         const uint64_t t_take = a.trace ? wall_clock64() : 0;

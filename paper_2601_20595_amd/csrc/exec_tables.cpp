@@ -32,6 +32,7 @@ void build_exec_tables(const Schedule& s, const TileMap& m, const ExecOptions& o
   // chunks (producer)
   const int32_t KT = static_cast<int32_t>(o.K / o.bk);
   std::vector<int32_t> tile_split(n_tiles, std::max(1, o.split_k));
+  std::vector<char> critical_tile(n_tiles, 0);
   if (o.tail_split > 1 && o.tail_chunks > 0) {
     std::vector<int32_t> pos(n_chunks);
     for (int32_t i = 0; i < n_chunks; ++i) pos[s.order[i]] = i;
@@ -42,9 +43,30 @@ void build_exec_tables(const Schedule& s, const TileMap& m, const ExecOptions& o
         hi = std::max(hi, pos[m.tile_chunks[q]]);
       }
       const bool critical = o.consumer ? hi >= n_chunks - o.tail_chunks : lo < o.tail_chunks;
-      if (critical) tile_split[t] = std::max(tile_split[t], o.tail_split);
+      if (critical) {
+        // tapered: the tiles of the j-th chunk from the end of the tail (j = 0: the last
+        // to arrive, or the first to be emitted) get ceil(S / (1 + j (S - 1) / (C - 1)))
+        // slices, S = tail_split, C = tail_chunks: S for the last chunk, 1 for the C-th;
+        // a chunk landing d before the last leaves its tiles about d to finish in, and
+        // the slice count falls roughly as 1 / d
+        int32_t sp = o.tail_split;
+        if (o.tail_taper && o.tail_chunks > 1) {
+          const int64_t j = o.consumer ? n_chunks - 1 - hi : lo;
+          const int64_t S = o.tail_split, Cn = o.tail_chunks;
+          // ceil(S (C - 1) / (C - 1 + j (S - 1)))
+          sp = static_cast<int32_t>((S * (Cn - 1) + (Cn - 1 + j * (S - 1)) - 1) / (Cn - 1 + j * (S - 1)));
+        }
+        tile_split[t] = std::max(tile_split[t], sp);
+        critical_tile[t] = 1;
+      }
     }
   }
+  // Static dispatch, consumers: the critical tiles read the last-arriving chunks, so
+  // they end the chunk-ordered list; the units from the first of that trailing run on
+  // are dealt from a shared ticket.
+  int32_t tail_tile = n_tiles;
+  if (o.tile_dispatch == 2 && o.consumer && o.tail_split > 1 && o.tail_chunks > 0)
+    while (tail_tile > 0 && critical_tile[exec_order[tail_tile - 1]]) --tail_tile;
   // Each die's last partial wave: with w workgroups on a die and L tiles in its list,
   // the last L mod w tiles would run with the rest of the die idle; split each of them
   // into up to w / (L mod w) K-slices (at most tail_wave) so that they fill the die.
@@ -68,6 +90,7 @@ void build_exec_tables(const Schedule& s, const TileMap& m, const ExecOptions& o
   std::vector<int32_t> unit_begin(kXcdLists + 1, 0);
   for (int32_t i = 0, x = 0; i < n_tiles; ++i) {
     while (x <= kXcdLists && list_begin[x] == i) unit_begin[x++] = static_cast<int32_t>(r.units.size());
+    if (i == tail_tile) r.tail_begin = static_cast<int32_t>(r.units.size());
     const int32_t t = exec_order[i];
     const RowTile& rt = m.row_tiles[t / nN];
     const int32_t split = tile_split[t];

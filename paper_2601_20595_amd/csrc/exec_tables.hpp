@@ -21,6 +21,7 @@ struct ExecOptions {
   int32_t split_k = 1;      // K-slices of every tile
   int32_t tail_split = 0;   // K-slices of the tiles on the critical path (0/1: none)
   int32_t tail_chunks = 0;  // ... those reading one of the last (consumers) / first (producer) chunks
+  int32_t tail_taper = 0;   // 1: the tail split tapers from tail_split (the last / first chunk) to 1
   int32_t tile_dispatch = 0;  // 2: one plain list (dealt statically, die-major), else per-die sub-lists
   int32_t grid = 0;         // persistent workgroups (round-robin over the dies)
   int32_t tail_wave = 0;    // > 1: K-slices (at most) for each die's last partial wave of tiles
@@ -34,6 +35,8 @@ struct ExecTables {
   std::vector<int32_t> need;         // per chunk: units reading it (consumers) / tiles writing it (producer)
   std::vector<int32_t> list_begin;   // [kXcdLists + 1]: die x runs units [list_begin[x], list_begin[x + 1])
   int32_t ws_slices = 0;             // partial-sum buffers of split tiles
+  int32_t tail_begin = 0;            // static dispatch, consumers: first unit of the trailing
+                                     // critical tiles, dealt from a shared ticket (0: none)
   bool lines_aligned = true;         // every chunk of A starts on a 128-byte line
 };
 

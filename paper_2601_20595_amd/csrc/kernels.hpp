@@ -73,6 +73,10 @@ struct GemmArgs {
   int32_t n_tiles;
   int32_t n_chunks;
   int32_t dynamic_ticket;
+  // Static dispatch: positions tail_begin .. n_tiles - 1 (the units of the tiles on the
+  // critical path, which end the list) are taken in order from ticket[0] by whichever
+  // workgroup is free first, instead of by a fixed workgroup. 0: every position static.
+  int32_t tail_begin;
   // Consumers: 1 if a cache line of A may hold rows of two chunks (a chunk boundary
   // or the buffer start not on a 128-byte line), so a line cached while one chunk was
   // ready could hold stale rows of the next; then a workgroup drops its caches when

@@ -83,7 +83,8 @@ def search_space(op: str, chunk_splits: Sequence[Optional[int]] = (None,), dispa
                  copy_workgroups: Sequence[int] = (32, 64, 128), sdma: bool = True,
                  kernel_copies: bool = True, tiles: Sequence[Optional[Tuple[int, int]]] = (None,),
                  grids: Sequence[int] = (0,), intra: Sequence[Tuple[int, int]] = ((0, 0),),
-                 tail_wave: Sequence[int] = (0,), copy_split: Sequence[int] = (0,)) -> List[Candidate]:
+                 tail_wave: Sequence[int] = (0,), copy_split: Sequence[int] = (0,),
+                 tail_taper: Sequence[int] = (0,)) -> List[Candidate]:
     """Candidates in a fixed order (the first one is the library's default plan).
 
     op: "ag", "rs" or "grouped". GEMM-RS has no copy workgroups (its kernel
@@ -97,7 +98,8 @@ def search_space(op: str, chunk_splits: Sequence[Optional[int]] = (None,), dispa
     pairs, (0, 0) the raster order. tail_wave: maximum K-slices for each die's last
     partial wave (0 = off); only combined with per-die dispatch and no other split.
     copy_split: the most pieces a chunk copy may be cut into on idle copy engines
-    (0 = whole chunks); copy-engine candidates only."""
+    (0 = whole chunks); copy-engine candidates only. tail_taper: 1 = the tail split
+    tapers from tail_split to 1 over the tail chunks; only with a tail split."""
     if op not in ("ag", "rs", "grouped"):
         raise ValueError("unknown op %r" % op)
     backends: List[Tuple[int, Optional[int]]] = []
@@ -110,8 +112,10 @@ def search_space(op: str, chunk_splits: Sequence[Optional[int]] = (None,), dispa
             backends += [(1, cw) for cw in copy_workgroups]
     out: List[Candidate] = []
     seen = set()
-    for q, (be, cw), disp, sk, (ts, tc), tile, grid, (io, gm), tw, cs in itertools.product(
-            chunk_splits, backends, dispatch, split_k, tail, tiles, grids, intra, tail_wave, copy_split):
+    for q, (be, cw), disp, sk, (ts, tc), tile, grid, (io, gm), tw, cs, tt in itertools.product(
+            chunk_splits, backends, dispatch, split_k, tail, tiles, grids, intra, tail_wave, copy_split, tail_taper):
+        if tt and not (ts > 1 and tc > 1):
+            continue
         if sk > 1 and ts > 1:
             continue
         if tw > 1 and (disp == 2 or sk > 1 or ts > 1):
@@ -123,7 +127,7 @@ def search_space(op: str, chunk_splits: Sequence[Optional[int]] = (None,), dispa
                               split_k=sk if sk > 1 else None, tail_split=ts or None, tail_chunks=tc or None,
                               bm=bm, bn=bn, bk=64 if tile is not None else None, num_workgroups=grid or None,
                               intra_order=io or None, group_m=gm if io else None, tail_wave=tw if tw > 1 else None,
-                              copy_split=cs if cs > 1 else None))
+                              copy_split=cs if cs > 1 else None, tail_taper=tt or None))
         if c not in seen:
             seen.add(c)
             out.append(c)

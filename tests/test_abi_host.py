@@ -156,7 +156,7 @@ def test_validation_errors():
     assert _status(csg.Plan, "ag", 128, 64, 64, "bf16", "bf16", s, cfg={"tail_split": -1}, device=-1) \
         == csg.CSG_ERR_INVALID
     for bad in ({"intra_order": 2}, {"intra_order": -1}, {"group_m": -1}, {"tail_wave": 65}, {"tail_wave": -1},
-                {"copy_split": -1}, {"copy_split": 33}):
+                {"copy_split": -1}, {"copy_split": 33}, {"tail_taper": -1}, {"tail_taper": 2}):
         assert _status(csg.Plan, "ag", 128, 64, 64, "bf16", "bf16", s, cfg=bad, device=-1) == csg.CSG_ERR_INVALID
     # pieces of chunk copies: copy engines only, and not for the all-reduce's copies
     assert _status(csg.Plan, "ag", 128, 64, 64, "bf16", "bf16", s, cfg={"copy_split": 4}, device=-1) == csg.CSG_OK

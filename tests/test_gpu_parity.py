@@ -378,6 +378,43 @@ def test_static_dispatch_die_major_slots_cover_every_unit(grid, split):
     assert_close(out_to_f64(c, "bf16"), R, tol_for("bf16", "bf16"), "ag static dispatch")
 
 
+@pytest.mark.parametrize("grid,tail_split,tail_chunks", [(16, 2, 3), (24, 4, 2), (256, 2, 4), (40, 3, 16)],
+                         ids=lambda v: str(v))
+def test_static_dispatch_shared_tail_ticket(grid, tail_split, tail_chunks):
+    """Static dispatch with a tail split: every position before the tail tiles runs on
+    its static workgroup, the tail tiles' K-slices on whichever workgroup took them from
+    the shared ticket, every position ran, and the output matches the oracle. With
+    every chunk in the tail (the last case) the whole list is static."""
+    _say("static dispatch shared tail grid %d split %d chunks %d" % (grid, tail_split, tail_chunks))
+    W, r, S, Q, kind, N, K = 4, 1, 512, 4, "ring", 776, 640
+    w, d, perm, chunks, order = _small_ag(W, r, S, Q, kind, N, K, "bf16", "bf16")
+    s = csg.Schedule.uniform(W, r, S, Q, kind, perm)
+    plan = csg.Plan("ag", W * S, N, K, "bf16", "bf16", s,
+                    cfg={"timeout_ms": 1000, "tile_dispatch": 2, "num_workgroups": grid, "tail_split": tail_split,
+                         "tail_chunks": tail_chunks, "trace": 1})
+    R = oracle.ag_gemm(d.A.device_array, d.B.device_array, chunks, order)
+    c, _ = run_ag(plan, chunks, d.A, d.B, "bf16")
+    assert_close(out_to_f64(c, "bf16"), R, tol_for("bf16", "bf16"), "ag static dispatch, shared tail")
+    tr = plan.trace()
+    assert (tr["t_take"] > 0).all() and (tr["t_end"] >= tr["t_start"]).all()
+    info = plan.info
+    dm = oracle.dep_map(chunks, order, W * S, N, info.bm, info.bn)
+    pos = {int(cid): p for p, cid in enumerate(order)}
+    n_chunks = len(chunks)
+    critical = [max(pos[int(cid)] for cid in dm.tile_chunks[dm.tile_ptr[t]:dm.tile_ptr[t + 1]]) >= n_chunks - tail_chunks
+                for t in range(len(dm.tile_ptr) - 1)]
+    per = grid // 8
+
+    def owner(p):
+        sl = p % grid
+        return (sl % per) * 8 + sl // per
+
+    moved = [i for i in range(len(tr)) if int(tr["workgroup"][i]) != owner(i)]
+    assert all(critical[int(tr["raster"][i])] for i in moved), moved[:8]
+    if all(critical):
+        assert not moved
+
+
 # ---------------------------------------------------------------------------------
 # Smaller bf16 tiles (256x128, 128x256, 128x128): the same results, to the same bar
 # ---------------------------------------------------------------------------------
@@ -453,6 +490,10 @@ TAIL_CASES = [
     ("ag", 4, 3, 256, 4, "swizzle1d", 520, 640, {"split_k": 2, "tail_split": 3, "tail_chunks": 5}),
     ("ag", 4, 0, 256, 4, "ring", 512, 512, {"tail_split": 2, "tail_chunks": 4, "num_workgroups": 8}),
     ("rs", 4, 1, 256, 2, "rs_ring", 512, 640, {"tail_split": 2, "tail_chunks": 3}),
+    ("ag", 4, 3, 256, 4, "swizzle1d", 520, 640, {"tail_split": 5, "tail_chunks": 6, "tail_taper": 1}),
+    ("ag", 4, 0, 256, 4, "ring", 512, 512, {"tail_split": 4, "tail_chunks": 8, "tail_taper": 1, "tile_dispatch": 2,
+                                             "num_workgroups": 16}),
+    ("rs", 4, 1, 256, 2, "rs_ring", 512, 640, {"tail_split": 3, "tail_chunks": 4, "tail_taper": 1}),
 ]
 
 
@@ -485,6 +526,44 @@ def test_tail_split_parity(case):
     for mode in ("overlap", "compute_only"):
         c, _ = run_ag(plan, chunks, d.A, d.B, "bf16", mode=mode)
         assert_close(out_to_f64(c, "bf16"), R, 2e-2, "ag tail %s" % mode)
+
+
+@pytest.mark.parametrize("op,S_,C_", [("ag", 6, 5), ("ag", 3, 12), ("rs", 4, 3)])
+def test_tapered_tail_split_unit_count(op, S_, C_):
+    """The tapered tail split gives the tiles of the j-th tail chunk (from the last
+    arrival, or the first emission) ceil(S / (1 + j (S - 1) / (C - 1))) K-slices: the
+    plan's unit count equals that sum over the oracle's dependence map, and the output
+    matches the oracle."""
+    W, r, S, Q, N, K = 4, 1, 256, 4, 520, 640
+    kind = "rs_ring" if op == "rs" else "ring"
+    _say("tapered tail %s S=%d C=%d" % (op, S_, C_))
+    chunks, order = oracle.uniform_schedule(W, r, S, Q, kind)
+    cfg = {"timeout_ms": 1000, "tail_split": S_, "tail_chunks": C_, "tail_taper": 1}
+    plan = csg.Plan(op, W * S, N, K, "bf16", "bf16", csg.Schedule.uniform(W, r, S, Q, kind), cfg=cfg)
+    info = plan.info
+    dm = oracle.dep_map(chunks, order, W * S, N, info.bm, info.bn, producer=(op == "rs"))
+    pos = {int(cid): p for p, cid in enumerate(order)}
+    n_chunks, KT = len(chunks), K // info.bk
+    expect = 0
+    for t in range(len(dm.tile_ptr) - 1):
+        ps = [pos[int(cid)] for cid in dm.tile_chunks[dm.tile_ptr[t]:dm.tile_ptr[t + 1]]]
+        j = (n_chunks - 1 - max(ps)) if op == "ag" else min(ps)
+        sp = 1
+        if j < C_:
+            sp = -(-S_ * (C_ - 1) // (C_ - 1 + j * (S_ - 1)))    # ceil
+        expect += min(sp, KT)
+    assert info.n_units == expect
+    if op == "rs":
+        w = si.Workload(103, "rs", "rs", M=W * S, N=N, K=K, dtype="bf16", out_dtype="bf16", dist="normal", world=W,
+                        rank=r, shard_rows=S, chunks_per_shard=Q, order="rs_ring")
+        d = si.draw(w)
+        c, out = run_rs(plan, d.A, d.B, "bf16")
+        R, _, _ = oracle.gemm_rs(d.A.device_array, d.B.device_array, chunks, order)
+    else:
+        w, d, perm, chunks, order = _small_ag(W, r, S, Q, kind, N, K, "bf16", "bf16")
+        c, _ = run_ag(plan, chunks, d.A, d.B, "bf16")
+        R = oracle.ag_gemm(d.A.device_array, d.B.device_array, chunks, order)
+    assert_close(out_to_f64(c, "bf16"), R, 2e-2, "tapered tail %s" % op)
 
 
 def test_grouped_tail_split_parity():

@@ -178,3 +178,15 @@ def test_search_space_copy_split_dimension():
     assert len(sdma) == 3 * sum(1 for c in sdma if "copy_split" not in c.cfg_dict())
     assert len(sp) - len(sdma) == len(base) - sum(1 for c in base if ("copy_backend", 1) not in c.cfg)
 
+
+def test_search_space_tail_taper_dimension():
+    """The tapered tail split is a dimension only of candidates with a tail split."""
+    tails = ((0, 0), (2, 4), (4, 12))
+    base = tune.search_space("ag", kernel_copies=False, tail=tails)
+    sp = tune.search_space("ag", kernel_copies=False, tail=tails, tail_taper=(0, 1))
+    assert sp[0] == base[0]
+    tapered = [c for c in sp if c.cfg_dict().get("tail_taper")]
+    assert all(c.cfg_dict().get("tail_split", 0) > 1 for c in tapered)
+    assert len(tapered) == sum(1 for c in base if c.cfg_dict().get("tail_split", 0) > 1)
+    assert len(sp) == len(base) + len(tapered)
+
