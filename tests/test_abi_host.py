@@ -293,3 +293,36 @@ def test_binding_checks_tensor_arguments():
         _buf(big, 64 * 64 * 2, "a")
     _buf(None, 1 << 20, "a")
     _buf(12345, 1 << 20, "a")
+
+
+def _header_structs():
+    """Field names and C types of every `typedef struct { ... } name;` in include/csg.h,
+    in declaration order (comma-separated declarators expanded)."""
+    text = open(os.path.join(os.path.dirname(__file__), "..", "include", "csg.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    out = {}
+    for body, name in re.findall(r"typedef struct\s*\{(.*?)\}\s*(\w+)\s*;", text, flags=re.S):
+        fields = []
+        for decl in body.split(";"):
+            decl = decl.strip()
+            if not decl:
+                continue
+            ctype, names = decl.split(None, 1)
+            fields += [(n.strip(), ctype) for n in names.split(",")]
+        out[name] = fields
+    return out
+
+
+def test_binding_structs_match_the_header():
+    """The ctypes structures of the binding list the header's fields in the header's
+    order with the same widths, so a field added to the C ABI cannot shift the others."""
+    import ctypes
+    widths = {"int32_t": ctypes.c_int32, "uint32_t": ctypes.c_uint32, "int64_t": ctypes.c_int64,
+              "uint64_t": ctypes.c_uint64}
+    structs = _header_structs()
+    for name in ("csg_chunk", "csg_plan_cfg", "csg_plan_info", "csg_trace_unit", "csg_diag"):
+        assert name in structs, name
+        py = getattr(csg, name)._fields_
+        assert [f for f, _ in py] == [f for f, _ in structs[name]], name
+        for (f, t), (_, ct) in zip(py, structs[name]):
+            assert ctypes.sizeof(t) == ctypes.sizeof(widths[ct]), (name, f)
