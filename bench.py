@@ -48,7 +48,10 @@ CAL_BYTES = 256 << 20    # bytes read (and written) by the calibration copy
 # isolated calls as the objective (`bench.py --config N --tune --objective isolated`),
 # among the copy-engine candidates (the copy engines stand in for the links of a real
 # collective; the kernel's own copies move chunks inside HBM faster than links would):
-# plan configuration fields. --default-plan measures the library's defaults instead.
+# plan configuration fields. GEMM + reduce-scatter and the grouped GEMM keep 256 x 256
+# tiles where the tuner's best used 128 x 256 tiles within 1-3 % per cold call: those
+# ran the back-to-back loop 4-20 % slower. --default-plan measures the library's
+# defaults instead.
 TUNED_PLAN_CFG = {
     2: {"bm": 128, "bn": 256, "bk": 64, "tile_dispatch": 2, "tail_split": 2, "tail_chunks": 4},
     3: {"intra_order": 1, "group_m": 4, "tile_dispatch": 2},
